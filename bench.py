@@ -1,0 +1,256 @@
+"""Benchmark of the W4A4 DiT-linear hot path on one MI355X.
+
+One step = the whole hot path over the four linears of a PixArt-style DiT
+block (hidden 1152, MLP 4608; 4096 image tokens x CFG batch 2 -> M = 8192;
+Hadamard block 64): for each linear, clq_rotate_quant_act on its fp16 input,
+then clq_w4a4_linear against its offline-quantized weights.  Inputs and
+weights are resident in HBM before timing starts; weights are quantized
+once, outside the timed region (as the method does offline).
+
+Prints ONE JSON line:
+  value      effective TOPS of the step = sum(2 M N K) / step time
+  roofline   the GEMM kernel (dominant): algorithmic int8-MFMA ops per launch
+             / average launch time (HIP events on the launch stream), against
+             the dense int8 peak (5.0 POP/s)
+  rotate_quant  algorithmic bytes per launch / average launch time, against
+             HBM (8 TB/s), measured in the same timed loop, and separately
+             with the 256 MB Infinity Cache flushed before every launch
+  cpu_baseline  the CPU oracle timed on the host cores on a bounded sample
+             of the same workload (token rows of every layer)
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads  # noqa: E402
+
+INT8_PEAK_TOPS = 5000.0      # dense int8 MFMA, MI355X (5.0 POP/s)
+HBM_PEAK_GBPS = 8000.0       # HBM3E, MI355X
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic_pixart_block_m8192.txt")
+
+
+def rq_bytes(l):
+    """Algorithmic HBM bytes of one rotate+quant launch: read M*K fp16, write
+    M*K/2 packed codes and M fp32 scales."""
+    return l.M * (2 * l.K + l.K // 2 + 4)
+
+
+def gemm_ops(l):
+    return 2 * l.M * l.N * l.K
+
+
+def load_traffic(kernel_src_sha):
+    """Per-launch HBM traffic from the committed rocprofv3 PMC summary, only
+    if it was taken on the current kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if line.startswith("traffic:"):
+            for kv in line.split()[1:]:
+                k, v = kv.split("=")
+                vals[k] = v
+    if vals.get("kernel_sha") != kernel_src_sha:
+        return None
+    return float(vals["bytes_per_launch"])
+
+
+def kernel_sha():
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2509_24416_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def cpu_baseline(layers, inputs, budget_s=15.0):
+    """Times the CPU oracle's online path (rotate + quantize the activations,
+    integer GEMM, fp64 epilogue) on a sample of token rows of every layer,
+    sized to roughly budget_s seconds; returns TOPS on that sample."""
+    import oracle
+    threads = oracle.get_threads()
+    wq = {}
+    for l in layers:  # offline step, not timed (as on the GPU)
+        _, W, b = inputs[l.name]
+        wq[l.name] = oracle.quantize_weights(W, l.block)
+
+    def run(rows):
+        ops = 0
+        t0 = time.perf_counter()
+        for l in layers:
+            X, _, b = inputs[l.name]
+            _, xc, xs = oracle.quantize_act(X[:rows], l.block)
+            _, wc, ws = wq[l.name]
+            acc = oracle.gemm_i32(xc, wc)
+            oracle.epilogue(acc, xs, ws, b)
+            ops += 2 * rows * l.N * l.K
+        return time.perf_counter() - t0, ops
+
+    t_cal, _ = run(64)
+    rows = int(min(layers[0].M, max(64, 64 * budget_s / max(t_cal, 1e-3))))
+    rows = max(16, rows // 16 * 16)
+    t, ops = run(rows)
+    return {"value": ops / t / 1e12, "unit": "TOPS", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} token rows of each of the {len(layers)} linears "
+                      f"({ops / 2e9:.1f} G MAC, {t:.1f} s; weights quantized beforehand, untimed)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--cold-reps", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the hot path shards by token rows with no collective; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2509_24416_amd as clq
+
+    dev = torch.device("cuda:0")
+    wl = workloads.C2
+    layers = list(wl.layers)
+    inputs = {l.name: workloads.layer_inputs(l) for l in layers}
+
+    # resident device data; weights quantized once (offline step)
+    state = []
+    for l in layers:
+        X, W, b = inputs[l.name]
+        Xd = torch.from_numpy(X).to(dev)
+        qw = clq.clq_quantize_weights(torch.from_numpy(W).to(dev), l.block)
+        bd = torch.from_numpy(b).to(dev)
+        Xq = torch.empty((l.M, l.K // 2), dtype=torch.uint8, device=dev)
+        xs = torch.empty(l.M, dtype=torch.float32, device=dev)
+        Y = torch.empty((l.M, l.N), dtype=torch.float16, device=dev)
+        state.append((l, Xd, qw, bd, Xq, xs, Y))
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(events=None):
+        for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
+            if events is not None:
+                events[i][0].record(stream)
+            clq.clq_rotate_quant_act(Xd, l.block, out=Xq, scale_out=xs)
+            if events is not None:
+                events[i][1].record(stream)
+            clq.clq_w4a4_linear(Xq, xs, qw, bd, out=Y)
+            if events is not None:
+                events[i][2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` steps, per-launch events on the launch stream
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+
+    rq_ms = np.zeros(len(layers))
+    gemm_ms = np.zeros(len(layers))
+    for s in range(args.steps):
+        for i in range(len(layers)):
+            rq_ms[i] += ev[s][i][0].elapsed_time(ev[s][i][1])
+            gemm_ms[i] += ev[s][i][1].elapsed_time(ev[s][i][2])
+    rq_ms /= args.steps
+    gemm_ms /= args.steps
+
+    total_ops = sum(gemm_ops(l) for l in layers)
+    value = total_ops / (ms_per_step * 1e-3) / 1e12
+    gemm_tops = [gemm_ops(l) / (gemm_ms[i] * 1e-3) / 1e12 for i, l in enumerate(layers)]
+    gemm_avg_ms = float(gemm_ms.mean())
+    gemm_ops_per_launch = total_ops / len(layers)
+    achieved = gemm_ops_per_launch / (gemm_avg_ms * 1e-3) / 1e12
+    rq_gbps = [rq_bytes(l) / (rq_ms[i] * 1e-3) / 1e9 for i, l in enumerate(layers)]
+    rq_avg_bytes = sum(rq_bytes(l) for l in layers) / len(layers)
+    rq_achieved = rq_avg_bytes / (float(rq_ms.mean()) * 1e-3) / 1e9
+
+    # rotate+quant and GEMM with the Infinity Cache flushed before each launch
+    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+    cold_rq = np.zeros(len(layers))
+    cold_gemm = np.zeros(len(layers))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
+        t_rq, t_g = [], []
+        for _ in range(args.cold_reps):
+            flush.zero_()
+            e0.record(stream)
+            clq.clq_rotate_quant_act(Xd, l.block, out=Xq, scale_out=xs)
+            e1.record(stream)
+            e1.synchronize()
+            t_rq.append(e0.elapsed_time(e1))
+            flush.zero_()
+            e0.record(stream)
+            clq.clq_w4a4_linear(Xq, xs, qw, bd, out=Y)
+            e1.record(stream)
+            e1.synchronize()
+            t_g.append(e0.elapsed_time(e1))
+        cold_rq[i] = np.median(t_rq)
+        cold_gemm[i] = np.median(t_g)
+    del flush
+
+    traffic = load_traffic(kernel_sha())
+    out = {
+        "metric": "W4A4 linear effective TOPS + % int8-MFMA peak; rotate+quant HBM GB/s",
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int4",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "M": layers[0].M, "hidden": 1152, "mlp": 4608,
+                   "block": 64, "layers": {l.name.split(".")[1]: [l.K, l.N] for l in layers},
+                   "parallelism": "none (one GPU)"},
+        "pct_int8_peak": round(100 * value / INT8_PEAK_TOPS, 2),
+        "roofline": {"kernel": "w4a4_gemm_kernel", "bound": "mfma", "achieved": round(achieved, 1),
+                     "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / INT8_PEAK_TOPS, 4),
+                     "traffic": traffic, "avg_launch_us": round(gemm_avg_ms * 1e3, 2),
+                     "ops_per_launch": gemm_ops_per_launch},
+        "rotate_quant": {"kernel": "rotate_quant_kernel<64>", "bound": "hbm",
+                         "achieved": round(rq_achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": round(rq_achieved / HBM_PEAK_GBPS, 4),
+                         "avg_launch_us": round(float(rq_ms.mean()) * 1e3, 2),
+                         "bytes_per_launch": rq_avg_bytes,
+                         "cold_cache_GBps": {l.name: round(rq_bytes(l) / (cold_rq[i] * 1e-3) / 1e9, 1)
+                                             for i, l in enumerate(layers)}},
+        "per_layer": {l.name: {"gemm_us": round(gemm_ms[i] * 1e3, 2), "gemm_TOPS": round(gemm_tops[i], 1),
+                               "gemm_cold_us": round(cold_gemm[i] * 1e3, 2),
+                               "rq_us": round(rq_ms[i] * 1e3, 2), "rq_GBps": round(rq_gbps[i], 1),
+                               "rq_cold_us": round(cold_rq[i] * 1e3, 2)}
+                      for i, l in enumerate(layers)},
+        "gpu": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(layers, inputs)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

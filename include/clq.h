@@ -1,0 +1,133 @@
+/*
+ * clq.h -- C ABI of the CLQ W4A4 linear-layer library for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The library implements the inference hot path of a W4A4-quantized
+ * diffusion-transformer linear layer as described in "CLQ: Cross-Layer Guided
+ * Orthogonal-based Quantization for Diffusion Transformers" (arXiv
+ * 2509.24416):
+ *
+ *   1. Sec. 3.3 (Orthogonal-Based Smoothing): the activations of a layer are
+ *      multiplied by G = S.H -- a column swap S (given as a gather vector s)
+ *      followed by a block-diagonal Hadamard matrix H with +-1 entries --
+ *      using a fast Hadamard transform at inference time, while the weights
+ *      absorb the same G offline.
+ *   2. Sec. 3.1, Eq. (1): uniform quantization Round(Clip(.)) with n = 4
+ *      bits.  Activations are quantized dynamically (scale from the live
+ *      row, one per token); weights are quantized once, one scale per output
+ *      channel (Sec. 4.1), with one clip ratio per matrix (Sec. 4.1).
+ *   3. The integer product of the codes, rescaled by activation scale x weight
+ *      scale (the rescale factor of Eq. (1)), giving Y = X W^T + bias.
+ *
+ * Conventions shared by every entry point
+ *   - All data pointers are DEVICE pointers (hipMalloc'd or equivalent) unless
+ *     stated; fp16 means IEEE binary16 stored as 2-byte values.
+ *   - The caller owns and allocates every buffer.  The library allocates no
+ *     device memory, keeps no global state, never synchronises, and never
+ *     writes to its inputs.  Each call validates its arguments on the host,
+ *     then enqueues its kernels on `stream` and returns; results are
+ *     available once the stream reaches that point.
+ *   - On a validation error nothing is enqueued and the error code is
+ *     returned.  CLQ_ERR_HIP reports a failed kernel launch.  On any error the
+ *     outputs are left undefined.
+ *   - Shapes: 1 <= M, N <= 2^31 - 1; 64 <= K <= 32768 with K % 64 == 0 and
+ *     K % block == 0; block in {32, 64, 128}.  Row strides (ldx, ldy, ldacc)
+ *     are in elements, at least the row length and multiples of 8 (ldacc: of
+ *     4).  Matrix pointers (X, W, Xq, Wq, Y, acc) must be 16-byte aligned;
+ *     scale pointers 4-byte aligned; bias and perm naturally aligned.
+ *   - Inputs must be finite; perm must be a permutation of 0..K-1 and the
+ *     activations must have been quantized with the same block and perm as the
+ *     weights.  These are not checked.
+ *
+ * Integer results are exact: codes are in [-7, 7] and |acc| <= 49 K < 2^24.
+ */
+#ifndef CLQ_H
+#define CLQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CLQ_OK = 0,
+    CLQ_ERR_NULL = 1,  /* a required pointer is NULL                        */
+    CLQ_ERR_SHAPE = 2, /* M, N, K, ld* out of range or not multiples         */
+    CLQ_ERR_BLOCK = 3, /* block not in {32, 64, 128} or K % block != 0       */
+    CLQ_ERR_ALIGN = 4, /* a pointer is not aligned as required               */
+    CLQ_ERR_ARG = 5,   /* clip_ratio outside (0, 1]                           */
+    CLQ_ERR_HIP = 6    /* a HIP launch failed (see hipGetLastError)           */
+} clq_status;
+
+/* Library version; bumps whenever the packed weight layout changes. */
+int clq_version(void);
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *clq_status_string(clq_status status);
+
+/* Size in bytes of the packed weight buffer `Wq` for an N x K weight.
+ * Returns 0 if the shape is invalid.  Query it; do not assume N*K/2 (rows are
+ * padded up to a multiple of 64). */
+size_t clq_weight_bytes(int64_t N, int64_t K);
+
+/* Offline weight transform (Sec. 3.3: W absorbs G; Sec. 3.1: weights are
+ * quantized once, per output channel; Sec. 4.1: one clip per matrix).
+ *   W        fp16 [N][K], row-major, contiguous (torch Linear layout).
+ *   perm     int32 [K] gather vector s (x'[k] = x[perm[k]]), or NULL.
+ *   block    Hadamard block size b.
+ *   clip_ratio  alpha in (0, 1]: the clip bound is alpha * max|w~| per row.
+ *   Wq       out, clq_weight_bytes(N, K) bytes, opaque layout (padding rows
+ *            are written as zero codes).
+ *   w_scale  out, fp32 [N]: (alpha * max|w~| / 7) / b -- the 1/b of the
+ *            unnormalised Hadamard transform is folded in (exact).
+ * Each row w~ = FWHT_b(gather(W[n], perm)) is quantized as
+ * q = clamp(rne(w~ * r), -7, 7) with r = fl32(7 / (alpha * max|w~|)). */
+clq_status clq_quantize_weights(const void *W, const int32_t *perm, int64_t N,
+                                int64_t K, int32_t block, float clip_ratio,
+                                void *Wq, float *w_scale, hipStream_t stream);
+
+/* Online activation rotate + quantize (Sec. 3.3 fast Hadamard transform;
+ * Sec. 3.1 dynamic per-token quantization).
+ *   X        fp16 [M][K] with row stride ldx (elements).
+ *   perm     int32 [K] gather vector, or NULL.
+ *   Xq       out, uint8 [M][K/2]: int4 codes, two's complement, byte j holds
+ *            code 2j in its low nibble and code 2j+1 in its high nibble.
+ *   x_scale  out, fp32 [M]: max|x~| / 7 for the row (0 for an all-zero row).
+ * x~ = FWHT_b(gather(X[m], perm)) in fp32 with the stage order h = 1, 2, 4,
+ * ..., b/2; q = rne(x~ * fl32(7 / max|x~|)), the product taken exactly. */
+clq_status clq_rotate_quant_act(const void *X, int64_t ldx, const int32_t *perm,
+                                int64_t M, int64_t K, int32_t block, void *Xq,
+                                float *x_scale, hipStream_t stream);
+
+/* W4A4 linear: Y = dequant(Xq . Wq^T) + bias, written as fp16.
+ *   Xq, x_scale   from clq_rotate_quant_act (M rows).
+ *   Wq, w_scale   from clq_quantize_weights (N rows).
+ *   bias          fp16 [N] or NULL.
+ *   Y             out, fp16 [M][N] with row stride ldy (elements).
+ * y[m][n] = fp16_rne(fma(fl32(acc * x_scale[m]), w_scale[n], bias[n])) with
+ * acc = sum_k qx[m][k] * qw[n][k] computed exactly in int32. */
+clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
+                           const float *w_scale, const void *bias, int64_t M,
+                           int64_t N, int64_t K, void *Y, int64_t ldy,
+                           hipStream_t stream);
+
+/* Diagnostic: the exact integer accumulators acc[m][n] = sum_k qx*qw as
+ * int32 [M][N] with row stride ldacc (elements).  Same kernels as
+ * clq_w4a4_linear with the epilogue replaced by an int32 store. */
+clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M,
+                              int64_t N, int64_t K, int32_t *acc, int64_t ldacc,
+                              hipStream_t stream);
+
+/* Diagnostic: converts the opaque Wq layout back to canonical packed codes,
+ * uint8 [N][K/2] (same nibble convention as Xq). */
+clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K,
+                                 void *Wq_canonical, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CLQ_H */

@@ -1,0 +1,199 @@
+"""Python binding of libclq.so: the W4A4 DiT linear hot path on MI355X.
+
+Argument marshalling only.  Every step of the path runs in the library's HIP
+kernels; torch supplies device memory and the current stream.  The functions
+carry the names of the C entry points declared in ``include/clq.h``:
+
+    clq_quantize_weights(W, block, perm=None, clip_ratio=1.0) -> QWeight
+    clq_rotate_quant_act(X, block, perm=None)                 -> (Xq, x_scale)
+    clq_w4a4_linear(Xq, x_scale, qw, bias=None)               -> Y
+    clq_w4a4_accum_i32(Xq, qw)                                 -> acc
+    clq_unswizzle_weights(qw)                                  -> canonical codes
+
+Paper: "CLQ" (arXiv 2509.24416) -- Sec. 3.3 (online block-Hadamard rotation,
+weights absorb it offline) and Sec. 3.1 Eq. (1) (4-bit quantizer; dynamic
+per-token activations, per-channel weights).
+
+Importing this package fails loudly if ``libclq.so`` has not been built;
+there is no fallback path.
+"""
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch  # loads the HIP runtime that libclq.so then shares
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libclq.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'` "
+        "(or python paper_2509_24416_amd/build.py)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+_i64, _i32, _f32, _p = ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_void_p
+_lib.clq_version.restype = ctypes.c_int
+_lib.clq_status_string.restype = ctypes.c_char_p
+_lib.clq_status_string.argtypes = [ctypes.c_int]
+_lib.clq_weight_bytes.restype = ctypes.c_size_t
+_lib.clq_weight_bytes.argtypes = [_i64, _i64]
+_lib.clq_quantize_weights.argtypes = [_p, _p, _i64, _i64, _i32, _f32, _p, _p, _p]
+_lib.clq_rotate_quant_act.argtypes = [_p, _i64, _p, _i64, _i64, _i32, _p, _p, _p]
+_lib.clq_w4a4_linear.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p]
+_lib.clq_w4a4_accum_i32.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _p]
+_lib.clq_unswizzle_weights.argtypes = [_p, _i64, _i64, _p, _p]
+for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
+           "clq_w4a4_accum_i32", "clq_unswizzle_weights"):
+    getattr(_lib, _f).restype = ctypes.c_int
+
+EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_quantize_weights",
+           "clq_rotate_quant_act", "clq_w4a4_linear", "clq_w4a4_accum_i32",
+           "clq_unswizzle_weights")
+
+CLQ_OK, CLQ_ERR_NULL, CLQ_ERR_SHAPE, CLQ_ERR_BLOCK, CLQ_ERR_ALIGN, CLQ_ERR_ARG, CLQ_ERR_HIP = range(7)
+
+
+class ClqError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {_lib.clq_status_string(status).decode()}")
+
+
+def lib():
+    """The raw ctypes handle (for tests that drive the C ABI directly)."""
+    return _lib
+
+
+def _check(status, where):
+    if status != CLQ_OK:
+        raise ClqError(status, where)
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t, name, dtype):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _perm(perm, K):
+    if perm is None:
+        return None
+    _dev(perm, "perm", torch.int32)
+    if perm.shape != (K,) or not perm.is_contiguous():
+        raise ValueError(f"perm must be a contiguous int32 [K={K}] tensor")
+    return perm
+
+
+def clq_version():
+    return int(_lib.clq_version())
+
+
+def clq_weight_bytes(N, K):
+    return int(_lib.clq_weight_bytes(N, K))
+
+
+@dataclass
+class QWeight:
+    """A weight matrix quantized by clq_quantize_weights."""
+    wq: torch.Tensor        # uint8 [clq_weight_bytes(N, K)], opaque layout
+    w_scale: torch.Tensor   # fp32 [N], includes the 1/block factor
+    N: int
+    K: int
+    block: int
+    perm: torch.Tensor = None
+    clip_ratio: float = 1.0
+
+
+def clq_quantize_weights(W, block, perm=None, clip_ratio=1.0, stream=None):
+    """Offline: rotate each weight row by G = S.H and quantize it to int4 with
+    one scale per output channel."""
+    _dev(W, "W", torch.float16)
+    if W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be a contiguous 2-D [N, K] tensor")
+    N, K = W.shape
+    perm = _perm(perm, K)
+    nbytes = clq_weight_bytes(N, K)
+    if nbytes == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_quantize_weights")
+    wq = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
+    ws = torch.empty(N, dtype=torch.float32, device=W.device)
+    _check(_lib.clq_quantize_weights(_ptr(W), _ptr(perm), N, K, block, clip_ratio,
+                                     _ptr(wq), _ptr(ws), _stream(stream)), "clq_quantize_weights")
+    return QWeight(wq, ws, N, K, block, perm, clip_ratio)
+
+
+def clq_rotate_quant_act(X, block, perm=None, out=None, scale_out=None, stream=None):
+    """Online: x~ = FWHT(gather(x, perm)) per token, quantized to int4 codes
+    (packed two per byte) with one fp32 scale per token.  X may have a row
+    stride larger than K (a column slice of a wider tensor)."""
+    _dev(X, "X", torch.float16)
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D [M, K] with unit column stride")
+    M, K = X.shape
+    perm = _perm(perm, K)
+    Xq = out if out is not None else torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    xs = scale_out if scale_out is not None else torch.empty(M, dtype=torch.float32, device=X.device)
+    _dev(Xq, "Xq", torch.uint8)
+    _dev(xs, "x_scale", torch.float32)
+    _check(_lib.clq_rotate_quant_act(_ptr(X), X.stride(0), _ptr(perm), M, K, block, _ptr(Xq),
+                                     _ptr(xs), _stream(stream)), "clq_rotate_quant_act")
+    return Xq, xs
+
+
+def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None):
+    """Y = dequant(Xq . Wq^T) + bias as fp16 [M, N]."""
+    _dev(Xq, "Xq", torch.uint8)
+    _dev(x_scale, "x_scale", torch.float32)
+    if bias is not None:
+        _dev(bias, "bias", torch.float16)
+        if bias.shape != (qw.N,) or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous fp16 [N] tensor")
+    M = Xq.shape[0]
+    if Xq.shape[1] * 2 != qw.K or not Xq.is_contiguous():
+        raise ValueError("Xq must be a contiguous [M, K/2] uint8 tensor matching the weight's K")
+    if out is None:  # rows padded to a multiple of 8 elements (16-byte aligned rows)
+        out = torch.empty((M, (qw.N + 7) // 8 * 8), dtype=torch.float16, device=Xq.device)[:, :qw.N]
+    Y = out
+    _dev(Y, "Y", torch.float16)
+    if Y.dim() != 2 or Y.stride(1) != 1 or Y.shape != (M, qw.N):
+        raise ValueError("Y must be 2-D [M, N] with unit column stride")
+    _check(_lib.clq_w4a4_linear(_ptr(Xq), _ptr(x_scale), _ptr(qw.wq), _ptr(qw.w_scale), _ptr(bias),
+                                M, qw.N, qw.K, _ptr(Y), Y.stride(0), _stream(stream)),
+           "clq_w4a4_linear")
+    return Y
+
+
+def clq_w4a4_accum_i32(Xq, qw, out=None, stream=None):
+    """The exact int32 accumulators sum_k qx * qw, [M, N] (diagnostic)."""
+    _dev(Xq, "Xq", torch.uint8)
+    M = Xq.shape[0]
+    if Xq.shape[1] * 2 != qw.K or not Xq.is_contiguous():
+        raise ValueError("Xq must be a contiguous [M, K/2] uint8 tensor matching the weight's K")
+    if out is None:  # rows padded to a multiple of 4 elements (16-byte aligned rows)
+        out = torch.empty((M, (qw.N + 3) // 4 * 4), dtype=torch.int32, device=Xq.device)[:, :qw.N]
+    acc = out
+    _dev(acc, "acc", torch.int32)
+    _check(_lib.clq_w4a4_accum_i32(_ptr(Xq), _ptr(qw.wq), M, qw.N, qw.K, _ptr(acc), acc.stride(0),
+                                   _stream(stream)), "clq_w4a4_accum_i32")
+    return acc
+
+
+def clq_unswizzle_weights(qw, stream=None):
+    """Canonical packed codes uint8 [N, K/2] of a QWeight (diagnostic)."""
+    out = torch.empty((qw.N, qw.K // 2), dtype=torch.uint8, device=qw.wq.device)
+    _check(_lib.clq_unswizzle_weights(_ptr(qw.wq), qw.N, qw.K, _ptr(out), _stream(stream)),
+           "clq_unswizzle_weights")
+    return out

@@ -1,0 +1,134 @@
+// C ABI of the CLQ W4A4 linear library: host-side validation and launches.
+// Every entry point checks its arguments before enqueuing anything and
+// returns a status code; kernels run on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/clq.h"
+#include "clq_internal.h"
+
+namespace {
+
+constexpr int kVersion = 1;
+constexpr int64_t kMaxK = 32768;
+constexpr int64_t kMaxRows = 2147483647;
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+clq_status check_block(int64_t K, int32_t block) {
+    if (block != 32 && block != 64 && block != 128) return CLQ_ERR_BLOCK;
+    if (K % block != 0) return CLQ_ERR_BLOCK;
+    return CLQ_OK;
+}
+
+clq_status check_k(int64_t K) {
+    if (K < 64 || K > kMaxK || K % 64 != 0) return CLQ_ERR_SHAPE;
+    return CLQ_OK;
+}
+
+clq_status check_rows(int64_t R) {
+    if (R < 1 || R > kMaxRows) return CLQ_ERR_SHAPE;
+    return CLQ_OK;
+}
+
+clq_status from_hip(hipError_t e) { return e == hipSuccess ? CLQ_OK : CLQ_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int clq_version(void) { return kVersion; }
+
+const char *clq_status_string(clq_status s) {
+    switch (s) {
+        case CLQ_OK: return "CLQ_OK";
+        case CLQ_ERR_NULL: return "CLQ_ERR_NULL: a required pointer is NULL";
+        case CLQ_ERR_SHAPE: return "CLQ_ERR_SHAPE: a size or row stride is out of range";
+        case CLQ_ERR_BLOCK: return "CLQ_ERR_BLOCK: block must be 32, 64 or 128 and divide K";
+        case CLQ_ERR_ALIGN: return "CLQ_ERR_ALIGN: a pointer is misaligned";
+        case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio must lie in [2^-24, 1]";
+        case CLQ_ERR_HIP: return "CLQ_ERR_HIP: a HIP launch failed";
+    }
+    return "CLQ: unknown status";
+}
+
+size_t clq_weight_bytes(int64_t N, int64_t K) {
+    if (check_rows(N) != CLQ_OK || check_k(K) != CLQ_OK) return 0;
+    return (size_t)clq::padded_rows(N) * (size_t)(K / 2);
+}
+
+clq_status clq_quantize_weights(const void *W, const int32_t *perm, int64_t N, int64_t K,
+                                int32_t block, float clip_ratio, void *Wq, float *w_scale,
+                                hipStream_t stream) {
+    if (!W || !Wq || !w_scale) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (!(clip_ratio >= 0x1p-24f && clip_ratio <= 1.0f)) return CLQ_ERR_ARG;
+    if (!aligned(W, 16) || !aligned(Wq, 16) || !aligned(w_scale, 4) || (perm && !aligned(perm, 4)))
+        return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_rotate_quant(
+        static_cast<const uint16_t *>(W), K, perm, N, clq::padded_rows(N), (int)K, block,
+        clip_ratio, true, 1.0f / (float)block, static_cast<uint8_t *>(Wq), w_scale, stream));
+}
+
+clq_status clq_rotate_quant_act(const void *X, int64_t ldx, const int32_t *perm, int64_t M,
+                                int64_t K, int32_t block, void *Xq, float *x_scale,
+                                hipStream_t stream) {
+    if (!X || !Xq || !x_scale) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (ldx < K || ldx % 8 != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(X, 16) || !aligned(Xq, 16) || !aligned(x_scale, 4) || (perm && !aligned(perm, 4)))
+        return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_rotate_quant(static_cast<const uint16_t *>(X), ldx, perm, M, M,
+                                             (int)K, block, 1.0f, false, 1.0f,
+                                             static_cast<uint8_t *>(Xq), x_scale, stream));
+}
+
+static clq_status check_gemm(const void *Xq, const void *Wq, int64_t M, int64_t N, int64_t K,
+                             const void *Y, int64_t ldy, int64_t ld_mult) {
+    if (!Xq || !Wq || !Y) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK)
+        return s;
+    if (ldy < N || ldy % ld_mult != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(Xq, 16) || !aligned(Wq, 16) || !aligned(Y, 16)) return CLQ_ERR_ALIGN;
+    return CLQ_OK;
+}
+
+clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
+                           const float *w_scale, const void *bias, int64_t M, int64_t N,
+                           int64_t K, void *Y, int64_t ldy, hipStream_t stream) {
+    if (!x_scale || !w_scale) return CLQ_ERR_NULL;
+    clq_status s = check_gemm(Xq, Wq, M, N, K, Y, ldy, 8);
+    if (s != CLQ_OK) return s;
+    if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2)))
+        return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_gemm(static_cast<const uint8_t *>(Xq), x_scale,
+                                     static_cast<const uint8_t *>(Wq), w_scale,
+                                     static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy,
+                                     false, stream));
+}
+
+clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M, int64_t N, int64_t K,
+                              int32_t *acc, int64_t ldacc, hipStream_t stream) {
+    clq_status s = check_gemm(Xq, Wq, M, N, K, acc, ldacc, 4);
+    if (s != CLQ_OK) return s;
+    return from_hip(clq::launch_gemm(static_cast<const uint8_t *>(Xq), nullptr,
+                                     static_cast<const uint8_t *>(Wq), nullptr, nullptr, M, N,
+                                     (int)K, acc, ldacc, true, stream));
+}
+
+clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K, void *Wq_canonical,
+                                 hipStream_t stream) {
+    if (!Wq || !Wq_canonical) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (!aligned(Wq, 16) || !aligned(Wq_canonical, 8)) return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_unswizzle(static_cast<const uint8_t *>(Wq), N, (int)K,
+                                          static_cast<uint8_t *>(Wq_canonical), stream));
+}
+
+}  // extern "C"

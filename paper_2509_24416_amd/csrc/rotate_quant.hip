@@ -1,0 +1,275 @@
+// Fused online rotation + per-row int4 quantization (gfx950).
+//
+// Paper (CLQ, arXiv 2509.24416): Sec. 3.3 applies G = S.H to the activations
+// at inference time with a fast Hadamard transform (S a column swap given as a
+// gather vector, H block-diagonal with +-1 entries) and absorbs the same G
+// into the weights offline; Sec. 3.1 Eq. (1) quantizes with Round(Clip(.)),
+// n = 4, dynamically per token for activations and once per output channel
+// for weights.
+//
+// One workgroup handles R whole rows.  The rows are first copied into LDS
+// with coalesced 16-byte loads (each 16-byte chunk of a Hadamard block lands
+// in an XOR-swizzled slot so that the later per-lane block reads hit distinct
+// banks).  Each lane then owns one Hadamard block of b elements in registers
+// and runs every butterfly stage there in fp32, stage order h = 1, 2, ...,
+// b/2 (the first stage is fused with the fp16 -> fp32 widening).  Block
+// abs-maxima meet in an LDS max per row; every lane derives the row's scale
+// and reciprocal with correctly rounded divisions, then quantizes with one
+// fma per element:
+//     fma(x, r, 1.5 * 2^23 + 8)
+// rounds the exact product x * r to the nearest integer, ties to even (the
+// sum lands in the binade where the float spacing is 1), and leaves q + 8 in
+// the low nibble of the result's bit pattern with bits 4..21 clear, which
+// makes packing a few shifts and one byte permute.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "clq_internal.h"
+
+namespace clq {
+namespace {
+
+constexpr float kMagic = 12582920.0f;  // 1.5 * 2^23 + 8
+
+// Slot of 16-byte chunk i of Hadamard block j inside its block's span in
+// LDS.  Eight consecutive lanes own eight consecutive blocks and read chunk i
+// at the same time; the XOR spreads those reads over distinct banks.
+template <int B>
+__device__ __forceinline__ int chunk_slot(int i, int j) {
+    if constexpr (B == 32) return i ^ ((j >> 1) & 3);
+    else return i ^ (j & 7);
+}
+
+__device__ __forceinline__ float half_lo(uint32_t w) {
+    return __half2float(__ushort_as_half((unsigned short)(w & 0xffffu)));
+}
+__device__ __forceinline__ float half_hi(uint32_t w) {
+    return __half2float(__ushort_as_half((unsigned short)(w >> 16)));
+}
+
+// Packs eight quantized words (code + 8 in bits 0..3, bits 4..21 clear) into
+// one dword of two's-complement nibbles, element e at bits 4e..4e+3.
+__device__ __forceinline__ uint32_t pack8(const uint32_t *w) {
+    const uint32_t p01 = (w[1] << 4) | w[0];
+    const uint32_t p23 = (w[3] << 4) | w[2];
+    const uint32_t p45 = (w[5] << 4) | w[4];
+    const uint32_t p67 = (w[7] << 4) | w[6];
+    const uint32_t q03 = (p23 << 8) | p01;  // bits 0..15 clean
+    const uint32_t q47 = (p67 << 8) | p45;
+    return __builtin_amdgcn_perm(q47, q03, 0x05040100u) ^ 0x88888888u;
+}
+
+// Lanes per workgroup never exceed 512 for b >= 64 (at most 512 blocks per
+// row, and rows are only batched up to 512 lanes), which lets the compiler
+// keep a 128-element block in registers.
+template <int B>
+constexpr int rq_max_threads() { return B == 32 ? 1024 : 512; }
+
+template <int B, bool WEIGHT>
+__global__ void __launch_bounds__(rq_max_threads<B>())
+rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
+                    const int32_t *__restrict__ perm, int64_t rows_valid,
+                    int64_t rows_alloc, int K, int R, float alpha, float post_scale,
+                    uint8_t *__restrict__ out, float *__restrict__ scale_out)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int CPB = B / 8;            // 16-byte chunks per block
+    const int cpr = K >> 3;               // chunks per row
+    const int nb = K / B;                 // blocks per row
+    uint4 *tile = reinterpret_cast<uint4 *>(smem);
+    unsigned *rowmax = reinterpret_cast<unsigned *>(smem + (size_t)R * K * 2);
+
+    const int t = threadIdx.x;
+    const int T = blockDim.x;
+    const int64_t row0 = (int64_t)blockIdx.x * R;
+    const int rows = (int)min((int64_t)R, rows_alloc - row0);
+
+    if (t < R) rowmax[t] = 0u;
+
+    // 1. coalesced copy of the rows into LDS (rows past rows_valid are zeros)
+    {
+        int r = t / cpr, cc = t - r * cpr;
+        const int dr = T / cpr, dc = T - dr * cpr;
+        while (r < rows) {
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            const int64_t grow = row0 + r;
+            if (grow < rows_valid)
+                v = *reinterpret_cast<const uint4 *>(X + grow * ldx + (int64_t)cc * 8);
+            const int j = cc / CPB, i = cc % CPB;
+            tile[r * cpr + j * CPB + chunk_slot<B>(i, j)] = v;
+            cc += dc;
+            r += dr;
+            if (cc >= cpr) { cc -= cpr; ++r; }
+        }
+    }
+    __syncthreads();
+
+    // 2. one Hadamard block per lane
+    const int r = t / nb, j = t - r * nb;
+    const bool active = r < rows;
+    float x[B];
+    float bmax = 0.0f;
+    if (active) {
+        if (perm == nullptr) {
+            const uint4 *src = tile + r * cpr + j * CPB;
+#pragma unroll
+            for (int i = 0; i < CPB; ++i) {
+                const uint4 v = src[chunk_slot<B>(i, j)];
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float u = half_lo(w[e]), s = half_hi(w[e]);
+                    x[8 * i + 2 * e] = u + s;       // stage h = 1
+                    x[8 * i + 2 * e + 1] = u - s;
+                }
+            }
+        } else {
+            const uint16_t *rowh = reinterpret_cast<const uint16_t *>(tile + r * cpr);
+            const int32_t *p = perm + j * B;
+#pragma unroll
+            for (int e = 0; e < B; e += 2) {
+                const int k0 = p[e], k1 = p[e + 1];
+                const int c0 = k0 >> 3, c1 = k1 >> 3;
+                const int s0 = (c0 / CPB) * CPB + chunk_slot<B>(c0 % CPB, c0 / CPB);
+                const int s1 = (c1 / CPB) * CPB + chunk_slot<B>(c1 % CPB, c1 / CPB);
+                const float u = __half2float(__ushort_as_half(rowh[s0 * 8 + (k0 & 7)]));
+                const float s = __half2float(__ushort_as_half(rowh[s1 * 8 + (k1 & 7)]));
+                x[e] = u + s;
+                x[e + 1] = u - s;
+            }
+        }
+#pragma unroll
+        for (int h = 2; h < B; h <<= 1) {
+#pragma unroll
+            for (int i = 0; i < B; ++i) {
+                if ((i & h) == 0) {
+                    const float u = x[i], v = x[i + h];
+                    x[i] = u + v;
+                    x[i + h] = u - v;
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < B; ++i) bmax = fmaxf(bmax, fabsf(x[i]));
+        atomicMax(&rowmax[r], __float_as_uint(bmax));
+    }
+    __syncthreads();
+    if (!active) return;
+
+    // 3. per-row scale and codes
+    const float a = __uint_as_float(rowmax[r]);
+    const float ac = WEIGHT ? alpha * a : a;
+    const float rc = (ac == 0.0f) ? 0.0f : 7.0f / ac;
+    const int64_t grow = row0 + r;
+    if (j == 0 && grow < rows_valid) scale_out[grow] = (ac / 7.0f) * post_scale;
+
+    uint32_t words[B / 8];
+#pragma unroll
+    for (int g = 0; g < B / 8; ++g) {
+        uint32_t w[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float v = __builtin_fmaf(x[8 * g + e], rc, kMagic);
+            if constexpr (WEIGHT) v = __builtin_amdgcn_fmed3f(v, kMagic - 7.0f, kMagic + 7.0f);
+            w[e] = __float_as_uint(v);
+        }
+        words[g] = pack8(w);
+    }
+
+    if constexpr (!WEIGHT) {
+        uint4 *dst = reinterpret_cast<uint4 *>(out + grow * (K >> 1) + (int64_t)j * (B / 2));
+#pragma unroll
+        for (int c = 0; c < B / 32; ++c)
+            dst[c] = make_uint4(words[4 * c], words[4 * c + 1], words[4 * c + 2], words[4 * c + 3]);
+    } else {
+        // packed weight layout: one 8-byte piece per k-group of 16 codes
+#pragma unroll
+        for (int g = 0; g < B / 16; ++g) {
+            const int64_t kg = (int64_t)j * (B / 16) + g;
+            uint2 *dst = reinterpret_cast<uint2 *>(out + wq_piece_offset(grow, kg, K));
+            *dst = make_uint2(words[2 * g], words[2 * g + 1]);
+        }
+    }
+}
+
+// Rows per workgroup: the largest lane utilisation R*nb / roundup(R*nb, 64)
+// with at most 512 lanes (unless one row alone needs more) and at most 64 KB
+// of staged fp16 rows.
+int pick_rows(int K, int block) {
+    const int nb = K / block;
+    int best = 1;
+    double best_u = -1.0;
+    for (int R = 1; R * nb <= 1024; ++R) {
+        if (R > 1 && (R * nb > 512 || (size_t)R * K * 2 > 65536)) break;
+        const int T = (R * nb + 63) / 64 * 64;
+        const double u = (double)(R * nb) / T;
+        if (u > best_u + 1e-9) { best_u = u; best = R; }
+    }
+    return best;
+}
+
+template <int B, bool WEIGHT>
+hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
+                     int64_t rows_valid, int64_t rows_alloc, int K, float alpha,
+                     float post_scale, uint8_t *out, float *scale, hipStream_t stream) {
+    const int R = pick_rows(K, B);
+    const int nb = K / B;
+    const int T = (R * nb + 63) / 64 * 64;
+    if (T > rq_max_threads<B>()) return hipErrorInvalidConfiguration;
+    const size_t lds = (size_t)R * K * 2 + (size_t)R * 4;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void *)rotate_quant_kernel<B, WEIGHT>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 65536 + 4096);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const int64_t grid = (rows_alloc + R - 1) / R;
+    hipLaunchKernelGGL((rotate_quant_kernel<B, WEIGHT>), dim3((unsigned)grid), dim3(T), lds,
+                       stream, X, ldx, perm, rows_valid, rows_alloc, K, R, alpha, post_scale,
+                       out, scale);
+    return hipGetLastError();
+}
+
+__global__ void unswizzle_kernel(const uint8_t *__restrict__ Wq, int64_t N, int K,
+                                 uint8_t *__restrict__ out) {
+    const int64_t kgs = K / 16;
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= N * kgs) return;
+    const int64_t n = idx / kgs, kg = idx - n * kgs;
+    const uint2 v = *reinterpret_cast<const uint2 *>(Wq + wq_piece_offset(n, kg, K));
+    *reinterpret_cast<uint2 *>(out + n * (K / 2) + kg * 8) = v;
+}
+
+}  // namespace
+
+hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
+                               int64_t rows, int64_t rows_alloc, int K, int block,
+                               float alpha, bool weight_mode, float post_scale,
+                               uint8_t *out, float *scale, hipStream_t stream) {
+    if (weight_mode) {
+        switch (block) {
+            case 32: return launch_rq<32, true>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
+            case 64: return launch_rq<64, true>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
+            case 128: return launch_rq<128, true>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
+        }
+    } else {
+        switch (block) {
+            case 32: return launch_rq<32, false>(X, ldx, perm, rows, rows, K, 1.0f, 1.0f, out, scale, stream);
+            case 64: return launch_rq<64, false>(X, ldx, perm, rows, rows, K, 1.0f, 1.0f, out, scale, stream);
+            case 128: return launch_rq<128, false>(X, ldx, perm, rows, rows, K, 1.0f, 1.0f, out, scale, stream);
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_unswizzle(const uint8_t *Wq, int64_t N, int K, uint8_t *out,
+                            hipStream_t stream) {
+    const int64_t total = N * (K / 16);
+    const int64_t grid = (total + 255) / 256;
+    hipLaunchKernelGGL(unswizzle_kernel, dim3((unsigned)grid), dim3(256), 0, stream, Wq, N, K, out);
+    return hipGetLastError();
+}
+
+}  // namespace clq

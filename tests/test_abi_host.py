@@ -1,0 +1,152 @@
+"""Host-side checks of the C ABI (no GPU needed, no kernel is ever launched).
+
+The library must load, export every entry point that include/clq.h declares,
+and reject every precondition violation with its documented status code
+before touching the GPU.  The fake device pointers used here are never
+dereferenced: each call fails validation first.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "clq.h")
+LIB = os.path.join(ROOT, "paper_2509_24416_amd", "libclq.so")
+
+OK, NULL, SHAPE, BLOCK, ALIGN, ARG, HIP = range(7)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(clq_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        import __graft_entry__
+        __graft_entry__.build()
+    L = ctypes.CDLL(LIB)
+    i64, i32, f32, p = ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_void_p
+    L.clq_status_string.restype = ctypes.c_char_p
+    L.clq_status_string.argtypes = [ctypes.c_int]
+    L.clq_weight_bytes.restype = ctypes.c_size_t
+    L.clq_weight_bytes.argtypes = [i64, i64]
+    L.clq_quantize_weights.argtypes = [p, p, i64, i64, i32, f32, p, p, p]
+    L.clq_rotate_quant_act.argtypes = [p, i64, p, i64, i64, i32, p, p, p]
+    L.clq_w4a4_linear.argtypes = [p, p, p, p, p, i64, i64, i64, p, i64, p]
+    L.clq_w4a4_accum_i32.argtypes = [p, p, i64, i64, i64, p, i64, p]
+    L.clq_unswizzle_weights.argtypes = [p, i64, i64, p, p]
+    return L
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) == 8, names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_binding_names_match_header():
+    src = open(os.path.join(ROOT, "paper_2509_24416_amd", "__init__.py")).read()
+    for n in declared_functions():
+        assert re.search(rf"\bdef {n}\(", src) or f'"{n}"' in src, n
+
+
+def test_version_and_strings(lib):
+    assert lib.clq_version() == 1
+    for code in range(7):
+        s = lib.clq_status_string(code).decode()
+        assert s.startswith("CLQ")
+    assert b"unknown" in lib.clq_status_string(99)
+
+
+def test_weight_bytes(lib):
+    assert lib.clq_weight_bytes(1152, 1152) == 1152 * 576
+    assert lib.clq_weight_bytes(1, 64) == 64 * 32            # rows padded to 64
+    assert lib.clq_weight_bytes(3456, 1152) == 3456 * 576
+    assert lib.clq_weight_bytes(100, 128) == 128 * 64
+    assert lib.clq_weight_bytes(0, 64) == 0
+    assert lib.clq_weight_bytes(8, 96) == 0                  # K % 64 != 0
+    assert lib.clq_weight_bytes(8, 65536) == 0               # K too large
+
+
+A = 0x10000          # aligned fake device address (never dereferenced)
+MIS = 0x10002        # misaligned
+
+
+def rq(lib, X=A, ldx=1152, perm=None, M=4, K=1152, block=64, Xq=A, xs=A):
+    return lib.clq_rotate_quant_act(X, ldx, perm, M, K, block, Xq, xs, None)
+
+
+def test_rotate_quant_validation(lib):
+    assert rq(lib, X=None) == NULL
+    assert rq(lib, Xq=None) == NULL
+    assert rq(lib, xs=None) == NULL
+    assert rq(lib, M=0) == SHAPE
+    assert rq(lib, K=32) == SHAPE
+    assert rq(lib, K=96, ldx=96) == SHAPE
+    assert rq(lib, K=65536, ldx=65536) == SHAPE
+    assert rq(lib, ldx=1000) == SHAPE
+    assert rq(lib, ldx=1156) == SHAPE                    # not a multiple of 8
+    assert rq(lib, block=16) == BLOCK
+    assert rq(lib, block=256) == BLOCK
+    assert rq(lib, K=192, ldx=192, block=128) == BLOCK   # K % block != 0
+    assert rq(lib, X=MIS) == ALIGN
+    assert rq(lib, Xq=A + 8) == ALIGN
+    assert rq(lib, xs=A + 2) == ALIGN
+    assert rq(lib, perm=A + 2) == ALIGN
+
+
+def qw(lib, W=A, perm=None, N=8, K=1152, block=64, clip=1.0, Wq=A, ws=A):
+    return lib.clq_quantize_weights(W, perm, N, K, block, clip, Wq, ws, None)
+
+
+def test_quantize_weights_validation(lib):
+    assert qw(lib, W=None) == NULL
+    assert qw(lib, Wq=None) == NULL
+    assert qw(lib, ws=None) == NULL
+    assert qw(lib, N=0) == SHAPE
+    assert qw(lib, K=1000) == SHAPE
+    assert qw(lib, block=48) == BLOCK
+    assert qw(lib, clip=0.0) == ARG
+    assert qw(lib, clip=1.5) == ARG
+    assert qw(lib, clip=-0.5) == ARG
+    assert qw(lib, clip=float("nan")) == ARG
+    assert qw(lib, W=MIS) == ALIGN
+    assert qw(lib, Wq=A + 4) == ALIGN
+
+
+def lin(lib, Xq=A, xs=A, Wq=A, ws=A, bias=None, M=4, N=8, K=1152, Y=A, ldy=8):
+    return lib.clq_w4a4_linear(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, None)
+
+
+def test_linear_validation(lib):
+    assert lin(lib, Xq=None) == NULL
+    assert lin(lib, xs=None) == NULL
+    assert lin(lib, Wq=None) == NULL
+    assert lin(lib, ws=None) == NULL
+    assert lin(lib, Y=None) == NULL
+    assert lin(lib, M=0) == SHAPE
+    assert lin(lib, N=0) == SHAPE
+    assert lin(lib, K=100) == SHAPE
+    assert lin(lib, ldy=4) == SHAPE
+    assert lin(lib, N=12, ldy=12) == SHAPE               # ldy % 8 != 0
+    assert lin(lib, Y=A + 8) == ALIGN
+    assert lin(lib, Xq=MIS) == ALIGN
+    assert lin(lib, bias=A + 1) == ALIGN
+
+
+def test_accum_and_unswizzle_validation(lib):
+    f = lib.clq_w4a4_accum_i32
+    assert f(None, A, 4, 8, 1152, A, 8, None) == NULL
+    assert f(A, A, 4, 8, 1152, A, 6, None) == SHAPE      # ldacc % 4 != 0
+    assert f(A, A, 4, 8, 1152, A, 4, None) == SHAPE      # ldacc < N
+    assert f(A, A, 4, 8, 1152, A + 4, 8, None) == ALIGN
+    g = lib.clq_unswizzle_weights
+    assert g(None, 8, 1152, A, None) == NULL
+    assert g(A, 0, 1152, A, None) == SHAPE
+    assert g(A, 8, 1152, A + 4, None) == ALIGN
