@@ -112,6 +112,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--cold-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 5 times (reference for the HBM "
+                         "byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported "
@@ -120,9 +123,19 @@ def main():
         sys.exit(2)
 
     import torch
-    import paper_2509_24416_amd as clq
 
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        src = torch.ones(1 << 29, dtype=torch.float16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_each_way": src.numel() * 2, "launches": 5}))
+        return
+
+    import paper_2509_24416_amd as clq
+
     wl = workloads.C2
     layers = list(wl.layers)
     inputs = {l.name: workloads.layer_inputs(l) for l in layers}
@@ -134,7 +147,7 @@ def main():
         Xd = torch.from_numpy(X).to(dev)
         qw = clq.clq_quantize_weights(torch.from_numpy(W).to(dev), l.block)
         bd = torch.from_numpy(b).to(dev)
-        Xq = torch.empty((l.M, l.K // 2), dtype=torch.uint8, device=dev)
+        Xq = torch.empty(clq.clq_act_bytes(l.M, l.K), dtype=torch.uint8, device=dev)
         xs = torch.empty(l.M, dtype=torch.float32, device=dev)
         Y = torch.empty((l.M, l.N), dtype=torch.float16, device=dev)
         state.append((l, Xd, qw, bd, Xq, xs, Y))

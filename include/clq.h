@@ -58,11 +58,11 @@ typedef enum {
     CLQ_ERR_SHAPE = 2, /* M, N, K, ld* out of range or not multiples         */
     CLQ_ERR_BLOCK = 3, /* block not in {32, 64, 128} or K % block != 0       */
     CLQ_ERR_ALIGN = 4, /* a pointer is not aligned as required               */
-    CLQ_ERR_ARG = 5,   /* clip_ratio outside (0, 1]                           */
+    CLQ_ERR_ARG = 5,   /* clip_ratio outside [2^-24, 1]                       */
     CLQ_ERR_HIP = 6    /* a HIP launch failed (see hipGetLastError)           */
 } clq_status;
 
-/* Library version; bumps whenever the packed weight layout changes. */
+/* Library version; bumps whenever a packed layout (Wq, Xq) changes. */
 int clq_version(void);
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -73,12 +73,17 @@ const char *clq_status_string(clq_status status);
  * padded up to a multiple of 64). */
 size_t clq_weight_bytes(int64_t N, int64_t K);
 
+/* Size in bytes of the packed activation buffer `Xq` for M tokens of K
+ * codes.  Returns 0 if the shape is invalid.  Rows are padded up to a
+ * multiple of 32 (padding rows hold zero codes). */
+size_t clq_act_bytes(int64_t M, int64_t K);
+
 /* Offline weight transform (Sec. 3.3: W absorbs G; Sec. 3.1: weights are
  * quantized once, per output channel; Sec. 4.1: one clip per matrix).
  *   W        fp16 [N][K], row-major, contiguous (torch Linear layout).
  *   perm     int32 [K] gather vector s (x'[k] = x[perm[k]]), or NULL.
  *   block    Hadamard block size b.
- *   clip_ratio  alpha in (0, 1]: the clip bound is alpha * max|w~| per row.
+ *   clip_ratio  alpha in [2^-24, 1]: the clip bound is alpha * max|w~| per row.
  *   Wq       out, clq_weight_bytes(N, K) bytes, opaque layout (padding rows
  *            are written as zero codes).
  *   w_scale  out, fp32 [N]: (alpha * max|w~| / 7) / b -- the 1/b of the
@@ -93,8 +98,10 @@ clq_status clq_quantize_weights(const void *W, const int32_t *perm, int64_t N,
  * Sec. 3.1 dynamic per-token quantization).
  *   X        fp16 [M][K] with row stride ldx (elements).
  *   perm     int32 [K] gather vector, or NULL.
- *   Xq       out, uint8 [M][K/2]: int4 codes, two's complement, byte j holds
- *            code 2j in its low nibble and code 2j+1 in its high nibble.
+ *   Xq       out, clq_act_bytes(M, K) bytes: int4 codes, two's complement,
+ *            two per byte (the lower-k code of a pair in the low nibble), in
+ *            an opaque tiled order that clq_w4a4_linear reads with whole-line
+ *            transfers; clq_unswizzle_act gives the row-major form.
  *   x_scale  out, fp32 [M]: max|x~| / 7 for the row (0 for an all-zero row).
  * x~ = FWHT_b(gather(X[m], perm)) in fp32 with the stage order h = 1, 2, 4,
  * ..., b/2; q = rne(x~ * fl32(7 / max|x~|)), the product taken exactly. */
@@ -103,7 +110,7 @@ clq_status clq_rotate_quant_act(const void *X, int64_t ldx, const int32_t *perm,
                                 float *x_scale, hipStream_t stream);
 
 /* W4A4 linear: Y = dequant(Xq . Wq^T) + bias, written as fp16.
- *   Xq, x_scale   from clq_rotate_quant_act (M rows).
+ *   Xq, x_scale   from clq_rotate_quant_act (M rows, same K).
  *   Wq, w_scale   from clq_quantize_weights (N rows).
  *   bias          fp16 [N] or NULL.
  *   Y             out, fp16 [M][N] with row stride ldy (elements).
@@ -122,9 +129,14 @@ clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M,
                               hipStream_t stream);
 
 /* Diagnostic: converts the opaque Wq layout back to canonical packed codes,
- * uint8 [N][K/2] (same nibble convention as Xq). */
+ * uint8 [N][K/2]: byte j of a row holds code 2j (low nibble) and 2j+1. */
 clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K,
                                  void *Wq_canonical, hipStream_t stream);
+
+/* Diagnostic: converts the opaque Xq layout back to canonical packed codes,
+ * uint8 [M][K/2] (16-byte aligned), same nibble convention. */
+clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K,
+                             void *Xq_canonical, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -7,8 +7,9 @@ carry the names of the C entry points declared in ``include/clq.h``:
     clq_quantize_weights(W, block, perm=None, clip_ratio=1.0) -> QWeight
     clq_rotate_quant_act(X, block, perm=None)                 -> (Xq, x_scale)
     clq_w4a4_linear(Xq, x_scale, qw, bias=None)               -> Y
-    clq_w4a4_accum_i32(Xq, qw)                                 -> acc
+    clq_w4a4_accum_i32(Xq, x_scale, qw)                        -> acc
     clq_unswizzle_weights(qw)                                  -> canonical codes
+    clq_unswizzle_act(Xq, M, K)                                -> canonical codes
 
 Paper: "CLQ" (arXiv 2509.24416) -- Sec. 3.3 (online block-Hadamard rotation,
 weights absorb it offline) and Sec. 3.1 Eq. (1) (4-bit quantizer; dynamic
@@ -39,18 +40,21 @@ _lib.clq_status_string.restype = ctypes.c_char_p
 _lib.clq_status_string.argtypes = [ctypes.c_int]
 _lib.clq_weight_bytes.restype = ctypes.c_size_t
 _lib.clq_weight_bytes.argtypes = [_i64, _i64]
+_lib.clq_act_bytes.restype = ctypes.c_size_t
+_lib.clq_act_bytes.argtypes = [_i64, _i64]
 _lib.clq_quantize_weights.argtypes = [_p, _p, _i64, _i64, _i32, _f32, _p, _p, _p]
 _lib.clq_rotate_quant_act.argtypes = [_p, _i64, _p, _i64, _i64, _i32, _p, _p, _p]
 _lib.clq_w4a4_linear.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p]
 _lib.clq_w4a4_accum_i32.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _p]
 _lib.clq_unswizzle_weights.argtypes = [_p, _i64, _i64, _p, _p]
+_lib.clq_unswizzle_act.argtypes = [_p, _i64, _i64, _p, _p]
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
-           "clq_w4a4_accum_i32", "clq_unswizzle_weights"):
+           "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act"):
     getattr(_lib, _f).restype = ctypes.c_int
 
-EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_quantize_weights",
-           "clq_rotate_quant_act", "clq_w4a4_linear", "clq_w4a4_accum_i32",
-           "clq_unswizzle_weights")
+EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
+           "clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
+           "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act")
 
 CLQ_OK, CLQ_ERR_NULL, CLQ_ERR_SHAPE, CLQ_ERR_BLOCK, CLQ_ERR_ALIGN, CLQ_ERR_ARG, CLQ_ERR_HIP = range(7)
 
@@ -105,6 +109,10 @@ def clq_weight_bytes(N, K):
     return int(_lib.clq_weight_bytes(N, K))
 
 
+def clq_act_bytes(M, K):
+    return int(_lib.clq_act_bytes(M, K))
+
+
 @dataclass
 class QWeight:
     """A weight matrix quantized by clq_quantize_weights."""
@@ -137,33 +145,45 @@ def clq_quantize_weights(W, block, perm=None, clip_ratio=1.0, stream=None):
 
 def clq_rotate_quant_act(X, block, perm=None, out=None, scale_out=None, stream=None):
     """Online: x~ = FWHT(gather(x, perm)) per token, quantized to int4 codes
-    (packed two per byte) with one fp32 scale per token.  X may have a row
-    stride larger than K (a column slice of a wider tensor)."""
+    with one fp32 scale per token.  Returns (Xq, x_scale): Xq is the opaque
+    packed buffer (uint8 [clq_act_bytes(M, K)]).  X may have a row stride
+    larger than K (a column slice of a wider tensor)."""
     _dev(X, "X", torch.float16)
     if X.dim() != 2 or X.stride(1) != 1:
         raise ValueError("X must be 2-D [M, K] with unit column stride")
     M, K = X.shape
     perm = _perm(perm, K)
-    Xq = out if out is not None else torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+    nbytes = clq_act_bytes(M, K)
+    if nbytes == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_rotate_quant_act")
+    Xq = out if out is not None else torch.empty(nbytes, dtype=torch.uint8, device=X.device)
     xs = scale_out if scale_out is not None else torch.empty(M, dtype=torch.float32, device=X.device)
     _dev(Xq, "Xq", torch.uint8)
     _dev(xs, "x_scale", torch.float32)
+    if Xq.numel() < nbytes or not Xq.is_contiguous() or xs.numel() < M:
+        raise ValueError("Xq / x_scale buffers are too small")
     _check(_lib.clq_rotate_quant_act(_ptr(X), X.stride(0), _ptr(perm), M, K, block, _ptr(Xq),
                                      _ptr(xs), _stream(stream)), "clq_rotate_quant_act")
     return Xq, xs
 
 
-def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None):
-    """Y = dequant(Xq . Wq^T) + bias as fp16 [M, N]."""
+def _check_xq(Xq, x_scale, K):
     _dev(Xq, "Xq", torch.uint8)
     _dev(x_scale, "x_scale", torch.float32)
+    M = x_scale.shape[0]
+    if not Xq.is_contiguous() or Xq.numel() < clq_act_bytes(M, K):
+        raise ValueError("Xq must be the contiguous buffer clq_rotate_quant_act produced for "
+                         "these M and K")
+    return M
+
+
+def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None):
+    """Y = dequant(Xq . Wq^T) + bias as fp16 [M, N] (M = len(x_scale))."""
+    M = _check_xq(Xq, x_scale, qw.K)
     if bias is not None:
         _dev(bias, "bias", torch.float16)
         if bias.shape != (qw.N,) or not bias.is_contiguous():
             raise ValueError("bias must be a contiguous fp16 [N] tensor")
-    M = Xq.shape[0]
-    if Xq.shape[1] * 2 != qw.K or not Xq.is_contiguous():
-        raise ValueError("Xq must be a contiguous [M, K/2] uint8 tensor matching the weight's K")
     if out is None:  # rows padded to a multiple of 8 elements (16-byte aligned rows)
         out = torch.empty((M, (qw.N + 7) // 8 * 8), dtype=torch.float16, device=Xq.device)[:, :qw.N]
     Y = out
@@ -176,12 +196,10 @@ def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None):
     return Y
 
 
-def clq_w4a4_accum_i32(Xq, qw, out=None, stream=None):
-    """The exact int32 accumulators sum_k qx * qw, [M, N] (diagnostic)."""
-    _dev(Xq, "Xq", torch.uint8)
-    M = Xq.shape[0]
-    if Xq.shape[1] * 2 != qw.K or not Xq.is_contiguous():
-        raise ValueError("Xq must be a contiguous [M, K/2] uint8 tensor matching the weight's K")
+def clq_w4a4_accum_i32(Xq, x_scale, qw, out=None, stream=None):
+    """The exact int32 accumulators sum_k qx * qw, [M, N] (diagnostic); the
+    scales only give M."""
+    M = _check_xq(Xq, x_scale, qw.K)
     if out is None:  # rows padded to a multiple of 4 elements (16-byte aligned rows)
         out = torch.empty((M, (qw.N + 3) // 4 * 4), dtype=torch.int32, device=Xq.device)[:, :qw.N]
     acc = out
@@ -196,4 +214,12 @@ def clq_unswizzle_weights(qw, stream=None):
     out = torch.empty((qw.N, qw.K // 2), dtype=torch.uint8, device=qw.wq.device)
     _check(_lib.clq_unswizzle_weights(_ptr(qw.wq), qw.N, qw.K, _ptr(out), _stream(stream)),
            "clq_unswizzle_weights")
+    return out
+
+
+def clq_unswizzle_act(Xq, M, K, stream=None):
+    """Canonical packed codes uint8 [M, K/2] of an activation buffer (diagnostic)."""
+    _dev(Xq, "Xq", torch.uint8)
+    out = torch.empty((M, K // 2), dtype=torch.uint8, device=Xq.device)
+    _check(_lib.clq_unswizzle_act(_ptr(Xq), M, K, _ptr(out), _stream(stream)), "clq_unswizzle_act")
     return out

@@ -9,7 +9,7 @@
 
 namespace {
 
-constexpr int kVersion = 1;
+constexpr int kVersion = 2;
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxRows = 2147483647;
 
@@ -57,6 +57,11 @@ size_t clq_weight_bytes(int64_t N, int64_t K) {
     return (size_t)clq::padded_rows(N) * (size_t)(K / 2);
 }
 
+size_t clq_act_bytes(int64_t M, int64_t K) {
+    if (check_rows(M) != CLQ_OK || check_k(K) != CLQ_OK) return 0;
+    return (size_t)clq::padded_act_rows(M) * (size_t)(K / 2);
+}
+
 clq_status clq_quantize_weights(const void *W, const int32_t *perm, int64_t N, int64_t K,
                                 int32_t block, float clip_ratio, void *Wq, float *w_scale,
                                 hipStream_t stream) {
@@ -82,9 +87,9 @@ clq_status clq_rotate_quant_act(const void *X, int64_t ldx, const int32_t *perm,
     if (ldx < K || ldx % 8 != 0) return CLQ_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(Xq, 16) || !aligned(x_scale, 4) || (perm && !aligned(perm, 4)))
         return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_rotate_quant(static_cast<const uint16_t *>(X), ldx, perm, M, M,
-                                             (int)K, block, 1.0f, false, 1.0f,
-                                             static_cast<uint8_t *>(Xq), x_scale, stream));
+    return from_hip(clq::launch_rotate_quant(static_cast<const uint16_t *>(X), ldx, perm, M,
+                                             clq::padded_act_rows(M), (int)K, block, 1.0f, false,
+                                             1.0f, static_cast<uint8_t *>(Xq), x_scale, stream));
 }
 
 static clq_status check_gemm(const void *Xq, const void *Wq, int64_t M, int64_t N, int64_t K,
@@ -129,6 +134,16 @@ clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K, void *Wq_
     if (!aligned(Wq, 16) || !aligned(Wq_canonical, 8)) return CLQ_ERR_ALIGN;
     return from_hip(clq::launch_unswizzle(static_cast<const uint8_t *>(Wq), N, (int)K,
                                           static_cast<uint8_t *>(Wq_canonical), stream));
+}
+
+clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K, void *Xq_canonical,
+                             hipStream_t stream) {
+    if (!Xq || !Xq_canonical) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (!aligned(Xq, 16) || !aligned(Xq_canonical, 16)) return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_unswizzle_act(static_cast<const uint8_t *>(Xq), M, (int)K,
+                                              static_cast<uint8_t *>(Xq_canonical), stream));
 }
 
 }  // extern "C"

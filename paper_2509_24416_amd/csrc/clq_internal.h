@@ -6,17 +6,17 @@
 
 namespace clq {
 
-// Packed weight layout (opaque to callers, version 1).
+// Packed weight layout (opaque to callers, version 2).
 //
-// Weight rows are grouped by 64.  Inside a group, "fragment" j (0..3) holds
-// the 16 rows n = 16*q + 4*j + i (q, i in 0..3) as its fragment rows
-// rho = 4*q + i.  A matrix-core fragment unit covers 16 rows x 64 k codes =
-// 512 packed bytes, stored in lane order: lane l = 16*g + rho holds the 8
-// bytes of k-group g (codes 16g .. 16g+15 of the unit's 64) of fragment row
-// rho.  Units are stored [unit row u = 4*G + j][k unit].  With this order a
-// wave reads one 16x64 operand fragment as one contiguous 512-byte run, and
-// the GEMM's output lane (q, i over the four fragments) owns 16 consecutive
-// output columns.
+// Rows are cut into units of 32 rows x 64 k codes (1 KB packed), each stored
+// in the lane order of a 32x32x32 int8 matrix-core operand read with one
+// 16-byte load per lane: lane l = 32*c + rho holds bytes 16c .. 16c+15 of
+// fragment row rho's 32-byte slice of the unit (codes 32c .. 32c+31).
+// Fragment row rho = 8g + 4h + i (g in 0..3, h, i in 0..1 / 0..3) holds
+// weight row n = 32u + 16h + 4g + i, so that accumulator element v of output
+// lane l is channel 32u + 16*(l/32) + v: each lane owns 16 consecutive output
+// channels.  Units are stored [row unit u][k unit]; rows are padded to a
+// multiple of 64 with zero codes.
 constexpr int kWeightRowPad = 64;
 
 __host__ __device__ inline int64_t padded_rows(int64_t N) {
@@ -25,12 +25,29 @@ __host__ __device__ inline int64_t padded_rows(int64_t N) {
 
 // Byte offset of the 8-byte piece (row n, k-group kg of 16 codes).
 __host__ __device__ inline int64_t wq_piece_offset(int64_t n, int64_t kg, int64_t K) {
-    const int64_t G = n >> 6;
-    const int w = (int)(n & 63);
-    const int q = w >> 4, j = (w >> 2) & 3, i = w & 3;
-    const int64_t u = 4 * G + j;
-    const int lane = (int)(kg & 3) * 16 + 4 * q + i;
-    return ((u * (K >> 6) + (kg >> 2)) * 64 + lane) * 8;
+    const int64_t u = n >> 5;
+    const int w = (int)(n & 31);
+    const int h = w >> 4, g = (w >> 2) & 3, i = w & 3;
+    const int rho = 8 * g + 4 * h + i;
+    const int lane = (int)((kg & 3) >> 1) * 32 + rho;
+    return ((u * (K >> 6) + (kg >> 2)) * 64 + lane) * 16 + (kg & 1) * 8;
+}
+
+// Packed activation layout (opaque to callers, version 2): the same unit
+// order as the weights without the row permutation.  Token rows are cut into
+// units of 32 rows x 64 codes (1 KB), lane l = 32*h + (row % 32) holding the
+// 16 bytes of codes 32h .. 32h+31 of the unit's 64; units are stored [row
+// unit][k unit]; rows are padded to a multiple of 32 with zero codes.  A GEMM
+// operand unit is then one contiguous, line-aligned 1 KB transfer.
+constexpr int kActRowPad = 32;
+
+__host__ __device__ inline int64_t padded_act_rows(int64_t M) {
+    return (M + kActRowPad - 1) / kActRowPad * kActRowPad;
+}
+
+// Byte offset of the 16-byte chunk holding codes 32c .. 32c+31 of row r.
+__host__ __device__ inline int64_t xq_chunk_offset(int64_t r, int64_t c, int64_t K) {
+    return (((r >> 5) * (K >> 6) + (c >> 1)) * 64 + (c & 1) * 32 + (r & 31)) * 16;
 }
 
 hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
@@ -40,6 +57,9 @@ hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *pe
 
 hipError_t launch_unswizzle(const uint8_t *Wq, int64_t N, int K, uint8_t *out,
                             hipStream_t stream);
+
+hipError_t launch_unswizzle_act(const uint8_t *Xq, int64_t M, int K, uint8_t *out,
+                                hipStream_t stream);
 
 hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
                        const float *ws, const uint16_t *bias, int64_t M, int64_t N,

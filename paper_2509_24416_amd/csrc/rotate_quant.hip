@@ -178,10 +178,13 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
     }
 
     if constexpr (!WEIGHT) {
-        uint4 *dst = reinterpret_cast<uint4 *>(out + grow * (K >> 1) + (int64_t)j * (B / 2));
+        // packed activation layout: one 16-byte chunk per 32 codes
 #pragma unroll
-        for (int c = 0; c < B / 32; ++c)
-            dst[c] = make_uint4(words[4 * c], words[4 * c + 1], words[4 * c + 2], words[4 * c + 3]);
+        for (int c = 0; c < B / 32; ++c) {
+            const int64_t c32 = (int64_t)j * (B / 32) + c;
+            *reinterpret_cast<uint4 *>(out + xq_chunk_offset(grow, c32, K)) =
+                make_uint4(words[4 * c], words[4 * c + 1], words[4 * c + 2], words[4 * c + 3]);
+        }
     } else {
         // packed weight layout: one 8-byte piece per k-group of 16 codes
 #pragma unroll
@@ -242,6 +245,16 @@ __global__ void unswizzle_kernel(const uint8_t *__restrict__ Wq, int64_t N, int 
     *reinterpret_cast<uint2 *>(out + n * (K / 2) + kg * 8) = v;
 }
 
+__global__ void unswizzle_act_kernel(const uint8_t *__restrict__ Xq, int64_t M, int K,
+                                     uint8_t *__restrict__ out) {
+    const int64_t cpr = K / 32;
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= M * cpr) return;
+    const int64_t r = idx / cpr, c = idx - r * cpr;
+    const uint4 v = *reinterpret_cast<const uint4 *>(Xq + xq_chunk_offset(r, c, K));
+    *reinterpret_cast<uint4 *>(out + r * (K / 2) + c * 16) = v;
+}
+
 }  // namespace
 
 hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
@@ -256,9 +269,9 @@ hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *pe
         }
     } else {
         switch (block) {
-            case 32: return launch_rq<32, false>(X, ldx, perm, rows, rows, K, 1.0f, 1.0f, out, scale, stream);
-            case 64: return launch_rq<64, false>(X, ldx, perm, rows, rows, K, 1.0f, 1.0f, out, scale, stream);
-            case 128: return launch_rq<128, false>(X, ldx, perm, rows, rows, K, 1.0f, 1.0f, out, scale, stream);
+            case 32: return launch_rq<32, false>(X, ldx, perm, rows, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
+            case 64: return launch_rq<64, false>(X, ldx, perm, rows, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
+            case 128: return launch_rq<128, false>(X, ldx, perm, rows, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
         }
     }
     return hipErrorInvalidValue;
@@ -269,6 +282,14 @@ hipError_t launch_unswizzle(const uint8_t *Wq, int64_t N, int K, uint8_t *out,
     const int64_t total = N * (K / 16);
     const int64_t grid = (total + 255) / 256;
     hipLaunchKernelGGL(unswizzle_kernel, dim3((unsigned)grid), dim3(256), 0, stream, Wq, N, K, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_unswizzle_act(const uint8_t *Xq, int64_t M, int K, uint8_t *out,
+                                hipStream_t stream) {
+    const int64_t total = M * (K / 32);
+    const int64_t grid = (total + 255) / 256;
+    hipLaunchKernelGGL(unswizzle_act_kernel, dim3((unsigned)grid), dim3(256), 0, stream, Xq, M, K, out);
     return hipGetLastError();
 }
 

@@ -35,6 +35,9 @@ def lib():
     L.clq_status_string.argtypes = [ctypes.c_int]
     L.clq_weight_bytes.restype = ctypes.c_size_t
     L.clq_weight_bytes.argtypes = [i64, i64]
+    L.clq_act_bytes.restype = ctypes.c_size_t
+    L.clq_act_bytes.argtypes = [i64, i64]
+    L.clq_unswizzle_act.argtypes = [p, i64, i64, p, p]
     L.clq_quantize_weights.argtypes = [p, p, i64, i64, i32, f32, p, p, p]
     L.clq_rotate_quant_act.argtypes = [p, i64, p, i64, i64, i32, p, p, p]
     L.clq_w4a4_linear.argtypes = [p, p, p, p, p, i64, i64, i64, p, i64, p]
@@ -45,7 +48,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 8, names
+    assert len(names) == 10, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -57,7 +60,7 @@ def test_binding_names_match_header():
 
 
 def test_version_and_strings(lib):
-    assert lib.clq_version() == 1
+    assert lib.clq_version() == 2
     for code in range(7):
         s = lib.clq_status_string(code).decode()
         assert s.startswith("CLQ")
@@ -72,6 +75,9 @@ def test_weight_bytes(lib):
     assert lib.clq_weight_bytes(0, 64) == 0
     assert lib.clq_weight_bytes(8, 96) == 0                  # K % 64 != 0
     assert lib.clq_weight_bytes(8, 65536) == 0               # K too large
+    assert lib.clq_act_bytes(8192, 1152) == 8192 * 576
+    assert lib.clq_act_bytes(45, 256) == 64 * 128           # rows padded to 32
+    assert lib.clq_act_bytes(0, 256) == 0
 
 
 A = 0x10000          # aligned fake device address (never dereferenced)
@@ -150,3 +156,7 @@ def test_accum_and_unswizzle_validation(lib):
     assert g(None, 8, 1152, A, None) == NULL
     assert g(A, 0, 1152, A, None) == SHAPE
     assert g(A, 8, 1152, A + 4, None) == ALIGN
+    h = lib.clq_unswizzle_act
+    assert h(None, 8, 1152, A, None) == NULL
+    assert h(A, 8, 100, A, None) == SHAPE
+    assert h(A, 8, 1152, A + 8, None) == ALIGN

@@ -54,7 +54,9 @@ def test_rotate_quant_bitexact(clq, M, K, block, law):
     Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
     ref_q, _, ref_s = oracle.quantize_act(X, block)
     assert np.array_equal(host(xs), ref_s)
-    assert np.array_equal(host(Xq), ref_q)
+    assert np.array_equal(host(clq.clq_unswizzle_act(Xq, M, K)), ref_q)
+    # padding rows of the packed buffer hold zero codes
+    assert Xq.numel() == clq.clq_act_bytes(M, K)
 
 
 @pytest.mark.parametrize("block", [32, 64, 128])
@@ -69,7 +71,7 @@ def test_rotate_quant_perm_and_stride(clq, block):
     Xq, xs = clq.clq_rotate_quant_act(Xd, block, dev(perm))
     ref_q, _, ref_s = oracle.quantize_act(X, block, perm)
     assert np.array_equal(host(xs), ref_s)
-    assert np.array_equal(host(Xq), ref_q)
+    assert np.array_equal(host(clq.clq_unswizzle_act(Xq, M, K)), ref_q)
 
 
 def test_rotate_quant_adversarial_rows(clq):
@@ -88,7 +90,17 @@ def test_rotate_quant_adversarial_rows(clq):
         Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
         ref_q, _, ref_s = oracle.quantize_act(X, block)
         assert np.array_equal(host(xs), ref_s), block
-        assert np.array_equal(host(Xq), ref_q), block
+        assert np.array_equal(host(clq.clq_unswizzle_act(Xq, 8, K)), ref_q), block
+
+
+def test_act_padding_rows_are_zero(clq):
+    M, K, block = 45, 256, 64                 # 45 rows -> 64 rows of storage
+    X = workloads.activations(M, K, "L1", seed=4)
+    Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
+    assert Xq.numel() == 64 * K // 2
+    full = host(clq.clq_unswizzle_act(Xq, 64, K))
+    assert np.array_equal(full[:M], oracle.quantize_act(X, block)[0])
+    assert not full[M:].any()
 
 
 # ---- weights -------------------------------------------------------------------
@@ -127,7 +139,7 @@ def test_accum_i32_bitexact(clq, M, N, K):
     W = workloads.weights(N, K, seed=N)
     qw = clq.clq_quantize_weights(dev(W), block)
     Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
-    acc = clq.clq_w4a4_accum_i32(Xq, qw)
+    acc = clq.clq_w4a4_accum_i32(Xq, xs, qw)
     _, xc, _ = oracle.quantize_act(X, block)
     _, wc, _ = oracle.quantize_weights(W, block)
     assert np.array_equal(host(acc), oracle.gemm_i32(xc, wc))
@@ -143,7 +155,7 @@ def test_accum_i32_extremes(clq):
     W[:, 0] = np.float16(1.0)
     qw = clq.clq_quantize_weights(dev(W), block)
     Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
-    acc = host(clq.clq_w4a4_accum_i32(Xq, qw))
+    acc = host(clq.clq_w4a4_accum_i32(Xq, xs, qw))
     _, xc, _ = oracle.quantize_act(X, block)
     _, wc, _ = oracle.quantize_weights(W, block)
     ref = oracle.gemm_i32(xc, wc)
@@ -192,7 +204,7 @@ def test_linear_block128_perm(clq):
     perm = workloads.random_perm(K, seed=15)
     qw = clq.clq_quantize_weights(dev(W), block, dev(perm))
     Xq, xs = clq.clq_rotate_quant_act(dev(X), block, dev(perm))
-    acc = clq.clq_w4a4_accum_i32(Xq, qw)
+    acc = clq.clq_w4a4_accum_i32(Xq, xs, qw)
     Y = clq.clq_w4a4_linear(Xq, xs, qw, dev(b))
     ref = oracle.linear(X, W, b, block, perm)
     assert np.array_equal(host(acc), ref["acc"])
@@ -214,7 +226,8 @@ def test_full_size_layer_sampled(clq, layer):
     rng = np.random.default_rng(layer.seed)
     rows = np.unique(np.concatenate([[0, layer.M - 1], rng.choice(layer.M, 30, replace=False)]))
     rows_t = torch.from_numpy(rows).cuda()
-    Xq_s, xs_s, Y_s = host(Xq[rows_t]), host(xs[rows_t]), host(Y[rows_t])
+    Xq_s = host(clq.clq_unswizzle_act(Xq, layer.M, layer.K)[rows_t])
+    xs_s, Y_s = host(xs[rows_t]), host(Y[rows_t])
     ref_xq, xc, ref_xs = oracle.quantize_act(X[rows], layer.block)
     assert np.array_equal(xs_s, ref_xs)
     assert np.array_equal(Xq_s, ref_xq)
@@ -224,5 +237,5 @@ def test_full_size_layer_sampled(clq, layer):
     y64, p64 = oracle.epilogue(acc, ref_xs, ws_ref, b)
     assert oracle.err_metric(Y_s.astype(np.float64), y64, p64, b) <= TOL
     # the exact accumulators on the same rows, through the int32 variant
-    acc_gpu = clq.clq_w4a4_accum_i32(Xq, qw)
+    acc_gpu = clq.clq_w4a4_accum_i32(Xq, xs, qw)
     assert np.array_equal(host(acc_gpu[rows_t]), acc)
