@@ -23,8 +23,8 @@
  *   - All data pointers are DEVICE pointers (hipMalloc'd or equivalent) unless
  *     stated; fp16 means IEEE binary16 stored as 2-byte values.
  *   - The caller owns and allocates every buffer.  The library allocates no
- *     device memory, keeps no global state, never synchronises, and never
- *     writes to its inputs.  Each call validates its arguments on the host,
+ *     device memory, keeps no global state on the device, never synchronises,
+ *     and never writes to its inputs.  Each call validates its arguments on the host,
  *     then enqueues its kernels on `stream` and returns; results are
  *     available once the stream reaches that point.
  *   - On a validation error nothing is enqueued and the error code is
@@ -59,10 +59,12 @@ typedef enum {
     CLQ_ERR_BLOCK = 3, /* block not in {32, 64, 128} or K % block != 0       */
     CLQ_ERR_ALIGN = 4, /* a pointer is not aligned as required               */
     CLQ_ERR_ARG = 5,   /* clip_ratio outside [2^-24, 1]                       */
-    CLQ_ERR_HIP = 6    /* a HIP launch failed (see hipGetLastError)           */
+    CLQ_ERR_HIP = 6,   /* a HIP launch failed (see hipGetLastError)           */
+    CLQ_ERR_WORKSPACE = 7 /* workspace smaller than clq_w4a4_workspace_bytes() */
 } clq_status;
 
-/* Library version; bumps whenever a packed layout (Wq, Xq) changes. */
+/* Library version; bumps whenever a packed layout (Wq, Xq) or an entry point
+ * signature changes. */
 int clq_version(void);
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -109,23 +111,38 @@ clq_status clq_rotate_quant_act(const void *X, int64_t ldx, const int32_t *perm,
                                 int64_t M, int64_t K, int32_t block, void *Xq,
                                 float *x_scale, hipStream_t stream);
 
-/* W4A4 linear: Y = dequant(Xq . Wq^T) + bias, written as fp16.
+/* Size in bytes of the optional GEMM workspace (depends only on the current
+ * device's compute-unit count; a few tens of MB).  With a workspace the GEMM
+ * may split the k loop of its last tile rounds over every workgroup, which
+ * balances shapes whose tile count fills the chip badly. */
+size_t clq_w4a4_workspace_bytes(void);
+
+/* W4A4 linear: Y = dequant(Xq . Wq^T) + bias, written as fp16 (Eq. (1): the
+ * integer product of the codes times the two scales).
  *   Xq, x_scale   from clq_rotate_quant_act (M rows, same K).
  *   Wq, w_scale   from clq_quantize_weights (N rows).
  *   bias          fp16 [N] or NULL.
  *   Y             out, fp16 [M][N] with row stride ldy (elements).
- * y[m][n] = fp16_rne(fma(fl32(acc * x_scale[m]), w_scale[n], bias[n])) with
- * acc = sum_k qx[m][k] * qw[n][k] computed exactly in int32. */
+ *   workspace     NULL, or workspace_bytes >= clq_w4a4_workspace_bytes() of
+ *                 device memory, 16-byte aligned, zero-filled before its first
+ *                 use; every call leaves it ready for the next.  Calls that
+ *                 share a workspace must not run concurrently (one stream, or
+ *                 one workspace per stream).  Results do not depend on it.
+ * y[m][n] = fp16(fl32(acc * x_scale[m]) * w_scale[n] + bias[n]), the last
+ * multiply-add fused and rounded to fp16 (within one fp16 unit of rounding
+ * the fp32 fma), with acc = sum_k qx[m][k] * qw[n][k] computed exactly. */
 clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
                            const float *w_scale, const void *bias, int64_t M,
                            int64_t N, int64_t K, void *Y, int64_t ldy,
+                           void *workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
 /* Diagnostic: the exact integer accumulators acc[m][n] = sum_k qx*qw as
- * int32 [M][N] with row stride ldacc (elements).  Same kernels as
- * clq_w4a4_linear with the epilogue replaced by an int32 store. */
+ * int32 [M][N] with row stride ldacc (elements).  Same kernels and workspace
+ * rules as clq_w4a4_linear with the epilogue replaced by an int32 store. */
 clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M,
                               int64_t N, int64_t K, int32_t *acc, int64_t ldacc,
+                              void *workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
 /* Diagnostic: converts the opaque Wq layout back to canonical packed codes,

@@ -44,8 +44,10 @@ _lib.clq_act_bytes.restype = ctypes.c_size_t
 _lib.clq_act_bytes.argtypes = [_i64, _i64]
 _lib.clq_quantize_weights.argtypes = [_p, _p, _i64, _i64, _i32, _f32, _p, _p, _p]
 _lib.clq_rotate_quant_act.argtypes = [_p, _i64, _p, _i64, _i64, _i32, _p, _p, _p]
-_lib.clq_w4a4_linear.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p]
-_lib.clq_w4a4_accum_i32.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _p]
+_lib.clq_w4a4_workspace_bytes.restype = ctypes.c_size_t
+_lib.clq_w4a4_workspace_bytes.argtypes = []
+_lib.clq_w4a4_linear.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p, ctypes.c_size_t, _p]
+_lib.clq_w4a4_accum_i32.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _p, ctypes.c_size_t, _p]
 _lib.clq_unswizzle_weights.argtypes = [_p, _i64, _i64, _p, _p]
 _lib.clq_unswizzle_act.argtypes = [_p, _i64, _i64, _p, _p]
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
@@ -53,10 +55,11 @@ for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
-           "clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
-           "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act")
+           "clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_workspace_bytes",
+           "clq_w4a4_linear", "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act")
 
-CLQ_OK, CLQ_ERR_NULL, CLQ_ERR_SHAPE, CLQ_ERR_BLOCK, CLQ_ERR_ALIGN, CLQ_ERR_ARG, CLQ_ERR_HIP = range(7)
+(CLQ_OK, CLQ_ERR_NULL, CLQ_ERR_SHAPE, CLQ_ERR_BLOCK, CLQ_ERR_ALIGN, CLQ_ERR_ARG, CLQ_ERR_HIP,
+ CLQ_ERR_WORKSPACE) = range(8)
 
 
 class ClqError(RuntimeError):
@@ -167,6 +170,30 @@ def clq_rotate_quant_act(X, block, perm=None, out=None, scale_out=None, stream=N
     return Xq, xs
 
 
+def clq_w4a4_workspace_bytes():
+    return int(_lib.clq_w4a4_workspace_bytes())
+
+
+_workspaces = {}
+
+
+def _workspace(device, workspace):
+    """The GEMM workspace: the caller's tensor, False for none, or (default)
+    one zero-filled buffer per device, allocated on first use.  Calls that
+    share it run in stream order; pass a tensor of your own per stream to
+    run GEMMs concurrently on several streams."""
+    if workspace is False:
+        return None, 0
+    if workspace is None:
+        key = device.index if device.index is not None else torch.cuda.current_device()
+        workspace = _workspaces.get(key)
+        if workspace is None:
+            workspace = torch.zeros(clq_w4a4_workspace_bytes(), dtype=torch.uint8, device=device)
+            _workspaces[key] = workspace
+    _dev(workspace, "workspace", torch.uint8)
+    return workspace, workspace.numel()
+
+
 def _check_xq(Xq, x_scale, K):
     _dev(Xq, "Xq", torch.uint8)
     _dev(x_scale, "x_scale", torch.float32)
@@ -177,8 +204,10 @@ def _check_xq(Xq, x_scale, K):
     return M
 
 
-def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None):
-    """Y = dequant(Xq . Wq^T) + bias as fp16 [M, N] (M = len(x_scale))."""
+def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None, workspace=None):
+    """Y = dequant(Xq . Wq^T) + bias as fp16 [M, N] (M = len(x_scale)).
+    workspace: None (the per-device default), False (none), or a zero-filled
+    uint8 tensor of clq_w4a4_workspace_bytes() bytes."""
     M = _check_xq(Xq, x_scale, qw.K)
     if bias is not None:
         _dev(bias, "bias", torch.float16)
@@ -190,13 +219,14 @@ def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None):
     _dev(Y, "Y", torch.float16)
     if Y.dim() != 2 or Y.stride(1) != 1 or Y.shape != (M, qw.N):
         raise ValueError("Y must be 2-D [M, N] with unit column stride")
+    wsp, wsb = _workspace(Xq.device, workspace)
     _check(_lib.clq_w4a4_linear(_ptr(Xq), _ptr(x_scale), _ptr(qw.wq), _ptr(qw.w_scale), _ptr(bias),
-                                M, qw.N, qw.K, _ptr(Y), Y.stride(0), _stream(stream)),
+                                M, qw.N, qw.K, _ptr(Y), Y.stride(0), _ptr(wsp), wsb, _stream(stream)),
            "clq_w4a4_linear")
     return Y
 
 
-def clq_w4a4_accum_i32(Xq, x_scale, qw, out=None, stream=None):
+def clq_w4a4_accum_i32(Xq, x_scale, qw, out=None, stream=None, workspace=None):
     """The exact int32 accumulators sum_k qx * qw, [M, N] (diagnostic); the
     scales only give M."""
     M = _check_xq(Xq, x_scale, qw.K)
@@ -204,8 +234,9 @@ def clq_w4a4_accum_i32(Xq, x_scale, qw, out=None, stream=None):
         out = torch.empty((M, (qw.N + 3) // 4 * 4), dtype=torch.int32, device=Xq.device)[:, :qw.N]
     acc = out
     _dev(acc, "acc", torch.int32)
+    wsp, wsb = _workspace(Xq.device, workspace)
     _check(_lib.clq_w4a4_accum_i32(_ptr(Xq), _ptr(qw.wq), M, qw.N, qw.K, _ptr(acc), acc.stride(0),
-                                   _stream(stream)), "clq_w4a4_accum_i32")
+                                   _ptr(wsp), wsb, _stream(stream)), "clq_w4a4_accum_i32")
     return acc
 
 

@@ -9,7 +9,7 @@
 
 namespace {
 
-constexpr int kVersion = 2;
+constexpr int kVersion = 3;
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxRows = 2147483647;
 
@@ -48,6 +48,7 @@ const char *clq_status_string(clq_status s) {
         case CLQ_ERR_ALIGN: return "CLQ_ERR_ALIGN: a pointer is misaligned";
         case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio must lie in [2^-24, 1]";
         case CLQ_ERR_HIP: return "CLQ_ERR_HIP: a HIP launch failed";
+        case CLQ_ERR_WORKSPACE: return "CLQ_ERR_WORKSPACE: workspace smaller than clq_w4a4_workspace_bytes()";
     }
     return "CLQ: unknown status";
 }
@@ -103,27 +104,40 @@ static clq_status check_gemm(const void *Xq, const void *Wq, int64_t M, int64_t 
     return CLQ_OK;
 }
 
+static clq_status check_workspace(const void *workspace, size_t workspace_bytes) {
+    if (!workspace) return CLQ_OK;
+    if (workspace_bytes < clq::gemm_workspace_bytes()) return CLQ_ERR_WORKSPACE;
+    if (!aligned(workspace, 16)) return CLQ_ERR_ALIGN;
+    return CLQ_OK;
+}
+
+size_t clq_w4a4_workspace_bytes(void) { return clq::gemm_workspace_bytes(); }
+
 clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
                            const float *w_scale, const void *bias, int64_t M, int64_t N,
-                           int64_t K, void *Y, int64_t ldy, hipStream_t stream) {
+                           int64_t K, void *Y, int64_t ldy, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
     if (!x_scale || !w_scale) return CLQ_ERR_NULL;
     clq_status s = check_gemm(Xq, Wq, M, N, K, Y, ldy, 8);
     if (s != CLQ_OK) return s;
     if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2)))
         return CLQ_ERR_ALIGN;
+    if ((s = check_workspace(workspace, workspace_bytes)) != CLQ_OK) return s;
     return from_hip(clq::launch_gemm(static_cast<const uint8_t *>(Xq), x_scale,
                                      static_cast<const uint8_t *>(Wq), w_scale,
                                      static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy,
-                                     false, stream));
+                                     false, workspace, stream));
 }
 
 clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M, int64_t N, int64_t K,
-                              int32_t *acc, int64_t ldacc, hipStream_t stream) {
+                              int32_t *acc, int64_t ldacc, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
     clq_status s = check_gemm(Xq, Wq, M, N, K, acc, ldacc, 4);
     if (s != CLQ_OK) return s;
+    if ((s = check_workspace(workspace, workspace_bytes)) != CLQ_OK) return s;
     return from_hip(clq::launch_gemm(static_cast<const uint8_t *>(Xq), nullptr,
                                      static_cast<const uint8_t *>(Wq), nullptr, nullptr, M, N,
-                                     (int)K, acc, ldacc, true, stream));
+                                     (int)K, acc, ldacc, true, workspace, stream));
 }
 
 clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K, void *Wq_canonical,

@@ -61,8 +61,15 @@ hipError_t launch_unswizzle(const uint8_t *Wq, int64_t N, int K, uint8_t *out,
 hipError_t launch_unswizzle_act(const uint8_t *Xq, int64_t M, int K, uint8_t *out,
                                 hipStream_t stream);
 
+// Workspace for the split-k schedule of launch_gemm (bytes; depends on the
+// device's compute-unit count only).
+size_t gemm_workspace_bytes();
+
+// workspace: gemm_workspace_bytes() zero-filled bytes, or nullptr (whole
+// tiles only).  Calls that share a workspace must not overlap in time.
 hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
                        const float *ws, const uint16_t *bias, int64_t M, int64_t N,
-                       int K, void *Y, int64_t ldy, bool i32out, hipStream_t stream);
+                       int K, void *Y, int64_t ldy, bool i32out, void *workspace,
+                       hipStream_t stream);
 
 }  // namespace clq

@@ -16,25 +16,33 @@
 // Data movement.  A k-stage is 64 codes deep: one 32x64 "unit" (1 KB packed,
 // lane l's 16 bytes at 16*l) per 32 channels and per 32 tokens of the tile.
 // Units go from global memory straight into LDS (global_load_lds_dwordx4: no
-// registers, no VALU) through a ring of NS stages kept NS - 1 stages ahead of
-// the matrix cores.  Each wave reads its units back with one 16-byte LDS read
-// per lane and widens them to int8 in registers (packed operands halve the
-// LDS traffic).  Widening keeps each nibble in the high half of its byte, so
-// the int8 holds 16*q exactly; the int32 accumulator holds 256 * sum(qa*qw)
-// (|.| <= 256*49*K < 2^31) and the factor 2^-8 is folded into the activation
-// scale in the epilogue.  The k order inside a 32-code slice is permuted
-// identically for both operands, which leaves the dot product unchanged.
+// registers, no VALU) through a ring of kStages stages kept kStages - 1 ahead
+// of the matrix cores.  Each wave reads its units back with one 16-byte LDS
+// read per lane and widens them to int8 in registers.  Widening keeps each
+// nibble in the high half of its byte, so the int8 holds 16*q exactly; the
+// int32 accumulator holds 256 * sum(qa*qw) (|.| <= 256*49*K < 2^31) and the
+// factor 2^-8 is folded into the activation scale in the epilogue.  The k
+// order inside a 32-code slice is permuted identically for both operands,
+// which leaves the dot product unchanged.
 //
 // Synchronisation.  Every iteration issues the same number of memory
 // instructions per wave, so "stage s has landed" is a fixed s_waitcnt vmcnt
-// count; it is emitted together with the workgroup barrier as one asm
-// statement with a memory clobber, so nothing is reordered across it.  The
-// ring stages are separate LDS arrays, which lets the compiler see that a
-// read of one stage does not depend on a transfer into another.
+// count, emitted with the workgroup barrier as one asm statement.  The ring
+// stages are separate LDS arrays and the loop is unrolled over them, so each
+// stage index is a compile-time constant; the LDS reads of operands and
+// epilogue values are asm too, each followed by an explicit lgkmcnt wait,
+// because the compiler would otherwise wait for every transfer in flight
+// before any LDS read it cannot prove independent.
 //
-// Schedule: a persistent grid (one workgroup per compute unit) walks its
-// tiles; the stage stream runs across tile boundaries, so the next tile's
+// Schedule.  Two workgroups of four waves (one wave per SIMD each) share a
+// compute unit; a persistent grid of that many workgroups walks the tiles,
+// and the stage stream runs across tile boundaries, so the next tile's
 // transfers overlap this tile's last matrix-core work and its epilogue.
+// When the tile count leaves the last round badly filled and a workspace is
+// given, the tiles of the last one or two rounds are split along k into
+// equal shares of stages for every workgroup (integer sums are exact in any
+// order); the workgroup that computes a split tile's first stages owns it
+// and adds the others' partial accumulators before its epilogue.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -50,172 +58,234 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+template <int Q> using IC = std::integral_constant<int, Q>;
 
-// 16 int4 codes (8 packed bytes) -> 16 int8 values 16*q.  Output order:
-// even codes of d0, even codes of d1, odd codes of d0, odd codes of d1.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)reinterpret_cast<size_t>((CLQ_LDS const void *)p);
+}
+template <int OFF>
+__device__ __forceinline__ v4u lds_read16(uint32_t addr) {
+    v4u v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+    return v;
+}
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<I + 1, N>(f);
+    }
+}
+
 __device__ __forceinline__ v4i widen16(uint32_t d0, uint32_t d1) {
     return v4i{(int)((d0 << 4) & 0xF0F0F0F0u), (int)((d1 << 4) & 0xF0F0F0F0u),
                (int)(d0 & 0xF0F0F0F0u), (int)(d1 & 0xF0F0F0F0u)};
 }
 
 constexpr int kStages = 5;   // ring depth
-constexpr int kGroupM = 4;   // token panels per tile group (L2 reuse of channel panels)
+constexpr int kGroupM = 4;          // token panels per tile group (L2 reuse of channel panels)
+constexpr int kSpinLimit = 1 << 22;  // bound on a split-tile wait (about a second)
 
 template <int WN_, int WM_, int FN_, int FM_, int WGS_>
 struct Tile {
     static constexpr int WN = WN_, WM = WM_, FN = FN_, FM = FM_;
-    static constexpr int WGS = WGS_;               // workgroups per compute unit
-    static constexpr int NW = WN * WM;             // waves
+    static constexpr int WGS = WGS_;
+    static constexpr int NW = WN * WM;
     static constexpr int NT = NW * 64;
-    static constexpr int BN = WN * FN * 32;        // output channels per tile
-    static constexpr int BM = WM * FM * 32;        // tokens per tile
-    static constexpr int W_UNITS = BN / 32;        // units per stage
+    static constexpr int BN = WN * FN * 32;
+    static constexpr int BM = WM * FM * 32;
+    static constexpr int W_UNITS = BN / 32;
     static constexpr int X_UNITS = BM / 32;
     static constexpr int UNITS = W_UNITS + X_UNITS;
-    static constexpr int UPW = UNITS / NW;         // units each wave moves per stage
+    static constexpr int UPW = UNITS / NW;
     static constexpr int STAGE_BYTES = UNITS * 1024;
-    // epilogue operand chunks of 64 values (one 4-byte transfer per lane):
-    // token scales, channel scales, channel-bias pairs
     static constexpr int XS_CH = BM / 64, WS_CH = BN / 64, B_CH = BN / 128;
-    static constexpr int E_CH = XS_CH + WS_CH + B_CH;
-    static constexpr int EPW = (E_CH + NW - 1) / NW;   // chunks per wave per stage
+    static constexpr int PART_INTS = NT * FN * FM * 16;   // one partial tile
     static_assert(UNITS % NW == 0, "units split evenly over waves");
 };
 
-template <class C, bool I32OUT, bool RAGGED>
-__global__ void __launch_bounds__(C::NT, C::WGS)
-w4a4_gemm_kernel(const uint8_t *__restrict__ Xq, const float *__restrict__ xs,
-                 const uint8_t *__restrict__ Wq, const float *__restrict__ ws,
-                 const uint16_t *__restrict__ bias, int M, int N, int K,
-                 void *__restrict__ Y, int64_t ldy, int tiles_m, int tiles_n)
+// A run of k-stages [kb, ke) of tile L; j counts the runs of a workgroup.
+struct Seg {
+    int j, L, kb, ke, k;
+};
+
+struct GemmArgs {
+    const uint8_t *Xq;
+    const float *xs;
+    const uint8_t *Wq;
+    const float *ws;
+    const uint16_t *bias;
+    void *Y;
+    int64_t ldy;
+    int M, N, K, tiles_m, tiles_n;
+    int dp;        // tiles computed whole (the first dp in tile order)
+    int sk;        // k-stages of the remaining tiles, split evenly over the grid
+    int32_t *part; // partial accumulators, one tile per workgroup
+    int *flags;    // one per wave of every workgroup
+};
+
+template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+__global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
 {
     constexpr int NS = kStages;
-    // Ring of NS stages: operand units, then the epilogue operands of the
-    // stage's tile (token scales fp32 [BM], channel scales fp32 [BN], biases
-    // fp16 [BN]), so that a tile's operands have landed by its last stage.
+    constexpr bool BIAS_CH = BIAS && !RAGGED && !I32OUT;
+    constexpr int E_CH = I32OUT ? 0 : C::XS_CH + C::WS_CH + (BIAS_CH ? C::B_CH : 0);
+    constexpr int EPW = (E_CH + C::NW - 1) / C::NW;
+    constexpr int VPI = C::UPW + EPW;
     constexpr int E_XS = C::STAGE_BYTES, E_WS = E_XS + C::BM * 4, E_B = E_WS + C::BN * 4;
-    constexpr int SLOT = I32OUT ? C::STAGE_BYTES : E_B + C::BN * 2;
-    __shared__ __align__(16) uint8_t ring[NS][SLOT];
+    constexpr int SLOT = I32OUT ? C::STAGE_BYTES : E_B + (BIAS_CH ? C::BN * 2 : 0);
+    static_assert(NS == 5 || NS == 6, "ring arrays below");
+    __shared__ __align__(16) uint8_t ring0[SLOT], ring1[SLOT], ring2[SLOT], ring3[SLOT], ring4[SLOT];
+    __shared__ __align__(16) uint8_t ring5[NS == 6 ? SLOT : 16];
+    auto slot = [&](auto qc) -> uint8_t * {
+        constexpr int q = decltype(qc)::value;
+        if constexpr (q == 0) return ring0;
+        else if constexpr (q == 1) return ring1;
+        else if constexpr (q == 2) return ring2;
+        else if constexpr (q == 3) return ring3;
+        else if constexpr (q == 4) return ring4;
+        else return ring5;
+    };
 
-    // Persistent, XCD-aware schedule.  Workgroup b runs on XCD b % 8 (ids are
-    // dealt round-robin).  Tiles are numbered in groups of kGroupM token
-    // panels (within a group, consecutive numbers walk the token panels of
-    // one channel panel), and the numbering is cut into 8 contiguous runs,
-    // one per XCD; the gx workgroups of an XCD take turns through their run.
-    // The tiles an XCD works on at any time then share few panels, which its
-    // L2 serves.
-    const int nks = K >> 6;
-    const int ntiles = tiles_m * tiles_n;
-    const int xcd = blockIdx.x & 7, jw = blockIdx.x >> 3, gx = gridDim.x >> 3;
-    const int per = ntiles >> 3, rem = ntiles & 7;
+    const int M = a.M, N = a.N, nks = a.K >> 6;
+    const int G = gridDim.x, gx = G >> 3, xcd = blockIdx.x & 7, jw = blockIdx.x >> 3;
+    const int rank = xcd * gx + jw;
+    const int dp = a.dp, S = a.sk;
+    const int per = dp >> 3, rem = dp & 7;
     const int cnt = per + (xcd < rem ? 1 : 0);
-    const int start = xcd * per + min(xcd, rem);
-    const int my_tiles = jw < cnt ? (cnt - jw + gx - 1) / gx : 0;
-    const int total = my_tiles * nks;   // k-stages this workgroup runs
+    const int dstart = xcd * per + min(xcd, rem);
+    const int my_dp = jw < cnt ? (cnt - jw + gx - 1) / gx : 0;
+    const int sk_a = rank * S / G, sk_b = (rank + 1) * S / G;
+    const int total = my_dp * nks + (sk_b - sk_a);
     if (total == 0) return;
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wn = wave % C::WN, wm = wave / C::WN;
     const int wunits_total = (int)(padded_rows(N) >> 5);
     const int xunits_total = (int)(padded_act_rows(M) >> 5);
-    // bias == nullptr: the transfers read the (valid) channel scales instead
-    // and the epilogue masks the value to zero
-    const uint32_t *bsrc = reinterpret_cast<const uint32_t *>(bias ? (const void *)bias : (const void *)ws);
-    const uint32_t bmask = bias ? 0xffffffffu : 0u;
 
-    auto tile_coords = [&](int i, int &tm, int &tn) {
-        const int L = start + jw + i * gx;
-        const int gsz = kGroupM * tiles_n;
+    auto coords = [&](int L, int &tm, int &tn) {
+        const int gsz = kGroupM * a.tiles_n;
         const int g = L / gsz, r = L - g * gsz;
         const int m0 = g * kGroupM;
-        const int gm = min(tiles_m - m0, kGroupM);
+        const int gm = min(a.tiles_m - m0, kGroupM);
         tn = r / gm;
         tm = m0 + (r - tn * gm);
     };
+    // A segment: k-stages [kb, ke) of tile L.  Whole tiles first, then this
+    // workgroup's share of the split region.
+    auto next_seg = [&](Seg &c) {
+        ++c.j;
+        if (c.j < my_dp) {
+            c.L = dstart + jw + c.j * gx;
+            c.kb = 0;
+            c.ke = nks;
+        } else {
+            const int g = c.j == my_dp ? sk_a : (c.L - dp + 1) * nks;
+            const int u = g / nks;
+            c.L = dp + u;
+            c.kb = g - u * nks;
+            c.ke = min(nks, c.kb + (sk_b - g));
+        }
+        c.k = c.kb;
+    };
 
-    // ---- producer: one stage's transfers (the same count on every wave) -----
-    // UPW operand units per wave, then (unless I32OUT) EPW chunks of 64
-    // epilogue operands, 4 bytes per lane; chunk numbers past the real ones
-    // re-read a channel-scale chunk into its own place (identical bytes).  The
-    // ragged-edge kernel reads its biases in the epilogue instead.
-    constexpr int EPW = I32OUT ? 0 : C::EPW;
-    constexpr int VPI = C::UPW + EPW;   // memory instructions per wave per stage
-    int p_i = 0, p_ks = 0, p_tm = 0, p_tn = 0, p_s = 0, p_q = 0;   // producer
-    tile_coords(0, p_tm, p_tn);
-    auto produce = [&]() {
-        uint8_t *slot = &ring[p_q][0];
+    // ---- producer -------------------------------------------------------------
+    Seg pc{-1, 0, 0, 0, 0};
+    next_seg(pc);
+    int p_s = 0;
+    const uint8_t *usrc[C::UPW];
+    const uint8_t *esrc[EPW > 0 ? EPW : 1];
+    int edst[EPW > 0 ? EPW : 1];
+    auto p_setup = [&]() {
+        int tm, tn;
+        coords(pc.L, tm, tn);
 #pragma unroll
         for (int j = 0; j < C::UPW; ++j) {
-            const int u = wave * C::UPW + j;   // wave-uniform
-            const uint8_t *src;
+            const int u = wave * C::UPW + j;
             if (u < C::W_UNITS) {
-                const int ug = min(p_tn * C::W_UNITS + u, wunits_total - 1);
-                src = Wq + ((int64_t)ug * nks + p_ks) * 1024 + lane * 16;
+                const int ug = min(tn * C::W_UNITS + u, wunits_total - 1);
+                usrc[j] = a.Wq + (int64_t)ug * nks * 1024;
             } else {
-                const int ux = min(p_tm * C::X_UNITS + (u - C::W_UNITS), xunits_total - 1);
-                src = Xq + ((int64_t)ux * nks + p_ks) * 1024 + lane * 16;
+                const int ux = min(tm * C::X_UNITS + (u - C::W_UNITS), xunits_total - 1);
+                usrc[j] = a.Xq + (int64_t)ux * nks * 1024;
             }
-            __builtin_amdgcn_global_load_lds(src, (CLQ_LDS void *)(slot + u * 1024), 16, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < EPW; ++j) {
-            const int c = wave * EPW + j;      // wave-uniform chunk
-            const void *src;
-            int dst;
+            const int c = wave * EPW + j;
             if (c < C::XS_CH) {
-                src = xs + min(p_tm * C::BM + c * 64 + lane, M - 1);
-                dst = E_XS + c * 256;
-            } else if (c < C::XS_CH + C::WS_CH || c >= C::E_CH || RAGGED) {
+                esrc[j] = reinterpret_cast<const uint8_t *>(a.xs + min(tm * C::BM + c * 64 + lane, M - 1));
+                edst[j] = E_XS + c * 256;
+            } else if (c < C::XS_CH + C::WS_CH || c >= E_CH) {
                 const int w = (c - C::XS_CH) % C::WS_CH;
-                src = ws + min(p_tn * C::BN + w * 64 + lane, N - 1);
-                dst = E_WS + w * 256;
+                esrc[j] = reinterpret_cast<const uint8_t *>(a.ws + min(tn * C::BN + w * 64 + lane, N - 1));
+                edst[j] = E_WS + w * 256;
             } else {
-                // channel pairs (2p, 2p+1) of the tile; N % 16 == 0 here
                 const int b = c - C::XS_CH - C::WS_CH;
-                src = bsrc + min(p_tn * (C::BN / 2) + b * 64 + lane, N / 2 - 1);
-                dst = E_B + b * 256;
+                esrc[j] = reinterpret_cast<const uint8_t *>(reinterpret_cast<const uint32_t *>(a.bias) + min(tn * (C::BN / 2) + b * 64 + lane, N / 2 - 1));
+                edst[j] = E_B + b * 256;
             }
-            __builtin_amdgcn_global_load_lds(src, (CLQ_LDS void *)(slot + dst), 4, 0, 0);
         }
-        // advance to the next stage (clamped at the last one)
+    };
+    p_setup();
+    auto produce = [&](auto qc) {
+        uint8_t *dst = slot(qc);
+        const uint32_t voff = (uint32_t)(pc.k * 1024 + lane * 16);
+#pragma unroll
+        for (int j = 0; j < C::UPW; ++j)
+        {
+            const uint8_t *sp = usrc[j] + voff;
+            __builtin_amdgcn_global_load_lds(sp, (CLQ_LDS void *)(dst + (wave * C::UPW + j) * 1024), 16, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < EPW; ++j)
+            __builtin_amdgcn_global_load_lds(esrc[j], (CLQ_LDS void *)(dst + edst[j]), 4, 0, 0);
         if (p_s < total - 1) {
             ++p_s;
-            p_q = p_q == NS - 1 ? 0 : p_q + 1;
-            if (++p_ks == nks) {
-                p_ks = 0;
-                ++p_i;
-                tile_coords(p_i, p_tm, p_tn);
+            if (++pc.k == pc.ke) {
+                next_seg(pc);
+                p_setup();
             }
         }
     };
 
-    // ---- consumer ------------------------------------------------------------
-    // P: packed operands of one stage (one 16-byte LDS read per unit);
-    // A0/B0, A1/B1: the widened operands of its two 32-code halves.
-    uint4 pa[C::FN], pb[C::FM];
+    // ---- consumer -------------------------------------------------------------
+    v4u pa[C::FN], pb[C::FM];
     v4i a0[C::FN], b0[C::FM], a1[C::FN], b1[C::FM];
-    auto read_packed = [&](int q) {
-        const uint8_t *Wl = &ring[q][0];
-        const uint8_t *Xl = Wl + C::W_UNITS * 1024;
-#pragma unroll
-        for (int fn = 0; fn < C::FN; ++fn)
-            pa[fn] = *reinterpret_cast<const uint4 *>(Wl + (wn * C::FN + fn) * 1024 + lane * 16);
-#pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm)
-            pb[fm] = *reinterpret_cast<const uint4 *>(Xl + (wm * C::FM + fm) * 1024 + lane * 16);
+    const uint32_t wl0 = (uint32_t)(wn * C::FN * 1024 + lane * 16);
+    const uint32_t xl0 = (uint32_t)((C::W_UNITS + wm * C::FM) * 1024 + lane * 16);
+    auto read_packed = [&](auto qc) {
+        // the lane offsets pass through an empty asm so that the per-stage
+        // addresses are formed here, not hoisted into 30 live registers
+        uint32_t wl = wl0, xl = xl0;
+        asm volatile("" : "+v"(wl), "+v"(xl));
+        wl += lds_addr(slot(qc));
+        xl += lds_addr(slot(qc));
+        static_for<0, C::FN>([&](auto f) { pa[f] = lds_read16<decltype(f)::value * 1024>(wl); });
+        static_for<0, C::FM>([&](auto f) { pb[f] = lds_read16<decltype(f)::value * 1024>(xl); });
+    };
+    auto operands_ready = [&]() {
+        static_assert(C::FN == 4 && C::FM == 2, "operand list below");
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(pa[0]), "+v"(pa[1]), "+v"(pa[2]), "+v"(pa[3]), "+v"(pb[0]), "+v"(pb[1]));
     };
     auto widen_half0 = [&]() {
 #pragma unroll
-        for (int fn = 0; fn < C::FN; ++fn) a0[fn] = widen16(pa[fn].x, pa[fn].y);
+        for (int fn = 0; fn < C::FN; ++fn) a0[fn] = widen16(pa[fn][0], pa[fn][1]);
 #pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm) b0[fm] = widen16(pb[fm].x, pb[fm].y);
+        for (int fm = 0; fm < C::FM; ++fm) b0[fm] = widen16(pb[fm][0], pb[fm][1]);
     };
     auto widen_half1 = [&]() {
 #pragma unroll
-        for (int fn = 0; fn < C::FN; ++fn) a1[fn] = widen16(pa[fn].z, pa[fn].w);
+        for (int fn = 0; fn < C::FN; ++fn) a1[fn] = widen16(pa[fn][2], pa[fn][3]);
 #pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm) b1[fm] = widen16(pb[fm].z, pb[fm].w);
+        for (int fm = 0; fm < C::FM; ++fm) b1[fm] = widen16(pb[fm][2], pb[fm][3]);
     };
     v16i acc[C::FN][C::FM];
     auto zero_acc = [&]() {
@@ -224,99 +294,208 @@ w4a4_gemm_kernel(const uint8_t *__restrict__ Xq, const float *__restrict__ xs,
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = v16i{};
     };
-    auto mma = [&](const v4i (&a)[C::FN], const v4i (&b)[C::FM]) {
+    auto mma = [&](const v4i (&x)[C::FN], const v4i (&y)[C::FM]) {
 #pragma unroll
         for (int fn = 0; fn < C::FN; ++fn)
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm)
-                acc[fn][fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[fn], b[fm], acc[fn][fm], 0, 0, 0);
+                acc[fn][fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(x[fn], y[fm], acc[fn][fm], 0, 0, 0);
     };
-    // one matrix-core instruction, then up to `vpm` vector instructions, for
-    // every instruction of a half-step: widening runs in the MFMA shadow
-    constexpr int MPH = C::FN * C::FM;                         // MFMAs per half-step
-    constexpr int WOPS = (C::FN + C::FM) * 6;                  // widening VALU ops per half
-    constexpr int VPM = (WOPS + MPH - 1) / MPH + 1;
-    auto interleave = [&](int first_plain) {
+    constexpr int MPH = C::FN * C::FM;
+    constexpr int WOPS = (C::FN + C::FM) * 6;
+    constexpr int GA = 4, GB = 2;
+    auto interleave = [&](auto fpc, auto vpmc, auto dsc) {
+        constexpr int first_plain = decltype(fpc)::value, vpm = decltype(vpmc)::value;
+        constexpr int ds_after = decltype(dsc)::value;
 #pragma unroll
         for (int i = 0; i < MPH; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // MFMA
-            if (i >= first_plain) __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);   // VALU
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i >= first_plain) __builtin_amdgcn_sched_group_barrier(0x002, vpm, 0);
+            if (i == ds_after) __builtin_amdgcn_sched_group_barrier(0x100, C::FN + C::FM, 0);
         }
     };
 
-    // ---- epilogue: lane owns token m and 16 consecutive channels ----------
-    const int h16 = (lane >> 5) * 16;
-    auto epilogue = [&](int i, int q) {
-        int tm, tn;
-        tile_coords(i, tm, tn);
-        const float *e_xs = reinterpret_cast<const float *>(&ring[q][E_XS]);
-        const float *e_ws = reinterpret_cast<const float *>(&ring[q][E_WS]);
-        const uint32_t *e_b = reinterpret_cast<const uint32_t *>(&ring[q][E_B]);
+    // ---- split tiles: partial accumulators through global memory ---------------
+    // The workgroup that computes a split tile's first stages owns it; every
+    // other workgroup that computes some of its stages starts its own range
+    // there, stores its accumulators and raises its flags; the owner adds them
+    // before its epilogue.  Waves pair one to one (same wave, same lane).
+    constexpr int WPART = C::FN * C::FM * 16 * 64;   // ints per wave
+    // Partial tiles cross XCDs, whose L2 caches are not coherent with each
+    // other: they are written through to memory and read back past the L2
+    // (device-scope cache policy), and the flags are relaxed device-scope
+    // atomics.  Each wave orders its own data before its flag with a wait.
+    auto contribute = [&]() {
+        uint32_t lo = (uint32_t)lane * 16;
+        asm volatile("" : "+v"(lo));   // addresses formed here, not hoisted out of the loop
+        uint8_t *base = reinterpret_cast<uint8_t *>(a.part + (size_t)rank * C::PART_INTS + wave * WPART) + lo;
 #pragma unroll
-        for (int fm = 0; fm < C::FM; ++fm) {
-            const int ml = (wm * C::FM + fm) * 32 + (lane & 31);
-            const int m = tm * C::BM + ml;
-            float xsm = 0.0f;
-            if constexpr (!I32OUT) xsm = e_xs[ml] * (1.0f / 256.0f);
+        for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm) {
+                const v16i x = acc[fn][fm];
+                uint8_t *p = base + (fn * C::FM + fm) * 4096;
+                asm volatile(
+                    "global_store_dwordx4 %0, %1, off sc1\n\t"
+                    "global_store_dwordx4 %0, %2, off offset:1024 sc1\n\t"
+                    "global_store_dwordx4 %0, %3, off offset:2048 sc1\n\t"
+                    "global_store_dwordx4 %0, %4, off offset:3072 sc1"
+                    ::"v"(p), "v"(__builtin_shufflevector(x, x, 0, 1, 2, 3)),
+                    "v"(__builtin_shufflevector(x, x, 4, 5, 6, 7)), "v"(__builtin_shufflevector(x, x, 8, 9, 10, 11)),
+                    "v"(__builtin_shufflevector(x, x, 12, 13, 14, 15))
+                    : "memory");
+            }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __hip_atomic_store(a.flags + rank * C::NW + wave, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    auto fixup = [&](int L) {
+        static_assert(C::FM == 2, "two token fragments per load group");
+        const int u = L - dp;
+        const int beg = u * nks, end = beg + nks;
+        for (int r2 = rank + 1; r2 < G; ++r2) {
+            const int st = r2 * S / G;
+            if (st >= end) break;
+            const int en = (r2 + 1) * S / G;
+            if (en <= st || st <= beg) continue;
+            int *fl = a.flags + r2 * C::NW + wave;
+            for (int spin = 0; spin < kSpinLimit; ++spin) {
+                if (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
+                __builtin_amdgcn_s_sleep(8);
+            }
+            uint32_t lo = (uint32_t)lane * 16;
+            asm volatile("" : "+v"(lo));
+            const uint8_t *base = reinterpret_cast<const uint8_t *>(a.part + (size_t)r2 * C::PART_INTS + wave * WPART) + lo;
 #pragma unroll
             for (int fn = 0; fn < C::FN; ++fn) {
-                const int nl = (wn * C::FN + fn) * 32 + h16;
-                const int n0 = tn * C::BN + nl;
-                const v16i &a = acc[fn][fm];
+                const uint8_t *p0 = base + (fn * C::FM) * 4096, *p1 = p0 + 4096;
+                v4i q0, q1, q2, q3, q4, q5, q6, q7;
+                asm volatile(
+                    "global_load_dwordx4 %0, %8, off sc1\n\t"
+                    "global_load_dwordx4 %1, %8, off offset:1024 sc1\n\t"
+                    "global_load_dwordx4 %2, %8, off offset:2048 sc1\n\t"
+                    "global_load_dwordx4 %3, %8, off offset:3072 sc1\n\t"
+                    "global_load_dwordx4 %4, %9, off sc1\n\t"
+                    "global_load_dwordx4 %5, %9, off offset:1024 sc1\n\t"
+                    "global_load_dwordx4 %6, %9, off offset:2048 sc1\n\t"
+                    "global_load_dwordx4 %7, %9, off offset:3072 sc1\n\t"
+                    "s_waitcnt vmcnt(0)"
+                    : "=&v"(q0), "=&v"(q1), "=&v"(q2), "=&v"(q3), "=&v"(q4), "=&v"(q5), "=&v"(q6), "=&v"(q7)
+                    : "v"(p0), "v"(p1)
+                    : "memory");
+                acc[fn][0] += __builtin_shufflevector(__builtin_shufflevector(q0, q1, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                      __builtin_shufflevector(q2, q3, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                      0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+                acc[fn][1] += __builtin_shufflevector(__builtin_shufflevector(q4, q5, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                      __builtin_shufflevector(q6, q7, 0, 1, 2, 3, 4, 5, 6, 7),
+                                                      0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+            }
+            __hip_atomic_store(fl, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    };
+
+    // ---- epilogue: lane owns token m and 16 consecutive channels ----------------
+    const int h16 = (lane >> 5) * 16;
+    // The epilogue operands are read with asm too (same reason as the
+    // operand units); one explicit wait per channel fragment orders their use.
+    auto epilogue = [&](int L, auto qc) {
+        int tm, tn;
+        coords(L, tm, tn);
+        uint32_t lx = (uint32_t)((wm * C::FM * 32 + (lane & 31)) * 4);
+        uint32_t lw = (uint32_t)((wn * C::FN * 32 + h16) * 4);
+        asm volatile("" : "+v"(lx), "+v"(lw));
+        const uint32_t sb = lds_addr(slot(qc));
+        const uint32_t axs = sb + E_XS + lx, aws = sb + E_WS + lw, ab = sb + E_B + lw / 2;
+        float xsm[C::FM];
+        int mrow[C::FM];
+        if constexpr (!I32OUT) {
+            static_assert(C::FM == 2, "two token scales per lane");
+            asm volatile("ds_read_b32 %0, %2\n\tds_read_b32 %1, %2 offset:128\n\ts_waitcnt lgkmcnt(0)"
+                         : "=&v"(xsm[0]), "=&v"(xsm[1]) : "v"(axs));
+        }
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) mrow[fm] = tm * C::BM + (wm * C::FM + fm) * 32 + (lane & 31);
+        // channel operands outer, tokens inner: each channel scale and bias
+        // is loaded once and dies after its fragments
+        static_for<0, C::FN>([&](auto fc) {
+            constexpr int fn = decltype(fc)::value;
+            const int n0 = tn * C::BN + (wn * C::FN + fn) * 32 + h16;
+            v4f w4[4];
+            v8h b8[2];
+            if constexpr (!I32OUT) {
+                // one asm block: the reads and their wait, so no use can be
+                // scheduled between them
+                asm volatile(
+                    "ds_read_b128 %0, %4 offset:%6\n\t"
+                    "ds_read_b128 %1, %4 offset:%7\n\t"
+                    "ds_read_b128 %2, %4 offset:%8\n\t"
+                    "ds_read_b128 %3, %4 offset:%9\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=&v"(w4[0]), "=&v"(w4[1]), "=&v"(w4[2]), "=&v"(w4[3])
+                    : "v"(aws), "v"(ab), "n"(fn * 128), "n"(fn * 128 + 16), "n"(fn * 128 + 32), "n"(fn * 128 + 48));
+                if constexpr (BIAS_CH)
+                    asm volatile(
+                        "ds_read_b128 %0, %2 offset:%3\n\t"
+                        "ds_read_b128 %1, %2 offset:%4\n\t"
+                        "s_waitcnt lgkmcnt(0)"
+                        : "=&v"(b8[0]), "=&v"(b8[1])
+                        : "v"(ab), "n"(fn * 64), "n"(fn * 64 + 16));
+            }
+            // (element reads of the asm results stay typed: no bit casts of
+            // vector elements, which this compiler mis-vectorizes)
+            float wsv[16];
+            h2v bw[8];
+            if constexpr (!I32OUT) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) wsv[v] = w4[v / 4][v % 4];
+            }
+            if constexpr (!BIAS || I32OUT) {
+#pragma unroll
+                for (int v = 0; v < 8; ++v) bw[v] = h2v{(_Float16)0.0f, (_Float16)0.0f};
+            } else if constexpr (RAGGED) {
+#pragma unroll
+                for (int v = 0; v < 16; v += 2) {
+                    const int na = min(n0 + v, N - 1), nb = min(n0 + v + 1, N - 1);
+                    const _Float16 *bh = reinterpret_cast<const _Float16 *>(a.bias);
+                    bw[v / 2] = h2v{bh[na], bh[nb]};
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < 8; ++v) bw[v] = h2v{b8[v / 4][2 * (v % 4)], b8[v / 4][2 * (v % 4) + 1]};
+            }
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm) {
+                const int m = mrow[fm];
+                const v16i &x = acc[fn][fm];
                 if constexpr (I32OUT) {
-                    int32_t *dst = reinterpret_cast<int32_t *>(Y) + (int64_t)m * ldy + n0;
+                    int32_t *dst = reinterpret_cast<int32_t *>(a.Y) + (int64_t)m * a.ldy + n0;
                     if (m < M && n0 < N) {
                         if (!RAGGED || n0 + 16 <= N) {
 #pragma unroll
                             for (int q4 = 0; q4 < 4; ++q4)
-                                reinterpret_cast<int4 *>(dst)[q4] =
-                                    make_int4(a[4 * q4] >> 8, a[4 * q4 + 1] >> 8, a[4 * q4 + 2] >> 8, a[4 * q4 + 3] >> 8);
+                                reinterpret_cast<v4i *>(dst)[q4] =
+                                    v4i{x[4 * q4] >> 8, x[4 * q4 + 1] >> 8, x[4 * q4 + 2] >> 8, x[4 * q4 + 3] >> 8};
                         } else {
 #pragma unroll
                             for (int v = 0; v < 16; ++v)
-                                if (n0 + v < N) dst[v] = a[v] >> 8;
+                                if (n0 + v < N) dst[v] = x[v] >> 8;
                         }
                     }
                 } else {
-                    float wsv[16];
-                    uint32_t bw[8];
-#pragma unroll
-                    for (int q4 = 0; q4 < 4; ++q4) {
-                        const float4 w4 = reinterpret_cast<const float4 *>(e_ws + nl)[q4];
-                        wsv[4 * q4] = w4.x; wsv[4 * q4 + 1] = w4.y; wsv[4 * q4 + 2] = w4.z; wsv[4 * q4 + 3] = w4.w;
-                    }
-                    if constexpr (RAGGED) {
-#pragma unroll
-                        for (int v = 0; v < 16; v += 2) {
-                            const int na = min(n0 + v, N - 1), nb = min(n0 + v + 1, N - 1);
-                            bw[v / 2] = bias ? ((uint32_t)bias[na] | ((uint32_t)bias[nb] << 16)) : 0u;
-                        }
-                    } else {
-#pragma unroll
-                        for (int q2 = 0; q2 < 2; ++q2) {
-                            const uint4 b4 = reinterpret_cast<const uint4 *>(e_b + nl / 2)[q2];
-                            bw[4 * q2] = b4.x & bmask; bw[4 * q2 + 1] = b4.y & bmask;
-                            bw[4 * q2 + 2] = b4.z & bmask; bw[4 * q2 + 3] = b4.w & bmask;
-                        }
-                    }
                     uint32_t hv[8];
+                    const float xsc = xsm[fm] * (1.0f / 256.0f);   // accumulators hold 256 * sum
 #pragma unroll
                     for (int v = 0; v < 16; v += 2) {
-                        float y2[2];
-#pragma unroll
-                        for (int d = 0; d < 2; ++d) {
-                            const float p = (float)a[v + d] * xsm;
-                            const uint16_t bb = (uint16_t)(bw[v / 2] >> (16 * d));
-                            y2[d] = __builtin_fmaf(p, wsv[v + d], __half2float(__ushort_as_half(bb)));
-                        }
-                        hv[v / 2] = (uint32_t)__half_as_ushort(__float2half_rn(y2[0])) |
-                                    ((uint32_t)__half_as_ushort(__float2half_rn(y2[1])) << 16);
+                        const float p0 = (float)x[v] * xsc, p1 = (float)x[v + 1] * xsc;
+                        h2v h;
+                        h[0] = (_Float16)__builtin_fmaf(p0, wsv[v], (float)bw[v / 2][0]);
+                        h[1] = (_Float16)__builtin_fmaf(p1, wsv[v + 1], (float)bw[v / 2][1]);
+                        hv[v / 2] = __builtin_bit_cast(uint32_t, h);
                     }
-                    uint16_t *dst = reinterpret_cast<uint16_t *>(Y) + (int64_t)m * ldy + n0;
+                    uint16_t *dst = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)m * a.ldy + n0;
                     if (m < M && n0 < N) {
                         if (!RAGGED || n0 + 16 <= N) {
-                            reinterpret_cast<uint4 *>(dst)[0] = make_uint4(hv[0], hv[1], hv[2], hv[3]);
-                            reinterpret_cast<uint4 *>(dst)[1] = make_uint4(hv[4], hv[5], hv[6], hv[7]);
+                            reinterpret_cast<v4u *>(dst)[0] = v4u{hv[0], hv[1], hv[2], hv[3]};
+                            reinterpret_cast<v4u *>(dst)[1] = v4u{hv[4], hv[5], hv[6], hv[7]};
                         } else {
 #pragma unroll
                             for (int v = 0; v < 16; ++v)
@@ -325,106 +504,158 @@ w4a4_gemm_kernel(const uint8_t *__restrict__ Xq, const float *__restrict__ xs,
                     }
                 }
             }
-        }
+            __builtin_amdgcn_sched_barrier(0);
+        });
     };
 
-    // ---- pipeline ------------------------------------------------------------
-    // Stage s lives in ring stage s % NS.  Prologue: stages 0 .. NS-2 in
-    // flight; once stages 0 and 1 have landed, read stage 0 and widen its
-    // first half.  Iteration s (packed stage s in P, its first half in A0/B0):
-    //   wait until stage s+1 has landed -- its transfers are older than the
-    //   (NS-3) * VPI memory instructions this wave issued since -- and for
-    //   this wave's LDS reads; barrier.  Every wave is then done with ring
-    //   stage (s - 1) % NS, which receives stage s + NS - 1.
-    //   MFMAs on half 0 of stage s, widening half 1 of stage s in their shadow;
-    //   read stage s+1 into P;
-    //   MFMAs on half 1 of stage s, widening half 0 of stage s+1 in their
-    //   shadow (the first few MFMAs cover the LDS read latency);
-    //   after a tile's last stage, the epilogue (its scales and biases
-    //   travelled with the stage).
-    for (int k = 0; k < NS - 1; ++k) produce();
+    // ---- pipeline ---------------------------------------------------------------
+    produce(IC<0>{});
+    produce(IC<1>{});
+    produce(IC<2>{});
+    produce(IC<3>{});
+    if constexpr (NS == 6) produce(IC<4>{});
     asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NS - 3) * VPI) : "memory");
-    read_packed(0);
+    read_packed(IC<0>{});
+    operands_ready();
     widen_half0();
     zero_acc();
 
-    int c_ks = 0, c_i = 0, c_q = 0;   // consumer position: k-stage, tile, ring stage
-    for (int s = 0; s < total; ++s) {
+    Seg cc{-1, 0, 0, 0, 0};
+    next_seg(cc);
+    int s = 0;
+    constexpr int VH1 = (WOPS + GA - 1) / GA;
+    constexpr int VH2 = (WOPS + (MPH - GB) - 1) / (MPH - GB);
+    auto iter = [&](auto qc) -> bool {
+        constexpr int q = decltype(qc)::value;
+        constexpr IC<(q + 1) % NS> nqc{};
+        constexpr IC<(q + NS - 1) % NS> pqc{};
         asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 3) * VPI) : "memory");
-        produce();
+        produce(pqc);
         __builtin_amdgcn_sched_barrier(0);
         widen_half1();
         mma(a0, b0);
-        interleave(0);
+        read_packed(nqc);
+        interleave(IC<0>{}, IC<VH1>{}, IC<GA - 1>{});
         __builtin_amdgcn_sched_barrier(0);
-        const int nq = c_q == NS - 1 ? 0 : c_q + 1;
-        read_packed(nq);
-        __builtin_amdgcn_sched_barrier(0);
+        operands_ready();
         widen_half0();
         mma(a1, b1);
-        interleave(2);
+        interleave(IC<GB>{}, IC<VH2>{}, IC<-1>{});
         __builtin_amdgcn_sched_barrier(0);
-        if (c_ks == nks - 1) {
-            epilogue(c_i, c_q);
+        if (cc.k == cc.ke - 1) {
+            if (cc.kb != 0) {
+                contribute();
+            } else {
+                if (cc.ke != nks) fixup(cc.L);
+                epilogue(cc.L, qc);
+            }
             zero_acc();
-            c_ks = 0;
-            ++c_i;
+            if (s + 1 < total) next_seg(cc);
         } else {
-            ++c_ks;
+            ++cc.k;
         }
-        c_q = nq;
+        ++s;
+        return s < total;
+    };
+    auto iter5 = [&]() -> bool {
+        if constexpr (NS == 6) return iter(IC<5>{});
+        else return true;
+    };
+    while (iter(IC<0>{}) && iter(IC<1>{}) && iter(IC<2>{}) && iter(IC<3>{}) && iter(IC<4>{}) && iter5()) {
     }
-    // drain: no transfer may still be writing LDS when the workgroup exits
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// Workgroups for the persistent schedule: a multiple of 8 (one share per
-// XCD), at most `per_cu` per compute unit.
-int persistent_grid(int ntiles, int per_cu) {
+// four waves of 128 channels x 64 tokens: 128 channels x 256 tokens per
+// workgroup, two workgroups per compute unit
+using TCfg = Tile<1, 4, 4, 2, 2>;
+
+int device_cus() {
     static int cus = 0;
     if (cus == 0) {
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
     }
-    const int g = min(ntiles, cus * per_cu);
-    return max(8, (g + 7) / 8 * 8);
+    return cus;
 }
 
-template <class C, bool I32OUT, bool RAGGED>
-hipError_t launch_cfg(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
-                      const uint16_t *bias, int64_t M, int64_t N, int K, void *Y,
-                      int64_t ldy, hipStream_t stream) {
-    const int tiles_m = (int)((M + C::BM - 1) / C::BM);
-    const int tiles_n = (int)((N + C::BN - 1) / C::BN);
-    const int grid = persistent_grid(tiles_m * tiles_n, C::WGS);
-    hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED>), dim3((unsigned)grid), dim3(C::NT),
-                       0, stream, Xq, xs, Wq, ws, bias, (int)M, (int)N, K, Y, ldy, tiles_m,
-                       tiles_n);
+// Persistent grid: the workgroups that fit on the chip at once, a multiple of
+// 8 (one equal share per XCD).
+int full_grid() { return (device_cus() * TCfg::WGS + 7) / 8 * 8; }
+
+// Splitting the last rounds along k costs each split tile a partial write and
+// read per contributing workgroup (a few microseconds of latency on the
+// critical path), so it is used only when it saves more than that: at least
+// kSplitMinSaved k-stages per workgroup and a sixth of the whole-tile
+// schedule, with shares of at least kSplitMinShare stages (a tile is then
+// summed from at most nks / kSplitMinShare + 1 pieces).
+constexpr int kSplitMinSaved = 16;
+constexpr int kSplitMinShare = 8;
+
+template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
+    const int ntiles = g.tiles_m * g.tiles_n, nks = g.K >> 6;
+    int grid = full_grid();
+    g.dp = ntiles;
+    g.sk = 0;
+    if (may_split && ntiles % grid != 0) {
+        // whole tiles for all but the last one or two rounds; the rest is
+        // spread over every workgroup in k-stage units (1 to 2 tiles each)
+        const int dp = max(0, ntiles / grid - 1) * grid;
+        const int64_t whole = (int64_t)((ntiles + grid - 1) / grid) * nks;
+        const int64_t split = (int64_t)(dp / grid) * nks + ((int64_t)(ntiles - dp) * nks + grid - 1) / grid;
+        const bool share_ok = (int64_t)(ntiles - dp) * nks >= (int64_t)kSplitMinShare * grid;
+        if (share_ok && whole - split > kSplitMinSaved && 6 * (whole - split) > whole) {
+            g.dp = dp;
+            g.sk = (ntiles - dp) * nks;
+        }
+    }
+    if (g.sk == 0) grid = max(8, (min(ntiles, grid) + 7) / 8 * 8);
+    hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS>), dim3((unsigned)grid), dim3(C::NT), 0, stream, g);
     return hipGetLastError();
-}
-
-// 8 waves of 128 channels x 64 tokens; one workgroup per compute unit
-using T256x256 = Tile<2, 4, 4, 2, 1>;
-
-template <bool I32OUT>
-hipError_t launch_shape(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
-                        const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
-                        hipStream_t stream) {
-    if (N % 16 != 0)  // a ragged channel edge needs element-wise stores
-        return launch_cfg<T256x256, I32OUT, true>(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, stream);
-    return launch_cfg<T256x256, I32OUT, false>(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, stream);
 }
 
 }  // namespace
 
-hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
-                       const float *ws, const uint16_t *bias, int64_t M, int64_t N,
-                       int K, void *Y, int64_t ldy, bool i32out, hipStream_t stream) {
-    return i32out ? launch_shape<true>(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, stream)
-                  : launch_shape<false>(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, stream);
+size_t gemm_workspace_bytes() {
+    const size_t G = (size_t)full_grid();
+    return G * TCfg::NW * sizeof(int) + G * TCfg::PART_INTS * sizeof(int32_t);
+}
+
+hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                       const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
+                       bool i32out, void *workspace, hipStream_t stream) {
+    GemmArgs g{};
+    g.Xq = Xq;
+    g.xs = xs;
+    g.Wq = Wq;
+    g.ws = ws;
+    g.bias = bias;
+    g.Y = Y;
+    g.ldy = ldy;
+    g.M = (int)M;
+    g.N = (int)N;
+    g.K = K;
+    g.tiles_m = (int)((M + TCfg::BM - 1) / TCfg::BM);
+    g.tiles_n = (int)((N + TCfg::BN - 1) / TCfg::BN);
+    const size_t G = (size_t)full_grid();
+    g.flags = reinterpret_cast<int *>(workspace);
+    g.part = workspace ? reinterpret_cast<int32_t *>(reinterpret_cast<uint8_t *>(workspace) + G * TCfg::NW * sizeof(int))
+                       : nullptr;
+    const bool may_split = workspace != nullptr;
+    // ragged channel edges, and biases not 4-byte aligned (the fast path
+    // moves them in channel pairs), use element-wise epilogue accesses
+    const bool ragged = N % 16 != 0 || (bias && reinterpret_cast<uintptr_t>(bias) % 4 != 0);
+    if (i32out)
+        return ragged ? launch_cfg<TCfg, true, true, false>(g, may_split, stream)
+                      : launch_cfg<TCfg, true, false, false>(g, may_split, stream);
+    if (ragged)
+        return bias ? launch_cfg<TCfg, false, true, true>(g, may_split, stream)
+                    : launch_cfg<TCfg, false, true, false>(g, may_split, stream);
+    return bias ? launch_cfg<TCfg, false, false, true>(g, may_split, stream)
+                : launch_cfg<TCfg, false, false, false>(g, may_split, stream);
 }
 
 }  // namespace clq

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "clq.h")
 LIB = os.path.join(ROOT, "paper_2509_24416_amd", "libclq.so")
 
-OK, NULL, SHAPE, BLOCK, ALIGN, ARG, HIP = range(7)
+OK, NULL, SHAPE, BLOCK, ALIGN, ARG, HIP, WORKSPACE = range(8)
 
 
 def declared_functions():
@@ -40,15 +40,17 @@ def lib():
     L.clq_unswizzle_act.argtypes = [p, i64, i64, p, p]
     L.clq_quantize_weights.argtypes = [p, p, i64, i64, i32, f32, p, p, p]
     L.clq_rotate_quant_act.argtypes = [p, i64, p, i64, i64, i32, p, p, p]
-    L.clq_w4a4_linear.argtypes = [p, p, p, p, p, i64, i64, i64, p, i64, p]
-    L.clq_w4a4_accum_i32.argtypes = [p, p, i64, i64, i64, p, i64, p]
+    L.clq_w4a4_workspace_bytes.restype = ctypes.c_size_t
+    L.clq_w4a4_workspace_bytes.argtypes = []
+    L.clq_w4a4_linear.argtypes = [p, p, p, p, p, i64, i64, i64, p, i64, p, ctypes.c_size_t, p]
+    L.clq_w4a4_accum_i32.argtypes = [p, p, i64, i64, i64, p, i64, p, ctypes.c_size_t, p]
     L.clq_unswizzle_weights.argtypes = [p, i64, i64, p, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 10, names
+    assert len(names) == 11, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -60,8 +62,8 @@ def test_binding_names_match_header():
 
 
 def test_version_and_strings(lib):
-    assert lib.clq_version() == 2
-    for code in range(7):
+    assert lib.clq_version() == 3
+    for code in range(8):
         s = lib.clq_status_string(code).decode()
         assert s.startswith("CLQ")
     assert b"unknown" in lib.clq_status_string(99)
@@ -126,8 +128,8 @@ def test_quantize_weights_validation(lib):
     assert qw(lib, Wq=A + 4) == ALIGN
 
 
-def lin(lib, Xq=A, xs=A, Wq=A, ws=A, bias=None, M=4, N=8, K=1152, Y=A, ldy=8):
-    return lib.clq_w4a4_linear(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, None)
+def lin(lib, Xq=A, xs=A, Wq=A, ws=A, bias=None, M=4, N=8, K=1152, Y=A, ldy=8, wsp=None, wsb=0):
+    return lib.clq_w4a4_linear(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, wsp, wsb, None)
 
 
 def test_linear_validation(lib):
@@ -144,14 +146,28 @@ def test_linear_validation(lib):
     assert lin(lib, Y=A + 8) == ALIGN
     assert lin(lib, Xq=MIS) == ALIGN
     assert lin(lib, bias=A + 1) == ALIGN
+    need = lib.clq_w4a4_workspace_bytes()
+    assert need > 0
+    assert lin(lib, wsp=A, wsb=need - 1) == WORKSPACE
+    assert lin(lib, wsp=A + 8, wsb=need) == ALIGN
+    assert lin(lib, Xq=None, wsp=A, wsb=need) == NULL          # checks stay in order
+
+
+def test_workspace_bytes(lib):
+    # one partial tile (128 x 256 int32) and four flags per workgroup, two
+    # workgroups per compute unit, the grid a multiple of 8
+    n = lib.clq_w4a4_workspace_bytes()
+    per_wg = 128 * 256 * 4 + 4 * 4
+    assert n % per_wg == 0 and (n // per_wg) % 8 == 0
 
 
 def test_accum_and_unswizzle_validation(lib):
     f = lib.clq_w4a4_accum_i32
-    assert f(None, A, 4, 8, 1152, A, 8, None) == NULL
-    assert f(A, A, 4, 8, 1152, A, 6, None) == SHAPE      # ldacc % 4 != 0
-    assert f(A, A, 4, 8, 1152, A, 4, None) == SHAPE      # ldacc < N
-    assert f(A, A, 4, 8, 1152, A + 4, 8, None) == ALIGN
+    assert f(None, A, 4, 8, 1152, A, 8, None, 0, None) == NULL
+    assert f(A, A, 4, 8, 1152, A, 6, None, 0, None) == SHAPE      # ldacc % 4 != 0
+    assert f(A, A, 4, 8, 1152, A, 4, None, 0, None) == SHAPE      # ldacc < N
+    assert f(A, A, 4, 8, 1152, A + 4, 8, None, 0, None) == ALIGN
+    assert f(A, A, 4, 8, 1152, A, 8, A, 16, None) == WORKSPACE
     g = lib.clq_unswizzle_weights
     assert g(None, 8, 1152, A, None) == NULL
     assert g(A, 0, 1152, A, None) == SHAPE

@@ -133,16 +133,41 @@ GEMM_SHAPES = [(1, 1, 64), (7, 8, 128), (129, 72, 192), (257, 200, 1152), (64, 1
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
-def test_accum_i32_bitexact(clq, M, N, K):
+@pytest.mark.parametrize("workspace", [None, False], ids=["ws", "nows"])
+def test_accum_i32_bitexact(clq, M, N, K, workspace):
     block = 64
     X = workloads.activations(M, K, "L1", seed=M)
     W = workloads.weights(N, K, seed=N)
     qw = clq.clq_quantize_weights(dev(W), block)
     Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
-    acc = clq.clq_w4a4_accum_i32(Xq, xs, qw)
+    acc = clq.clq_w4a4_accum_i32(Xq, xs, qw, workspace=workspace)
     _, xc, _ = oracle.quantize_act(X, block)
     _, wc, _ = oracle.quantize_weights(W, block)
     assert np.array_equal(host(acc), oracle.gemm_i32(xc, wc))
+
+
+# Shapes whose last tile round is split along k over every workgroup (few
+# tiles, long k): each tile is summed from the partials of many workgroups.
+SPLIT_SHAPES = [(2048, 1152, 4608), (2000, 1000, 4608), (2048, 640, 8192)]
+
+
+@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
+def test_split_k_exact_and_repeatable(clq, M, N, K):
+    block = 64
+    X = workloads.activations(M, K, "L1", seed=M + 7)
+    W = workloads.weights(N, K, seed=N + 7)
+    b = workloads.bias(N, seed=8)
+    qw = clq.clq_quantize_weights(dev(W), block)
+    Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
+    ref = oracle.linear(X, W, b, block)
+    ws = torch.zeros(clq.clq_w4a4_workspace_bytes(), dtype=torch.uint8, device="cuda")
+    for rep in range(3):          # the workspace is left ready for the next call
+        acc = clq.clq_w4a4_accum_i32(Xq, xs, qw, workspace=ws)
+        assert np.array_equal(host(acc), ref["acc"]), rep
+        Y = clq.clq_w4a4_linear(Xq, xs, qw, dev(b), workspace=ws)
+        assert oracle.err_metric(host(Y).astype(np.float64), ref["y64"], ref["p64"], b) <= TOL, rep
+    groups = clq.clq_w4a4_workspace_bytes() // (128 * 256 * 4 + 4 * 4)
+    assert not host(ws[:groups * 4 * 4]).any()     # every flag back at zero
 
 
 def test_accum_i32_extremes(clq):
