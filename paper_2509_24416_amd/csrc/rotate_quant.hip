@@ -7,6 +7,9 @@
 // n = 4, dynamically per token for activations and once per output channel
 // for weights.
 //
+// Weights (offline) use a one-shot kernel; activations use a persistent,
+// software-pipelined variant of the same per-block arithmetic (below).
+//
 // One workgroup handles R whole rows.  The rows are first copied into LDS
 // with coalesced 16-byte loads (each 16-byte chunk of a Hadamard block lands
 // in an XOR-swizzled slot so that the later per-lane block reads hit distinct
@@ -24,6 +27,8 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <algorithm>
 
 #include "clq_internal.h"
 
@@ -196,6 +201,152 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
     }
 }
 
+// Activation path: persistent, software-pipelined over batches of R rows.
+// Batch i's rows are converted and transformed from one LDS buffer while
+// batch i+1 (already in registers) is written to the other buffer and batch
+// i+2's loads are in flight, so HBM never waits for the arithmetic.  One
+// barrier per batch: before it, block maxima meet in rowmax[i % 3]; after it,
+// codes are formed and stored.  The third rowmax buffer is cleared one batch
+// after its use, when no lane can still be reading it.
+template <int B>
+__global__ void __launch_bounds__(256)
+rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__restrict__ perm,
+              int64_t rows_valid, int64_t rows_alloc, int64_t nbatch, int K, int R,
+              uint8_t *__restrict__ out, float *__restrict__ scale_out)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int CPB = B / 8;
+    constexpr int LPT = CPB;   // chunks each lane loads per batch (T >= R * nb lanes)
+    const int cpr = K >> 3;
+    const int nb = K / B;
+    const int chunks = R * cpr;
+    uint4 *tile0 = reinterpret_cast<uint4 *>(smem);
+    uint4 *tile1 = tile0 + chunks;
+    unsigned *rowmax = reinterpret_cast<unsigned *>(tile1 + chunks);   // [3][R]
+
+    const int t = threadIdx.x, T = blockDim.x;
+    const int64_t G = gridDim.x;
+
+    // this lane's load chunks (the same for every batch): row, source
+    // offset within the batch, swizzled LDS slot
+    int lrow[LPT], lsrc[LPT], lslot[LPT];
+#pragma unroll
+    for (int k = 0; k < LPT; ++k) {
+        const int c = t + k * T;
+        const int r = c / cpr, cc = c - r * cpr;
+        lrow[k] = c < chunks ? r : -1;
+        lsrc[k] = r * (int)ldx + cc * 8;
+        const int jj = cc / CPB, ii = cc - jj * CPB;
+        lslot[k] = r * cpr + jj * CPB + chunk_slot<B>(ii, jj);
+    }
+    uint4 ld[LPT];
+    auto load = [&](int64_t batch) {
+        const int64_t row0 = batch * R;
+        const uint16_t *base = X + row0 * ldx;
+#pragma unroll
+        for (int k = 0; k < LPT; ++k) {
+            ld[k] = make_uint4(0u, 0u, 0u, 0u);
+            if (lrow[k] >= 0 && row0 + lrow[k] < rows_valid)
+                ld[k] = *reinterpret_cast<const uint4 *>(base + lsrc[k]);
+        }
+    };
+    auto stash = [&](uint4 *tile) {
+#pragma unroll
+        for (int k = 0; k < LPT; ++k)
+            if (lrow[k] >= 0) tile[lslot[k]] = ld[k];
+    };
+
+    const int r = t / nb, j = t - r * nb;
+    const bool active = r < R;
+    int64_t b = blockIdx.x;
+    if (b >= nbatch) return;
+    for (int q = t; q < 3 * R; q += T) rowmax[q] = 0u;
+    load(b);
+    stash(tile0);
+    if (b + G < nbatch) load(b + G);
+    __syncthreads();
+
+    for (int i = 0; b < nbatch; ++i, b += G) {
+        const uint4 *tcur = (i & 1) ? tile1 : tile0;
+        uint4 *tnxt = (i & 1) ? tile0 : tile1;
+        unsigned *rm = rowmax + (i % 3) * R;
+
+        // 1. one Hadamard block per lane, fp32, stage order h = 1, 2, ..., b/2
+        float x[B];
+        if (active) {
+            float bmax = 0.0f;
+            if (perm == nullptr) {
+                const uint4 *src = tcur + r * cpr + j * CPB;
+#pragma unroll
+                for (int ii = 0; ii < CPB; ++ii) {
+                    const uint4 v = src[chunk_slot<B>(ii, j)];
+                    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float u = half_lo(w[e]), s = half_hi(w[e]);
+                        x[8 * ii + 2 * e] = u + s;       // stage h = 1
+                        x[8 * ii + 2 * e + 1] = u - s;
+                    }
+                }
+            } else {
+                const uint16_t *rowh = reinterpret_cast<const uint16_t *>(tcur + r * cpr);
+                const int32_t *p = perm + j * B;
+#pragma unroll
+                for (int e = 0; e < B; e += 2) {
+                    const int k0 = p[e], k1 = p[e + 1];
+                    const int c0 = k0 >> 3, c1 = k1 >> 3;
+                    const int s0 = (c0 / CPB) * CPB + chunk_slot<B>(c0 % CPB, c0 / CPB);
+                    const int s1 = (c1 / CPB) * CPB + chunk_slot<B>(c1 % CPB, c1 / CPB);
+                    const float u = __half2float(__ushort_as_half(rowh[s0 * 8 + (k0 & 7)]));
+                    const float s = __half2float(__ushort_as_half(rowh[s1 * 8 + (k1 & 7)]));
+                    x[e] = u + s;
+                    x[e + 1] = u - s;
+                }
+            }
+#pragma unroll
+            for (int h = 2; h < B; h <<= 1) {
+#pragma unroll
+                for (int ii = 0; ii < B; ++ii) {
+                    if ((ii & h) == 0) {
+                        const float u = x[ii], v = x[ii + h];
+                        x[ii] = u + v;
+                        x[ii + h] = u - v;
+                    }
+                }
+            }
+#pragma unroll
+            for (int ii = 0; ii < B; ii += 2) bmax = fmaxf(bmax, fmaxf(fabsf(x[ii]), fabsf(x[ii + 1])));
+            atomicMax(&rm[r], __float_as_uint(bmax));
+        }
+        // 2. the next batch into the other buffer, the one after into registers
+        if (b + G < nbatch) stash(tnxt);
+        if (b + 2 * G < nbatch) load(b + 2 * G);
+        __syncthreads();
+        // 3. codes of this batch; the rowmax buffer of the previous batch is free
+        if (t < R) rowmax[((i + 2) % 3) * R + t] = 0u;
+        if (!active) continue;
+        const float a = __uint_as_float(rm[r]);
+        const float rc = (a == 0.0f) ? 0.0f : 7.0f / a;
+        const int64_t grow = b * R + r;
+        if (grow >= rows_alloc) continue;   // past the padded rows
+        if (j == 0 && grow < rows_valid) scale_out[grow] = a / 7.0f;
+        uint32_t words[B / 8];
+#pragma unroll
+        for (int g = 0; g < B / 8; ++g) {
+            uint32_t w[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) w[e] = __float_as_uint(__builtin_fmaf(x[8 * g + e], rc, kMagic));
+            words[g] = pack8(w);
+        }
+#pragma unroll
+        for (int c = 0; c < B / 32; ++c) {
+            const int64_t c32 = (int64_t)j * (B / 32) + c;
+            *reinterpret_cast<uint4 *>(out + xq_chunk_offset(grow, c32, K)) =
+                make_uint4(words[4 * c], words[4 * c + 1], words[4 * c + 2], words[4 * c + 3]);
+        }
+    }
+}
+
 // Rows per workgroup: the largest lane utilisation R*nb / roundup(R*nb, 64)
 // with at most 512 lanes (unless one row alone needs more) and at most 64 KB
 // of staged fp16 rows.
@@ -235,6 +386,52 @@ hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
     return hipGetLastError();
 }
 
+// Activation batches: the largest lane utilisation R*nb / roundup(R*nb, 64)
+// with at most 256 lanes and two staged batches within 64 KB of LDS.
+int pick_act_rows(int K, int block) {
+    const int nb = K / block;
+    int best = 1;
+    double best_u = -1.0;
+    for (int R = 1; R * nb <= 256; ++R) {
+        if ((size_t)2 * R * K * 2 > 65536) break;
+        const int T = (R * nb + 63) / 64 * 64;
+        const double u = (double)(R * nb) / T;
+        if (u > best_u + 1e-9) { best_u = u; best = R; }
+    }
+    return best;
+}
+
+template <int B>
+hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, int64_t rows_valid,
+                         int64_t rows_alloc, int K, uint8_t *out, float *scale, hipStream_t stream) {
+    const int R = pick_act_rows(K, B);
+    const int nb = K / B;
+    const int T = (R * nb + 63) / 64 * 64;
+    const size_t lds = (size_t)2 * R * K * 2 + (size_t)3 * R * 4;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void *)rq_act_kernel<B>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 65536 + 4096);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+    }
+    if ((int64_t)R * ldx > INT32_MAX)   // 32-bit in-batch offsets: very wide strides take the one-shot kernel
+        return launch_rq<B, false>(X, ldx, perm, rows_valid, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
+    const int64_t nbatch = (rows_alloc + R - 1) / R;
+    const int per_cu = (int)std::min<size_t>(4, (160 * 1024) / lds);
+    const int64_t grid = std::min<int64_t>(nbatch, (int64_t)cus * per_cu);
+    hipLaunchKernelGGL((rq_act_kernel<B>), dim3((unsigned)grid), dim3(T), lds, stream, X, ldx, perm,
+                       rows_valid, rows_alloc, nbatch, K, R, out, scale);
+    return hipGetLastError();
+}
+
 __global__ void unswizzle_kernel(const uint8_t *__restrict__ Wq, int64_t N, int K,
                                  uint8_t *__restrict__ out) {
     const int64_t kgs = K / 16;
@@ -269,9 +466,9 @@ hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *pe
         }
     } else {
         switch (block) {
-            case 32: return launch_rq<32, false>(X, ldx, perm, rows, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
-            case 64: return launch_rq<64, false>(X, ldx, perm, rows, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
-            case 128: return launch_rq<128, false>(X, ldx, perm, rows, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
+            case 32: return launch_rq_act<32>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
+            case 64: return launch_rq_act<64>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
+            case 128: return launch_rq_act<128>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
         }
     }
     return hipErrorInvalidValue;
