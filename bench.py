@@ -11,7 +11,9 @@ Prints ONE JSON line:
   value      effective TOPS of the step = sum(2 M N K) / step time
   roofline   the GEMM kernel (dominant): algorithmic int8-MFMA ops per launch
              / average launch time (HIP events on the launch stream), against
-             the dense int8 peak (5.0 POP/s)
+             the dense int8 peak (5.0 POP/s); traffic = HBM bytes per launch
+             from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary when
+             it was taken on the current kernel sources, else null
   rotate_quant  algorithmic bytes per launch / average launch time, against
              HBM (8 TB/s), measured in the same timed loop, and separately
              with the 256 MB Infinity Cache flushed before every launch
@@ -109,7 +111,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--cold-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -241,12 +243,12 @@ def main():
                    "block": 64, "layers": {l.name.split(".")[1]: [l.K, l.N] for l in layers},
                    "parallelism": "none (one GPU)"},
         "pct_int8_peak": round(100 * value / INT8_PEAK_TOPS, 2),
-        "roofline": {"kernel": "w4a4_gemm_kernel", "bound": "mfma", "achieved": round(achieved, 1),
+        "roofline": {"kernel": "w4a4_gemm_kernel (128 ch x 256 tok tiles, 2 per CU)", "bound": "mfma", "achieved": round(achieved, 1),
                      "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / INT8_PEAK_TOPS, 4),
                      "traffic": traffic, "avg_launch_us": round(gemm_avg_ms * 1e3, 2),
                      "ops_per_launch": gemm_ops_per_launch},
-        "rotate_quant": {"kernel": "rotate_quant_kernel<64>", "bound": "hbm",
+        "rotate_quant": {"kernel": "rq_act_kernel<64>", "bound": "hbm",
                          "achieved": round(rq_achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": round(rq_achieved / HBM_PEAK_GBPS, 4),
                          "avg_launch_us": round(float(rq_ms.mean()) * 1e3, 2),
