@@ -17,7 +17,8 @@
 // lane l's 16 bytes at 16*l) per 32 channels and per 32 tokens of the tile.
 // Units go from global memory straight into LDS (global_load_lds_dwordx4: no
 // registers, no VALU) through a ring of kStages stages kept kStages - 1 ahead
-// of the matrix cores.  Each wave reads its units back with one 16-byte LDS
+// of the matrix cores; the epilogue operands of a tile (scales, biases) go
+// once per tile, with its first stage, into a small ring of their own.  Each wave reads its units back with one 16-byte LDS
 // read per lane and widens them to int8 in registers.  Widening keeps each
 // nibble in the high half of its byte, so the int8 holds 16*q exactly; the
 // int32 accumulator holds 256 * sum(qa*qw) (|.| <= 256*49*K < 2^31) and the
@@ -25,9 +26,11 @@
 // order inside a 32-code slice is permuted identically for both operands,
 // which leaves the dot product unchanged.
 //
-// Synchronisation.  Every iteration issues the same number of memory
-// instructions per wave, so "stage s has landed" is a fixed s_waitcnt vmcnt
-// count, emitted with the workgroup barrier as one asm statement.  The ring
+// Synchronisation.  Vector-memory operations complete in issue order, so
+// "stage s has landed" is an s_waitcnt vmcnt count of the transfers issued
+// after it (one of three immediates, depending on whether the last two
+// productions carried epilogue operands), emitted with the workgroup barrier
+// as one asm statement.  The ring
 // stages are separate LDS arrays and the loop is unrolled over them, so each
 // stage index is a compile-time constant; the LDS reads of operands and
 // epilogue values are asm too, each followed by an explicit lgkmcnt wait,
@@ -135,12 +138,17 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
     constexpr bool BIAS_CH = BIAS && !RAGGED && !I32OUT;
     constexpr int E_CH = I32OUT ? 0 : C::XS_CH + C::WS_CH + (BIAS_CH ? C::B_CH : 0);
     constexpr int EPW = (E_CH + C::NW - 1) / C::NW;
-    constexpr int VPI = C::UPW + EPW;
-    constexpr int E_XS = C::STAGE_BYTES, E_WS = E_XS + C::BM * 4, E_B = E_WS + C::BN * 4;
-    constexpr int SLOT = I32OUT ? C::STAGE_BYTES : E_B + (BIAS_CH ? C::BN * 2 : 0);
+    // epilogue operands of a segment (token scales fp32 [BM], channel scales
+    // fp32 [BN], bias fp16 [BN]) travel once per segment into their own ring
+    // of NS entries indexed by segment number: the producer runs at most
+    // NS - 1 stages, hence NS - 1 segments, ahead of the consumer
+    constexpr int E_XS = 0, E_WS = E_XS + C::BM * 4, E_B = E_WS + C::BN * 4;
+    constexpr int E_BYTES = I32OUT ? 16 : E_B + (BIAS_CH ? C::BN * 2 : 0);
+    constexpr int SLOT = C::STAGE_BYTES;
     static_assert(NS == 5 || NS == 6, "ring arrays below");
     __shared__ __align__(16) uint8_t ring0[SLOT], ring1[SLOT], ring2[SLOT], ring3[SLOT], ring4[SLOT];
     __shared__ __align__(16) uint8_t ring5[NS == 6 ? SLOT : 16];
+    __shared__ __align__(16) uint8_t ebuf[NS][E_BYTES];
     auto slot = [&](auto qc) -> uint8_t * {
         constexpr int q = decltype(qc)::value;
         if constexpr (q == 0) return ring0;
@@ -234,7 +242,21 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
         }
     };
     p_setup();
+    int e_next = 0;          // stage whose production carries the next segment's operands
+    unsigned phist = 0;      // 1 bit per production call: epilogue operands issued
     auto produce = [&](auto qc) {
+        // the segment's epilogue operands go out with its first stage,
+        // ahead of the units (the wait counts below rely on that order)
+        int e_now = 0;
+        if (EPW > 0 && pc.k == pc.kb && p_s == e_next) {
+            uint8_t *ed = &ebuf[pc.j % NS][0];
+#pragma unroll
+            for (int j = 0; j < EPW; ++j)
+                __builtin_amdgcn_global_load_lds(esrc[j], (CLQ_LDS void *)(ed + edst[j]), 4, 0, 0);
+            e_now = 1;
+            e_next = -1;
+        }
+        phist = (phist << 1) | e_now;
         uint8_t *dst = slot(qc);
         const uint32_t voff = (uint32_t)(pc.k * 1024 + lane * 16);
 #pragma unroll
@@ -243,14 +265,12 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
             const uint8_t *sp = usrc[j] + voff;
             __builtin_amdgcn_global_load_lds(sp, (CLQ_LDS void *)(dst + (wave * C::UPW + j) * 1024), 16, 0, 0);
         }
-#pragma unroll
-        for (int j = 0; j < EPW; ++j)
-            __builtin_amdgcn_global_load_lds(esrc[j], (CLQ_LDS void *)(dst + edst[j]), 4, 0, 0);
         if (p_s < total - 1) {
             ++p_s;
             if (++pc.k == pc.ke) {
                 next_seg(pc);
                 p_setup();
+                e_next = p_s;
             }
         }
     };
@@ -397,13 +417,13 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
     const int h16 = (lane >> 5) * 16;
     // The epilogue operands are read with asm too (same reason as the
     // operand units); one explicit wait per channel fragment orders their use.
-    auto epilogue = [&](int L, auto qc) {
+    auto epilogue = [&](int L, int sj, auto qc) {
         int tm, tn;
         coords(L, tm, tn);
         uint32_t lx = (uint32_t)((wm * C::FM * 32 + (lane & 31)) * 4);
         uint32_t lw = (uint32_t)((wn * C::FN * 32 + h16) * 4);
         asm volatile("" : "+v"(lx), "+v"(lw));
-        const uint32_t sb = lds_addr(slot(qc));
+        const uint32_t sb = lds_addr(&ebuf[0][0]) + (uint32_t)((sj % NS) * E_BYTES);
         const uint32_t axs = sb + E_XS + lx, aws = sb + E_WS + lw, ab = sb + E_B + lw / 2;
         float xsm[C::FM];
         int mrow[C::FM];
@@ -508,13 +528,29 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
         });
     };
 
+    // Stage s+1 has landed once at most the VMEM instructions issued after
+    // its last transfer are outstanding (completion is in issue order): the
+    // NS-3 later productions, with their epilogue operand transfers if any
+    // (operands precede a production's units, so only the last NS-3 calls
+    // count).  Epilogue stores are not counted, which only makes the wait
+    // stricter.
+    static_assert(NS == 5, "two-call history below");
+    constexpr int W0 = (NS - 3) * C::UPW;
+    auto landed_wait = [&]() {
+        switch (__builtin_popcount(phist & 3u)) {
+            case 0: asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W0) : "memory"); break;
+            case 1: asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W0 + EPW) : "memory"); break;
+            default: asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W0 + 2 * EPW) : "memory"); break;
+        }
+    };
+
     // ---- pipeline ---------------------------------------------------------------
     produce(IC<0>{});
     produce(IC<1>{});
     produce(IC<2>{});
     produce(IC<3>{});
     if constexpr (NS == 6) produce(IC<4>{});
-    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((NS - 3) * VPI) : "memory");
+    landed_wait();
     read_packed(IC<0>{});
     operands_ready();
     widen_half0();
@@ -529,7 +565,7 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
         constexpr int q = decltype(qc)::value;
         constexpr IC<(q + 1) % NS> nqc{};
         constexpr IC<(q + NS - 1) % NS> pqc{};
-        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 3) * VPI) : "memory");
+        landed_wait();
         produce(pqc);
         __builtin_amdgcn_sched_barrier(0);
         widen_half1();
@@ -547,7 +583,7 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
                 contribute();
             } else {
                 if (cc.ke != nks) fixup(cc.L);
-                epilogue(cc.L, qc);
+                epilogue(cc.L, cc.j, qc);
             }
             zero_acc();
             if (s + 1 < total) next_seg(cc);
