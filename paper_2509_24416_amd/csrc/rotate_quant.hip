@@ -46,6 +46,20 @@ __device__ __forceinline__ int chunk_slot(int i, int j) {
     else return i ^ (j & 7);
 }
 
+// Activation kernel lane order: for b >= 64 lane t owns block j = t / R of
+// row r = t % R (rows fastest), so that the code stores of consecutive lanes
+// land side by side in the tiled code layout; the eight lanes reading chunk
+// i together then differ in j * R + r, which picks the XOR key.  For b = 32
+// lanes stay blocks-fastest with the shared slot rule.
+template <int B>
+constexpr bool rows_fastest() { return B >= 64; }
+
+template <int B>
+__device__ __forceinline__ int act_slot(int i, int j, int r, int R) {
+    if constexpr (rows_fastest<B>()) return i ^ ((j * R + r) & 7);
+    else return chunk_slot<B>(i, j);
+}
+
 __device__ __forceinline__ float half_lo(uint32_t w) {
     return __half2float(__ushort_as_half((unsigned short)(w & 0xffffu)));
 }
@@ -237,7 +251,7 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
         lrow[k] = c < chunks ? r : -1;
         lsrc[k] = r * (int)ldx + cc * 8;
         const int jj = cc / CPB, ii = cc - jj * CPB;
-        lslot[k] = r * cpr + jj * CPB + chunk_slot<B>(ii, jj);
+        lslot[k] = r * cpr + jj * CPB + act_slot<B>(ii, jj, r, R);
     }
     uint4 ld[LPT];
     auto load = [&](int64_t batch) {
@@ -256,8 +270,15 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
             if (lrow[k] >= 0) tile[lslot[k]] = ld[k];
     };
 
-    const int r = t / nb, j = t - r * nb;
-    const bool active = r < R;
+    int r, j;
+    if constexpr (rows_fastest<B>()) {
+        j = t / R;
+        r = t - j * R;
+    } else {
+        r = t / nb;
+        j = t - r * nb;
+    }
+    const bool active = rows_fastest<B>() ? j < nb : r < R;
     int64_t b = blockIdx.x;
     if (b >= nbatch) return;
     for (int q = t; q < 3 * R; q += T) rowmax[q] = 0u;
@@ -279,7 +300,7 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
                 const uint4 *src = tcur + r * cpr + j * CPB;
 #pragma unroll
                 for (int ii = 0; ii < CPB; ++ii) {
-                    const uint4 v = src[chunk_slot<B>(ii, j)];
+                    const uint4 v = src[act_slot<B>(ii, j, r, R)];
                     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -295,8 +316,8 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
                 for (int e = 0; e < B; e += 2) {
                     const int k0 = p[e], k1 = p[e + 1];
                     const int c0 = k0 >> 3, c1 = k1 >> 3;
-                    const int s0 = (c0 / CPB) * CPB + chunk_slot<B>(c0 % CPB, c0 / CPB);
-                    const int s1 = (c1 / CPB) * CPB + chunk_slot<B>(c1 % CPB, c1 / CPB);
+                    const int s0 = (c0 / CPB) * CPB + act_slot<B>(c0 % CPB, c0 / CPB, r, R);
+                    const int s1 = (c1 / CPB) * CPB + act_slot<B>(c1 % CPB, c1 / CPB, r, R);
                     const float u = __half2float(__ushort_as_half(rowh[s0 * 8 + (k0 & 7)]));
                     const float s = __half2float(__ushort_as_half(rowh[s1 * 8 + (k1 & 7)]));
                     x[e] = u + s;
