@@ -106,6 +106,35 @@ def bias(N, seed=2):
     return (np.float32(0.1) * rng.standard_normal(N, dtype=np.float32)).astype(np.float16)
 
 
+def calibration(B, N, D, law="L1", seed=0):
+    """fp16 [B][N][D] calibration activations for the OBS derivation: the
+    outlier channels and their factors are drawn once and shared by every
+    sample and token (the paper observes statistics that are stable along
+    the batch); the Gaussian body (and, for L2, the per-token scale) is drawn
+    per sample."""
+    p = law_params(law)
+    rng = np.random.default_rng(seed)
+    n_out = int(round(p["frac"] * D))
+    ch = rng.choice(D, size=n_out, replace=False) if n_out else np.zeros(0, np.int64)
+    fac = np.exp(rng.uniform(np.log(p["lo"]), np.log(p["hi"]), size=n_out)).astype(np.float32)
+    out = np.empty((B, N, D), np.float16)
+    for b in range(B):
+        x = rng.standard_normal((N, D), dtype=np.float32)
+        x[:, ch] *= fac[None, :]
+        if p["token_sigma"]:
+            x *= np.exp(p["token_sigma"] * rng.standard_normal(N, dtype=np.float32))[:, None]
+        out[b] = x.astype(np.float16)
+    return out
+
+
+def calibration_outliers(D, law="L1", seed=0):
+    """The planted outlier channels of calibration(B, N, D, law, seed)."""
+    p = law_params(law)
+    rng = np.random.default_rng(seed)
+    n_out = int(round(p["frac"] * D))
+    return np.sort(rng.choice(D, size=n_out, replace=False)) if n_out else np.zeros(0, np.int64)
+
+
 def random_perm(K, seed=3):
     """A seeded gather vector s (a permutation of 0..K-1) for tests of the
     optional column swap."""
