@@ -58,9 +58,9 @@ typedef enum {
     CLQ_ERR_SHAPE = 2, /* M, N, K, ld* out of range or not multiples         */
     CLQ_ERR_BLOCK = 3, /* block not in {32, 64, 128} or K % block != 0       */
     CLQ_ERR_ALIGN = 4, /* a pointer is not aligned as required               */
-    CLQ_ERR_ARG = 5,   /* clip_ratio outside [2^-24, 1]                       */
+    CLQ_ERR_ARG = 5,   /* clip_ratio outside [2^-24, 1], or an unknown metric  */
     CLQ_ERR_HIP = 6,   /* a HIP launch failed (see hipGetLastError)           */
-    CLQ_ERR_WORKSPACE = 7 /* workspace smaller than clq_w4a4_workspace_bytes() */
+    CLQ_ERR_WORKSPACE = 7 /* workspace smaller than the *_workspace_bytes() query */
 } clq_status;
 
 /* Library version; bumps whenever a packed layout (Wq, Xq) or an entry point
@@ -154,6 +154,56 @@ clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K,
  * uint8 [M][K/2] (16-byte aligned), same nibble convention. */
 clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K,
                              void *Xq_canonical, hipStream_t stream);
+
+/* ---- OBS calibration (Sec. 3.3 "Orthogonal-Based Smoothing", outlier
+ * detection; Sec. 4.3 ablation of the outlier metric) ----------------------
+ * Produces the gather vector s (perm) that the entry points above take:
+ * calibration activations are averaged over the batch, each channel gets an
+ * outlier score, and the top-scoring half of the channels moves to the left
+ * half of the columns, each half keeping the channels' original order.
+ * Arithmetic is fp32 and fixed, so scores and s are reproducible bit for
+ * bit: the B samples are added in batch order and the sum divided once by B;
+ * sums over tokens are pairwise (zero-padded to a power of two, upper half
+ * added onto lower half); percentiles are order statistics; ties in the
+ * ranking go to the lower channel index. */
+typedef enum {
+    CLQ_OBS_ABSMAX = 0,     /* max_n |S[n][d]| (the paper's choice)             */
+    CLQ_OBS_RANGE = 1,      /* max_n S - min_n S                                */
+    CLQ_OBS_PAR = 2,        /* max|S| / (pairwise sum |S| / N); 0 if the sum is 0 */
+    CLQ_OBS_TOPK_MEAN = 3,  /* pairwise sum of the k largest |S| (descending) / k,
+                               k = max(1, (N + 50) / 100)                       */
+    CLQ_OBS_PERCENTILE = 4  /* S_(N-1-l) - S_(l), ascending order statistics,
+                               l = (N - 1) / 100 (the 1% and 99% points)         */
+} clq_obs_metric;
+
+/* Workspace bytes clq_obs_channel_scores needs: 8*D for abs-max and range,
+ * 4*N*D (the fp32 mean matrix) for the others, rounded up to 256; 0 for
+ * sizes or a metric out of range. */
+size_t clq_obs_workspace_bytes(int64_t N, int64_t D, int32_t metric);
+
+/* Channel outlier scores of calibration activations.
+ *   X          fp16 [B][N][D]: B samples of N tokens, token row stride ldx
+ *              (elements, >= D, multiple of 8), sample stride N * ldx;
+ *              16-byte aligned.
+ *   B, N, D    B >= 1 (< 2^24), N >= 1, 8 <= D <= 65536 with D % 8 == 0; the
+ *              metrics other than abs-max and range need N <= 32768.
+ *   metric     a clq_obs_metric (else CLQ_ERR_ARG).
+ *   workspace  device memory of at least clq_obs_workspace_bytes(N, D,
+ *              metric), 16-byte aligned; overwritten (no initial contents
+ *              needed).
+ *   scores     out, fp32 [D]. */
+clq_status clq_obs_channel_scores(const void *X, int64_t ldx, int64_t B, int64_t N,
+                                  int64_t D, int32_t metric, void *workspace,
+                                  size_t workspace_bytes, float *scores,
+                                  hipStream_t stream);
+
+/* The gather vector s from channel scores.
+ *   scores  fp32 [D], finite; 2 <= D <= 65536, D even.
+ *   perm    out, int32 [D]: perm[0 .. D/2) are the D/2 highest-ranked
+ *           channels in ascending order, perm[D/2 .. D) the others in
+ *           ascending order (x'[k] = x[perm[k]]). */
+clq_status clq_obs_permutation(const float *scores, int64_t D, int32_t *perm,
+                               hipStream_t stream);
 
 #ifdef __cplusplus
 }

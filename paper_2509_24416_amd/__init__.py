@@ -10,6 +10,8 @@ carry the names of the C entry points declared in ``include/clq.h``:
     clq_w4a4_accum_i32(Xq, x_scale, qw)                        -> acc
     clq_unswizzle_weights(qw)                                  -> canonical codes
     clq_unswizzle_act(Xq, M, K)                                -> canonical codes
+    clq_obs_channel_scores(X, metric="absmax")                 -> scores [D]
+    clq_obs_permutation(scores)                                -> perm [D]
 
 Paper: "CLQ" (arXiv 2509.24416) -- Sec. 3.3 (online block-Hadamard rotation,
 weights absorb it offline) and Sec. 3.1 Eq. (1) (4-bit quantizer; dynamic
@@ -50,13 +52,21 @@ _lib.clq_w4a4_linear.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64,
 _lib.clq_w4a4_accum_i32.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _p, ctypes.c_size_t, _p]
 _lib.clq_unswizzle_weights.argtypes = [_p, _i64, _i64, _p, _p]
 _lib.clq_unswizzle_act.argtypes = [_p, _i64, _i64, _p, _p]
+_lib.clq_obs_workspace_bytes.restype = ctypes.c_size_t
+_lib.clq_obs_workspace_bytes.argtypes = [_i64, _i64, _i32]
+_lib.clq_obs_channel_scores.argtypes = [_p, _i64, _i64, _i64, _i64, _i32, _p, ctypes.c_size_t, _p, _p]
+_lib.clq_obs_permutation.argtypes = [_p, _i64, _p, _p]
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
-           "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act"):
+           "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
+           "clq_obs_channel_scores", "clq_obs_permutation"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
            "clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_workspace_bytes",
-           "clq_w4a4_linear", "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act")
+           "clq_w4a4_linear", "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
+           "clq_obs_workspace_bytes", "clq_obs_channel_scores", "clq_obs_permutation")
+
+OBS_METRICS = ("absmax", "range", "par", "topk_mean", "percentile")
 
 (CLQ_OK, CLQ_ERR_NULL, CLQ_ERR_SHAPE, CLQ_ERR_BLOCK, CLQ_ERR_ALIGN, CLQ_ERR_ARG, CLQ_ERR_HIP,
  CLQ_ERR_WORKSPACE) = range(8)
@@ -254,3 +264,51 @@ def clq_unswizzle_act(Xq, M, K, stream=None):
     out = torch.empty((M, K // 2), dtype=torch.uint8, device=Xq.device)
     _check(_lib.clq_unswizzle_act(_ptr(Xq), M, K, _ptr(out), _stream(stream)), "clq_unswizzle_act")
     return out
+
+
+def clq_obs_workspace_bytes(N, D, metric):
+    return int(_lib.clq_obs_workspace_bytes(N, D, _metric(metric)))
+
+
+def _metric(metric):
+    if isinstance(metric, str):
+        if metric not in OBS_METRICS:
+            raise ValueError(f"metric must be one of {OBS_METRICS}")
+        return OBS_METRICS.index(metric)
+    return int(metric)
+
+
+def clq_obs_channel_scores(X, metric="absmax", workspace=None, out=None, stream=None):
+    """OBS outlier score per channel of calibration activations X, fp16
+    [B, N, D] (tokens with unit channel stride; the batch stride must be N
+    token rows).  Returns fp32 [D]."""
+    _dev(X, "X", torch.float16)
+    if X.dim() != 3 or X.stride(2) != 1 or X.stride(0) != X.shape[1] * X.stride(1):
+        raise ValueError("X must be [B, N, D] with unit channel stride and batch stride N * ldx")
+    B, N, D = X.shape
+    m = _metric(metric)
+    need = clq_obs_workspace_bytes(N, D, m)
+    if need == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_obs_channel_scores")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    _dev(workspace, "workspace", torch.uint8)
+    scores = out if out is not None else torch.empty(D, dtype=torch.float32, device=X.device)
+    _dev(scores, "scores", torch.float32)
+    _check(_lib.clq_obs_channel_scores(_ptr(X), X.stride(1), B, N, D, m, _ptr(workspace),
+                                       workspace.numel(), _ptr(scores), _stream(stream)),
+           "clq_obs_channel_scores")
+    return scores
+
+
+def clq_obs_permutation(scores, out=None, stream=None):
+    """The gather vector s (int32 [D]) that moves the top-scoring half of the
+    channels to the left half, each half in ascending channel order."""
+    _dev(scores, "scores", torch.float32)
+    if scores.dim() != 1 or not scores.is_contiguous():
+        raise ValueError("scores must be a contiguous fp32 [D] tensor")
+    D = scores.shape[0]
+    perm = out if out is not None else torch.empty(D, dtype=torch.int32, device=scores.device)
+    _dev(perm, "perm", torch.int32)
+    _check(_lib.clq_obs_permutation(_ptr(scores), D, _ptr(perm), _stream(stream)), "clq_obs_permutation")
+    return perm

@@ -9,7 +9,7 @@
 
 namespace {
 
-constexpr int kVersion = 3;
+constexpr int kVersion = 4;
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxRows = 2147483647;
 
@@ -46,9 +46,9 @@ const char *clq_status_string(clq_status s) {
         case CLQ_ERR_SHAPE: return "CLQ_ERR_SHAPE: a size or row stride is out of range";
         case CLQ_ERR_BLOCK: return "CLQ_ERR_BLOCK: block must be 32, 64 or 128 and divide K";
         case CLQ_ERR_ALIGN: return "CLQ_ERR_ALIGN: a pointer is misaligned";
-        case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio must lie in [2^-24, 1]";
+        case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio outside [2^-24, 1], or an unknown metric";
         case CLQ_ERR_HIP: return "CLQ_ERR_HIP: a HIP launch failed";
-        case CLQ_ERR_WORKSPACE: return "CLQ_ERR_WORKSPACE: workspace smaller than clq_w4a4_workspace_bytes()";
+        case CLQ_ERR_WORKSPACE: return "CLQ_ERR_WORKSPACE: workspace smaller than the entry point's *_workspace_bytes()";
     }
     return "CLQ: unknown status";
 }
@@ -158,6 +158,33 @@ clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K, void *Xq_cano
     if (!aligned(Xq, 16) || !aligned(Xq_canonical, 16)) return CLQ_ERR_ALIGN;
     return from_hip(clq::launch_unswizzle_act(static_cast<const uint8_t *>(Xq), M, (int)K,
                                               static_cast<uint8_t *>(Xq_canonical), stream));
+}
+
+size_t clq_obs_workspace_bytes(int64_t N, int64_t D, int32_t metric) {
+    if (N < 1 || N > kMaxRows || D < 8 || D > 65536 || D % 8 != 0 || metric < 0 || metric > 4) return 0;
+    return clq::obs_workspace_bytes(N, D, metric);
+}
+
+clq_status clq_obs_channel_scores(const void *X, int64_t ldx, int64_t B, int64_t N, int64_t D,
+                                  int32_t metric, void *workspace, size_t workspace_bytes,
+                                  float *scores, hipStream_t stream) {
+    if (!X || !scores || !workspace) return CLQ_ERR_NULL;
+    if (metric < 0 || metric > 4) return CLQ_ERR_ARG;
+    if (B < 1 || B >= (1 << 24) || N < 1 || N > kMaxRows || D < 8 || D > 65536 || D % 8 != 0)
+        return CLQ_ERR_SHAPE;
+    if (metric >= 2 && N > 32768) return CLQ_ERR_SHAPE;
+    if (ldx < D || ldx % 8 != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(X, 16) || !aligned(workspace, 16) || !aligned(scores, 4)) return CLQ_ERR_ALIGN;
+    if (workspace_bytes < clq::obs_workspace_bytes(N, D, metric)) return CLQ_ERR_WORKSPACE;
+    return from_hip(clq::launch_obs_scores(static_cast<const uint16_t *>(X), ldx, B, N, (int)D, metric,
+                                           workspace, scores, stream));
+}
+
+clq_status clq_obs_permutation(const float *scores, int64_t D, int32_t *perm, hipStream_t stream) {
+    if (!scores || !perm) return CLQ_ERR_NULL;
+    if (D < 2 || D > 65536 || D % 2 != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(scores, 4) || !aligned(perm, 4)) return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_obs_permutation(scores, (int)D, perm, stream));
 }
 
 }  // extern "C"

@@ -72,4 +72,14 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
                        int K, void *Y, int64_t ldy, bool i32out, void *workspace,
                        hipStream_t stream);
 
+// OBS calibration (batch mean, channel outlier scores, column swap).
+// metric: 0 abs-max, 1 range, 2 peak-to-average ratio, 3 top-k mean,
+// 4 percentile spread.
+size_t obs_workspace_bytes(int64_t N, int64_t D, int metric);
+
+hipError_t launch_obs_scores(const uint16_t *X, int64_t ldx, int64_t B, int64_t N, int D, int metric,
+                             void *workspace, float *scores, hipStream_t stream);
+
+hipError_t launch_obs_permutation(const float *scores, int D, int32_t *perm, hipStream_t stream);
+
 }  // namespace clq

@@ -45,12 +45,16 @@ def lib():
     L.clq_w4a4_linear.argtypes = [p, p, p, p, p, i64, i64, i64, p, i64, p, ctypes.c_size_t, p]
     L.clq_w4a4_accum_i32.argtypes = [p, p, i64, i64, i64, p, i64, p, ctypes.c_size_t, p]
     L.clq_unswizzle_weights.argtypes = [p, i64, i64, p, p]
+    L.clq_obs_workspace_bytes.restype = ctypes.c_size_t
+    L.clq_obs_workspace_bytes.argtypes = [i64, i64, i32]
+    L.clq_obs_channel_scores.argtypes = [p, i64, i64, i64, i64, i32, p, ctypes.c_size_t, p, p]
+    L.clq_obs_permutation.argtypes = [p, i64, p, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 11, names
+    assert len(names) == 14, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -62,7 +66,7 @@ def test_binding_names_match_header():
 
 
 def test_version_and_strings(lib):
-    assert lib.clq_version() == 3
+    assert lib.clq_version() == 4
     for code in range(8):
         s = lib.clq_status_string(code).decode()
         assert s.startswith("CLQ")
@@ -176,3 +180,44 @@ def test_accum_and_unswizzle_validation(lib):
     assert h(None, 8, 1152, A, None) == NULL
     assert h(A, 8, 100, A, None) == SHAPE
     assert h(A, 8, 1152, A + 8, None) == ALIGN
+
+
+def test_obs_workspace_bytes(lib):
+    f = lib.clq_obs_workspace_bytes
+    assert f(4096, 1152, 0) == 1152 * 8 and f(4096, 1152, 1) == 1152 * 8
+    for m in (2, 3, 4):
+        assert f(4096, 1152, m) == 4096 * 1152 * 4
+    assert f(10, 8, 2) == 512                        # rounded up to 256
+    assert f(0, 1152, 0) == 0 and f(16, 12, 0) == 0 and f(16, 1152, 5) == 0 and f(16, 1152, -1) == 0
+
+
+def test_obs_validation(lib):
+    f = lib.clq_obs_channel_scores
+    need = lib.clq_obs_workspace_bytes(64, 1152, 0)
+
+    def sc(X=A, ldx=1152, B=4, N=64, D=1152, metric=0, ws=A, wsb=need, out=A):
+        return f(X, ldx, B, N, D, metric, ws, wsb, out, None)
+    assert sc(X=None) == NULL
+    assert sc(ws=None) == NULL
+    assert sc(out=None) == NULL
+    assert sc(metric=5) == ARG
+    assert sc(metric=-1) == ARG
+    assert sc(B=0) == SHAPE
+    assert sc(N=0) == SHAPE
+    assert sc(D=12, ldx=16) == SHAPE                  # D % 8 != 0
+    assert sc(D=4, ldx=8) == SHAPE
+    assert sc(ldx=1000) == SHAPE                      # ldx < D
+    assert sc(ldx=1156) == SHAPE                      # ldx % 8 != 0
+    assert sc(N=40000, metric=3, wsb=1 << 40) == SHAPE    # sort metrics: N <= 32768
+    assert sc(X=A + 8) == ALIGN
+    assert sc(ws=A + 8) == ALIGN
+    assert sc(out=A + 2) == ALIGN
+    assert sc(wsb=need - 1) == WORKSPACE
+    assert sc(metric=2, wsb=need) == WORKSPACE        # the mean matrix is larger
+    g = lib.clq_obs_permutation
+    assert g(None, 64, A, None) == NULL
+    assert g(A, 64, None, None) == NULL
+    assert g(A, 63, A, None) == SHAPE
+    assert g(A, 0, A, None) == SHAPE
+    assert g(A, 65538, A, None) == SHAPE
+    assert g(A + 2, 64, A, None) == ALIGN

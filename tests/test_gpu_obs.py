@@ -1,0 +1,133 @@
+"""GPU parity of the OBS calibration (channel scores and the column swap)
+against the CPU oracle: scores and the gather vector must match bit for bit
+(both sides use the same fp32 arithmetic in the same order, so the integer
+result -- the swap -- is decided identically).
+
+Paper: "CLQ" (arXiv 2509.24416), Sec. 3.3 (Orthogonal-Based Smoothing) and
+the outlier-metric ablation of Sec. 4.3.
+"""
+import numpy as np
+import pytest
+
+from oracle import obs
+import workloads
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def clq():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2509_24416_amd as m
+    return m
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    print(f"\n[gpu case] {request.node.nodeid}", flush=True)
+    yield
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+SHAPES = [(1, 1, 8), (3, 7, 64), (2, 33, 136), (5, 300, 1152), (4, 1000, 520), (32, 64, 4608)]
+
+
+@pytest.mark.parametrize("B,N,D", SHAPES)
+@pytest.mark.parametrize("metric", obs.METRICS)
+def test_scores_and_swap_bitexact(clq, B, N, D, metric):
+    X = workloads.calibration(B, N, D, "L1", seed=B * 1000 + N + D)
+    S, ref_sc, ref_s = obs.obs(X, metric)
+    sc = clq.clq_obs_channel_scores(dev(X), metric)
+    got = host(sc)
+    assert np.array_equal(got, ref_sc), np.nonzero(got != ref_sc)[0][:8]
+    s = clq.clq_obs_permutation(sc)
+    assert np.array_equal(host(s), ref_s)
+
+
+@pytest.mark.parametrize("metric", obs.METRICS)
+def test_law_l2_and_strided_rows(clq, metric):
+    # tokens with a row stride wider than D (a column slice of a wider tensor)
+    B, N, D, ld = 3, 200, 256, 320
+    X = workloads.calibration(B, N, D, "L2", seed=77)
+    wide = np.zeros((B, N, ld), np.float16)
+    wide[:, :, :D] = X
+    t = dev(wide)[:, :, :D]
+    _, ref_sc, ref_s = obs.obs(X, metric)
+    sc = clq.clq_obs_channel_scores(t, metric)
+    assert np.array_equal(host(sc), ref_sc)
+    assert np.array_equal(host(clq.clq_obs_permutation(sc)), ref_s)
+
+
+@pytest.mark.parametrize("metric", ["par", "topk_mean", "percentile"])
+def test_long_token_columns(clq, metric):
+    # N past a power of two (zero / sentinel padding to 32768 in LDS)
+    B, N, D = 2, 21600, 16
+    X = workloads.calibration(B, N, D, "L1", seed=5)
+    _, ref_sc, _ = obs.obs(X, metric)
+    assert np.array_equal(host(clq.clq_obs_channel_scores(dev(X), metric)), ref_sc)
+
+
+def test_ties_and_degenerate_columns(clq):
+    # few distinct values: many equal scores (ties go to the lower channel),
+    # all-zero channels (peak-to-average 0), constant channels
+    B, N, D = 2, 64, 128
+    rng = np.random.default_rng(3)
+    X = rng.integers(-2, 3, size=(B, N, D)).astype(np.float16)
+    X[:, :, 5] = 0
+    X[:, :, 9] = 1.5
+    for metric in obs.METRICS:
+        _, ref_sc, ref_s = obs.obs(X, metric)
+        sc = clq.clq_obs_channel_scores(dev(X), metric)
+        assert np.array_equal(host(sc), ref_sc), metric
+        assert np.array_equal(host(clq.clq_obs_permutation(sc)), ref_s), metric
+
+
+@pytest.mark.parametrize("D", [2, 64, 4096, 12288, 65536])
+def test_permutation_bitexact(clq, D):
+    rng = np.random.default_rng(D)
+    sc = rng.integers(0, max(2, D // 8), size=D).astype(np.float32)   # ties
+    sc[rng.integers(0, D, size=max(1, D // 100))] *= 50
+    got = host(clq.clq_obs_permutation(dev(sc)))
+    assert np.array_equal(got, obs.permutation(sc))
+
+
+def test_full_size_pixart_calibration(clq):
+    # PixArt-style calibration batch: 32 samples x 4096 tokens x 1152
+    # channels, the abs-max metric the paper keeps; the planted outlier
+    # channels all land in the left half
+    B, N, D = 32, 4096, 1152
+    X = workloads.calibration(B, N, D, "L1", seed=2024)
+    _, ref_sc, ref_s = obs.obs(X, "absmax")
+    sc = clq.clq_obs_channel_scores(dev(X), "absmax")
+    s = host(clq.clq_obs_permutation(sc))
+    assert np.array_equal(host(sc), ref_sc)
+    assert np.array_equal(s, ref_s)
+    assert set(workloads.calibration_outliers(D, "L1", 2024).tolist()) <= set(s[:D // 2].tolist())
+
+
+def test_swap_feeds_the_linear(clq):
+    # the derived s drives the hot path: quantized linear with perm = s
+    # matches the oracle run with the same s
+    B, N, K, Nout, b = 4, 256, 1152, 256, 64
+    X = workloads.calibration(B, N, K, "L1", seed=31)
+    s = clq.clq_obs_permutation(clq.clq_obs_channel_scores(dev(X), "absmax"))
+    x = X[0]
+    W, bias = workloads.weights(Nout, K, 32), workloads.bias(Nout, 33)
+    perm = host(s)
+    ref = __import__("oracle").linear(x, W, bias, b, perm)
+    qw = clq.clq_quantize_weights(dev(W), b, perm=s)
+    Xq, xs = clq.clq_rotate_quant_act(dev(x), b, perm=s)
+    assert np.array_equal(host(xs), ref["x_scale"])
+    acc = host(clq.clq_w4a4_accum_i32(Xq, xs, qw))
+    assert np.array_equal(acc, ref["acc"])
