@@ -109,6 +109,96 @@ def cpu_baseline(layers, inputs, budget_s=15.0):
                       f"({ops / 2e9:.1f} G MAC, {t:.1f} s; weights quantized beforehand, untimed)"}
 
 
+def obs_bytes(B, N, D, metric):
+    """Algorithmic HBM bytes of one OBS channel-score pass: read the fp16
+    calibration batch, write D scores; the sort / sum metrics also write and
+    read back the fp32 mean matrix."""
+    b = B * N * D * 2 + D * 4
+    if metric not in ("absmax", "range"):
+        b += 2 * N * D * 4
+    return b
+
+
+def bench_obs(args, clq, torch, dev):
+    """OBS calibration (Sec. 3.3): channel scores of a PixArt-style
+    calibration batch (32 samples x 4096 tokens x 1152 channels, the input
+    width of qkv/proj/fc1) with the abs-max metric the paper keeps, then the
+    column swap.  value = GB/s of the score pass (HBM-bound)."""
+    B, N, D = 32, 4096, 1152
+    X = workloads.calibration(B, N, D, "L1", seed=2024)
+    Xd = torch.from_numpy(X).to(dev)
+    metrics = ("absmax", "range", "par", "topk_mean", "percentile")
+    ws = {m: torch.zeros(clq.clq_obs_workspace_bytes(N, D, m), dtype=torch.uint8, device=dev)
+          for m in metrics}
+    scores = torch.empty(D, dtype=torch.float32, device=dev)
+    perm = torch.empty(D, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        clq.clq_obs_channel_scores(Xd, "absmax", workspace=ws["absmax"], out=scores)
+        clq.clq_obs_permutation(scores, out=perm)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # per-launch times (HIP events on the launch stream around `steps`
+    # back-to-back launches of one entry point, so that host-side launch
+    # overhead overlaps the GPU work), per metric, and of the swap
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    per = {}
+    for m in metrics:
+        t_sc = timed(lambda: clq.clq_obs_channel_scores(Xd, m, workspace=ws[m], out=scores))
+        t_pm = timed(lambda: clq.clq_obs_permutation(scores, out=perm))
+        per[m] = (t_sc, t_pm)
+    sc_ms = per["absmax"][0]
+    achieved = obs_bytes(B, N, D, "absmax") / (sc_ms * 1e-3) / 1e9
+    value = obs_bytes(B, N, D, "absmax") / (ms_per_step * 1e-3) / 1e9
+    out = {
+        "metric": "OBS calibration channel-score pass, HBM GB/s",
+        "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "obs_calibration_b32_n4096_d1152", "B": B, "N": N, "D": D,
+                   "metric": "absmax", "parallelism": "none (one GPU)"},
+        "roofline": {"kernel": "obs_mean_kernel<0> (+ obs_finish_kernel)", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "avg_launch_us": round(sc_ms * 1e3, 2),
+                     "bytes_per_launch": obs_bytes(B, N, D, "absmax")},
+        "per_metric": {m: {"scores_us": round(per[m][0] * 1e3, 2),
+                           "scores_GBps": round(obs_bytes(B, N, D, m) / (per[m][0] * 1e-3) / 1e9, 1),
+                           "swap_us": round(per[m][1] * 1e3, 2)} for m in metrics},
+        "gpu": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline:
+        # the oracle on the first 4 samples of the same batch
+        from oracle import obs as oobs
+        t0 = time.perf_counter()
+        oobs.obs(X[:4], "absmax")
+        t = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(obs_bytes(4, N, D, "absmax") / t / 1e9, 3), "unit": "GB/s",
+                               "cores": 1, "kind": "oracle",
+                               "sample": f"first 4 of the 32 samples ({t:.2f} s, numpy, one thread)"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,6 +206,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--cold-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default="pixart_block", choices=["pixart_block", "obs_calibration"],
+                    help="pixart_block: the W4A4 linear hot path (default); obs_calibration: the OBS "
+                         "channel-score pass over a calibration batch")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (reference for the HBM "
                          "byte counters) and exit")
@@ -139,6 +232,10 @@ def main():
         return
 
     import paper_2509_24416_amd as clq
+
+    if args.workload == "obs_calibration":
+        bench_obs(args, clq, torch, dev)
+        return
 
     wl = workloads.C2
     layers = list(wl.layers)
@@ -211,20 +308,22 @@ def main():
     rq_achieved = rq_avg_bytes / (float(rq_ms.mean()) * 1e-3) / 1e9
 
     # rotate+quant and GEMM with the Infinity Cache flushed before each launch
-    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+    # (by reading 512 MB: a flush that writes would leave dirty lines to be
+    # written back during the timed launch)
+    flush = torch.ones(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
     cold_rq = np.zeros(len(layers))
     cold_gemm = np.zeros(len(layers))
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
         t_rq, t_g = [], []
         for _ in range(args.cold_reps):
-            flush.zero_()
+            flush.sum()
             e0.record(stream)
             clq.clq_rotate_quant_act(Xd, l.block, out=Xq, scale_out=xs)
             e1.record(stream)
             e1.synchronize()
             t_rq.append(e0.elapsed_time(e1))
-            flush.zero_()
+            flush.sum()
             e0.record(stream)
             clq.clq_w4a4_linear(Xq, xs, qw, bd, out=Y)
             e1.record(stream)

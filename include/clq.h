@@ -176,7 +176,7 @@ typedef enum {
                                l = (N - 1) / 100 (the 1% and 99% points)         */
 } clq_obs_metric;
 
-/* Workspace bytes clq_obs_channel_scores needs: 8*D for abs-max and range,
+/* Workspace bytes clq_obs_channel_scores needs: 128*D for abs-max and range,
  * 4*N*D (the fp32 mean matrix) for the others, rounded up to 256; 0 for
  * sizes or a metric out of range. */
 size_t clq_obs_workspace_bytes(int64_t N, int64_t D, int32_t metric);
@@ -189,8 +189,10 @@ size_t clq_obs_workspace_bytes(int64_t N, int64_t D, int32_t metric);
  *              metrics other than abs-max and range need N <= 32768.
  *   metric     a clq_obs_metric (else CLQ_ERR_ARG).
  *   workspace  device memory of at least clq_obs_workspace_bytes(N, D,
- *              metric), 16-byte aligned; overwritten (no initial contents
- *              needed).
+ *              metric), 16-byte aligned.  Abs-max and range: zero-filled
+ *              before its first use, and every call leaves it zero-filled
+ *              again (calls sharing it must not overlap in time).  The other
+ *              metrics: overwritten, no initial contents needed.
  *   scores     out, fp32 [D]. */
 clq_status clq_obs_channel_scores(const void *X, int64_t ldx, int64_t B, int64_t N,
                                   int64_t D, int32_t metric, void *workspace,

@@ -281,7 +281,8 @@ def _metric(metric):
 def clq_obs_channel_scores(X, metric="absmax", workspace=None, out=None, stream=None):
     """OBS outlier score per channel of calibration activations X, fp16
     [B, N, D] (tokens with unit channel stride; the batch stride must be N
-    token rows).  Returns fp32 [D]."""
+    token rows).  Returns fp32 [D].  A workspace passed in for abs-max or
+    range must be zero-filled before its first use (each call leaves it so)."""
     _dev(X, "X", torch.float16)
     if X.dim() != 3 or X.stride(2) != 1 or X.stride(0) != X.shape[1] * X.stride(1):
         raise ValueError("X must be [B, N, D] with unit channel stride and batch stride N * ldx")
@@ -290,8 +291,8 @@ def clq_obs_channel_scores(X, metric="absmax", workspace=None, out=None, stream=
     need = clq_obs_workspace_bytes(N, D, m)
     if need == 0:
         raise ClqError(CLQ_ERR_SHAPE, "clq_obs_channel_scores")
-    if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    if workspace is None:   # abs-max / range need it zero-filled; calls leave it so
+        workspace = torch.zeros(need, dtype=torch.uint8, device=X.device)
     _dev(workspace, "workspace", torch.uint8)
     scores = out if out is not None else torch.empty(D, dtype=torch.float32, device=X.device)
     _dev(scores, "scores", torch.float32)

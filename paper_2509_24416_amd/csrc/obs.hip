@@ -18,13 +18,15 @@
 //                          per-channel max |.| (abs-max) or max and min
 //                          (range) with order-preserving integer atomics;
 //                          MODE 2 writes the mean matrix [N][D] fp32.
+//                          (16 copies of the accumulators spread the
+//                          atomics of different workgroups.)
 //   obs_column_kernel<M>   one workgroup per channel over the mean matrix:
 //                          pairwise sum (peak-to-average ratio) or a bitonic
 //                          sort in LDS (top-k mean, percentile).
-//   obs_rank_kernel        rank of every score against all others; flags the
-//                          top half.
-//   obs_partition_kernel   one workgroup: stable partition of the flags into
-//                          the gather vector.
+//   obs_rank_kernel        how many channels beat each channel, over ranges
+//                          of the scores split across workgroups.
+//   obs_partition_kernel   one workgroup: the top half (beaten by fewer than
+//                          D/2) and a stable partition into the gather vector.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -48,12 +50,12 @@ __device__ __forceinline__ float ord_dec(uint32_t e) {
 __device__ __forceinline__ float h_lo(uint32_t w) { return __half2float(__ushort_as_half((unsigned short)(w & 0xffffu))); }
 __device__ __forceinline__ float h_hi(uint32_t w) { return __half2float(__ushort_as_half((unsigned short)(w >> 16))); }
 
-__global__ void obs_init_kernel(uint32_t *acc, int D) {
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < D; i += gridDim.x * blockDim.x) {
-        acc[i] = 0u;               // max accumulator: below every encoding
-        acc[D + i] = 0xFFFFFFFFu;  // min accumulator: above every encoding
-    }
-}
+// Max / min accumulators: kCopies copies of [2][D], so that the atomics of
+// different workgroups spread over more cache lines.  Both halves are
+// maxima of integer keys (the max of ord_enc(v), and the max of ~ord_enc(v)
+// for the minimum), so zero is the neutral start for both; the finishing
+// kernel reduces the copies and writes the zeros back for the next call.
+constexpr int kCopies = 16;
 
 // MODE 0: abs-max, 1: max and min, 2: write the mean matrix
 template <int MODE>
@@ -80,13 +82,13 @@ obs_mean_kernel(const uint16_t *__restrict__ X, int64_t ldx, int64_t B, int64_t 
 #pragma unroll
             for (int e = 0; e < 8; ++e) s[e] = 0.0f;
             int64_t b = 0;
-            // the samples in batch order; loads of four samples in flight
-            for (; b + 4 <= B; b += 4) {
-                uint4 v[4];
+            // the samples in batch order; loads of eight samples in flight
+            for (; b + 8 <= B; b += 8) {
+                uint4 v[8];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const uint4 *>(p + (b + q) * bstride);
+                for (int q = 0; q < 8; ++q) v[q] = *reinterpret_cast<const uint4 *>(p + (b + q) * bstride);
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
+                for (int q = 0; q < 8; ++q) {
                     const uint32_t w[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
@@ -128,7 +130,7 @@ obs_mean_kernel(const uint16_t *__restrict__ X, int64_t ldx, int64_t B, int64_t 
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             red[0][wave][lane * 8 + e] = MODE == 0 ? __float_as_uint(mx[e]) : ord_enc(mx[e]);
-            red[1][wave][lane * 8 + e] = ord_enc(mn[e]);
+            red[1][wave][lane * 8 + e] = ~ord_enc(mn[e]);
         }
         __syncthreads();
         if (wave == 0 && ok) {
@@ -139,20 +141,29 @@ obs_mean_kernel(const uint16_t *__restrict__ X, int64_t ldx, int64_t B, int64_t 
 #pragma unroll
                 for (int q = 1; q < 4; ++q) {
                     a = max(a, red[0][q][i]);
-                    c = min(c, red[1][q][i]);
+                    c = max(c, red[1][q][i]);
                 }
                 const int d = chunk * 8 + e;
-                atomicMax(&acc[d], a);
-                if constexpr (MODE == 1) atomicMin(&acc[D + d], c);
+                uint32_t *cp = acc + (blockIdx.y % kCopies) * 2 * D;
+                atomicMax(&cp[d], a);
+                if constexpr (MODE == 1) atomicMax(&cp[D + d], c);
             }
         }
     }
 }
 
-__global__ void obs_finish_kernel(const uint32_t *__restrict__ acc, int D, int metric,
+__global__ void obs_finish_kernel(uint32_t *__restrict__ acc, int D, int metric,
                                   float *__restrict__ scores) {
-    for (int d = blockIdx.x * blockDim.x + threadIdx.x; d < D; d += gridDim.x * blockDim.x)
-        scores[d] = metric == 0 ? __uint_as_float(acc[d]) : ord_dec(acc[d]) - ord_dec(acc[D + d]);
+    for (int d = blockIdx.x * blockDim.x + threadIdx.x; d < D; d += gridDim.x * blockDim.x) {
+        uint32_t a = 0u, c = 0u;
+        for (int k = 0; k < kCopies; ++k) {
+            a = max(a, acc[k * 2 * D + d]);
+            c = max(c, acc[k * 2 * D + D + d]);
+            acc[k * 2 * D + d] = 0u;
+            acc[k * 2 * D + D + d] = 0u;
+        }
+        scores[d] = metric == 0 ? __uint_as_float(a) : ord_dec(a) - ord_dec(~c);
+    }
 }
 
 constexpr int kColThreads = 1024;
@@ -231,29 +242,55 @@ obs_column_kernel(const float *__restrict__ S, int64_t N, int D, int P, float *_
     }
 }
 
-// flags[d] = 1 if fewer than D/2 channels beat d (higher score, or equal
-// score and lower index)
-__global__ void __launch_bounds__(256)
-obs_rank_kernel(const float *__restrict__ scores, int D, int32_t *__restrict__ flags)
-{
-    __shared__ float tile[4096];
-    const int d = blockIdx.x * 256 + threadIdx.x;
-    const float sd = d < D ? scores[d] : 0.0f;
-    int beaten = 0;
-    for (int base = 0; base < D; base += 4096) {
-        const int n = min(4096, D - base);
-        __syncthreads();
-        for (int i = threadIdx.x; i < n; i += 256) tile[i] = scores[base + i];
-        __syncthreads();
-        for (int i = 0; i < n; ++i) {
-            const float s = tile[i];
-            beaten += (s > sd) || (s == sd && base + i < d);
-        }
-    }
-    if (d < D) flags[d] = beaten < (D >> 1) ? 1 : 0;
+__global__ void obs_zero_kernel(int32_t *p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
-// one workgroup: perm holds the flags on entry and the gather vector on exit
+// count[d] += the channels in [by * chunk, (by + 1) * chunk) that beat d
+// (higher score, or equal score and lower index); chunk <= 4096
+__global__ void __launch_bounds__(256)
+obs_rank_kernel(const float *__restrict__ scores, int D, int chunk, int32_t *__restrict__ count)
+{
+    __shared__ float4 tile[1024];   // 4096 scores
+    float *tf = reinterpret_cast<float *>(tile);
+    const int d = blockIdx.x * 256 + threadIdx.x;
+    const float sd = d < D ? scores[d] : 0.0f;
+    const int base = blockIdx.y * chunk;
+    const int n = min(chunk, D - base);
+    // pad the tile's last float4 with scores that beat no one
+    for (int i = threadIdx.x; i < (n + 3) / 4 * 4; i += 256)
+        tf[i] = i < n ? scores[base + i] : -__builtin_inff();
+    __syncthreads();
+    // every lane reads the same float4 (an LDS broadcast), 8 in flight
+    int beaten = 0;
+    const int n4 = (n + 3) / 4;
+    int i4 = 0;
+    for (; i4 + 8 <= n4; i4 += 8) {
+        float4 v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = tile[i4 + q];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int e = base + 4 * (i4 + q);
+            beaten += (v[q].x > sd) || (v[q].x == sd && e < d);
+            beaten += (v[q].y > sd) || (v[q].y == sd && e + 1 < d);
+            beaten += (v[q].z > sd) || (v[q].z == sd && e + 2 < d);
+            beaten += (v[q].w > sd) || (v[q].w == sd && e + 3 < d);
+        }
+    }
+    for (; i4 < n4; ++i4) {
+        const float4 v = tile[i4];
+        const int e = base + 4 * i4;
+        beaten += (v.x > sd) || (v.x == sd && e < d);
+        beaten += (v.y > sd) || (v.y == sd && e + 1 < d);
+        beaten += (v.z > sd) || (v.z == sd && e + 2 < d);
+        beaten += (v.w > sd) || (v.w == sd && e + 3 < d);
+    }
+    if (d < D && beaten) atomicAdd(&count[d], beaten);
+}
+
+// one workgroup: perm holds the beat counts on entry (a channel is in the
+// top half when fewer than D/2 channels beat it) and the gather vector on exit
 __global__ void __launch_bounds__(1024)
 obs_partition_kernel(int D, int32_t *__restrict__ perm)
 {
@@ -264,7 +301,7 @@ obs_partition_kernel(int D, int32_t *__restrict__ perm)
     const int lo = min(D, t * per), hi = min(D, lo + per);
     int c = 0;
     for (int i = lo; i < hi; ++i) {
-        const int f = perm[i];
+        const int f = perm[i] < (D >> 1) ? 1 : 0;
         fl[i] = (uint8_t)f;
         c += f;
     }
@@ -295,18 +332,18 @@ int obs_pow2(int64_t n) {
 }
 
 size_t obs_workspace_bytes(int64_t N, int64_t D, int metric) {
-    const size_t b = metric <= 1 ? (size_t)D * 8 : (size_t)N * (size_t)D * 4;
+    const size_t b = metric <= 1 ? (size_t)kCopies * D * 8 : (size_t)N * (size_t)D * 4;
     return (b + 255) / 256 * 256;
 }
 
 hipError_t launch_obs_scores(const uint16_t *X, int64_t ldx, int64_t B, int64_t N, int D, int metric,
                              void *workspace, float *scores, hipStream_t stream) {
+    // about 2048 workgroups; each wave walks at least four token rows
     const int gx = (D / 8 + 63) / 64;
-    const int64_t gy = std::max<int64_t>(1, std::min<int64_t>((N + 3) / 4, (2048 + gx - 1) / gx));
+    const int64_t gy = std::max<int64_t>(1, std::min<int64_t>((N + 15) / 16, (2048 + gx - 1) / gx));
     const dim3 grid((unsigned)gx, (unsigned)gy);
     if (metric <= 1) {
         uint32_t *acc = static_cast<uint32_t *>(workspace);
-        hipLaunchKernelGGL(obs_init_kernel, dim3((D + 255) / 256), dim3(256), 0, stream, acc, D);
         if (metric == 0)
             hipLaunchKernelGGL(obs_mean_kernel<0>, grid, dim3(256), 0, stream, X, ldx, B, N, D, nullptr, acc);
         else
@@ -339,7 +376,15 @@ hipError_t launch_obs_scores(const uint16_t *X, int64_t ldx, int64_t B, int64_t 
 }
 
 hipError_t launch_obs_permutation(const float *scores, int D, int32_t *perm, hipStream_t stream) {
-    hipLaunchKernelGGL(obs_rank_kernel, dim3((D + 255) / 256), dim3(256), 0, stream, scores, D, perm);
+    // about 1024 workgroups: channels in groups of 256 x compared ranges of
+    // at least 256 scores
+    const int gx = (D + 255) / 256;
+    int parts = std::max(1, std::min((1024 + gx - 1) / gx, D / 256));
+    int chunk = (D + parts - 1) / parts;
+    chunk = std::min(4096, (chunk + 3) / 4 * 4);
+    parts = (D + chunk - 1) / chunk;
+    hipLaunchKernelGGL(obs_zero_kernel, dim3((D + 255) / 256), dim3(256), 0, stream, perm, D);
+    hipLaunchKernelGGL(obs_rank_kernel, dim3(gx, parts), dim3(256), 0, stream, scores, D, chunk, perm);
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void *)obs_partition_kernel,

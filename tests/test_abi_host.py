@@ -184,7 +184,7 @@ def test_accum_and_unswizzle_validation(lib):
 
 def test_obs_workspace_bytes(lib):
     f = lib.clq_obs_workspace_bytes
-    assert f(4096, 1152, 0) == 1152 * 8 and f(4096, 1152, 1) == 1152 * 8
+    assert f(4096, 1152, 0) == 1152 * 128 and f(4096, 1152, 1) == 1152 * 128
     for m in (2, 3, 4):
         assert f(4096, 1152, m) == 4096 * 1152 * 4
     assert f(10, 8, 2) == 512                        # rounded up to 256
