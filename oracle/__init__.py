@@ -11,8 +11,9 @@ result); this module marshals numpy arrays into it and adds the fp64
 references used to pin it (dense Hadamard matrix, unquantised linear, error
 metric).  Paper references are to "CLQ" (arXiv 2509.24416):
 
-  Sec. 3.1, Eq. (1)  uniform quantizer Round(Clip(.)), n = 4 bits; dynamic
-                     activation bounds, weights quantized once.
+  Sec. 3.1, Eq. (1)  uniform quantizer Round(Clip(.)), n = 4 bits (8 for the
+                     W4A8 / W8A8 settings of Sec. 4.1); dynamic activation
+                     bounds, weights quantized once.
   Sec. 3.3           OBS: G = S.H (gather vector s, block Hadamard H with
                      +-1 entries); weights absorb G offline, activations get a
                      fast Hadamard transform online.
@@ -51,11 +52,12 @@ def _load():
     lib.clqo_get_threads.restype = ctypes.c_int
     lib.clqo_rotate.argtypes = [_p, _i64, _p, _i64, _i64, _i32, _p]
     lib.clqo_quantize.argtypes = [_p, _i64, _i64, _f32, _p, _p, _p]
+    lib.clqo_quantize_q.argtypes = [_p, _i64, _i64, _f32, _f32, _p, _p, _p]
     lib.clqo_pack.argtypes = [_p, _i64, _i64, _p]
     lib.clqo_unpack.argtypes = [_p, _i64, _i64, _p]
     lib.clqo_gemm_i32.argtypes = [_p, _p, _i64, _i64, _i64, _p]
     lib.clqo_epilogue.argtypes = [_p, _p, _p, _p, _i64, _i64, _p, _p]
-    for f in ("clqo_set_threads", "clqo_rotate", "clqo_quantize", "clqo_pack",
+    for f in ("clqo_set_threads", "clqo_rotate", "clqo_quantize", "clqo_quantize_q", "clqo_pack",
               "clqo_unpack", "clqo_gemm_i32", "clqo_epilogue"):
         getattr(lib, f).restype = None
     _lib = lib
@@ -128,15 +130,23 @@ def rotate(X, block, perm=None):
     return out
 
 
-def quantize(xr, alpha=1.0):
-    """Symmetric per-row int4 quantizer of Eq. (1).  Returns (codes int8
-    [rows][K] in [-7, 7], scale fp32 [rows], nclamp int32 [rows])."""
+def qmax(bits):
+    """Largest code of the symmetric n-bit grid: 2^(n-1) - 1."""
+    return (1 << (bits - 1)) - 1
+
+
+def quantize(xr, alpha=1.0, bits=4):
+    """Symmetric per-row quantizer of Eq. (1) with n = bits (4 or 8).
+    Returns (codes int8 [rows][K] in [-qmax, qmax], scale fp32 [rows],
+    nclamp int32 [rows])."""
+    assert bits in (4, 8)
     xr = np.ascontiguousarray(xr, dtype=np.float32)
     rows, K = xr.shape
     codes = np.empty((rows, K), np.int8)
     scale = np.empty(rows, np.float32)
     ncl = np.empty(rows, np.int32)
-    _load().clqo_quantize(_ptr(xr), rows, K, float(alpha), _ptr(codes), _ptr(scale), _ptr(ncl))
+    _load().clqo_quantize_q(_ptr(xr), rows, K, float(alpha), float(qmax(bits)), _ptr(codes),
+                            _ptr(scale), _ptr(ncl))
     return codes, scale, ncl
 
 
@@ -156,21 +166,23 @@ def unpack(packed, K):
     return out
 
 
-def quantize_act(X, block, perm=None):
-    """Online activation path: rotate, per-token quantize (alpha = 1), pack.
-    Returns (packed uint8 [M][K/2], codes int8 [M][K], x_scale fp32 [M])."""
-    codes, xs, _ = quantize(rotate(X, block, perm), 1.0)
-    return pack(codes), codes, xs
+def quantize_act(X, block, perm=None, bits=4):
+    """Online activation path: rotate, per-token quantize (alpha = 1) and,
+    for 4 bits, pack.  Returns (packed uint8 [M][K/2] for 4 bits or the int8
+    codes themselves for 8, codes int8 [M][K], x_scale fp32 [M])."""
+    codes, xs, _ = quantize(rotate(X, block, perm), 1.0, bits)
+    return (pack(codes) if bits == 4 else codes), codes, xs
 
 
-def quantize_weights(W, block, perm=None, clip_ratio=1.0):
+def quantize_weights(W, block, perm=None, clip_ratio=1.0, bits=4):
     """Offline weight path: W~ = W . G row-wise, per-output-channel quantizer
     with clip ratio alpha, w_scale = s / b (the Hadamard normalisation folded
     in, exact since b is a power of two).  Returns (packed canonical uint8
-    [N][K/2], codes int8 [N][K], w_scale fp32 [N])."""
-    codes, s, _ = quantize(rotate(W, block, perm), clip_ratio)
+    [N][K/2] for 4 bits or the int8 codes for 8, codes int8 [N][K], w_scale
+    fp32 [N])."""
+    codes, s, _ = quantize(rotate(W, block, perm), clip_ratio, bits)
     ws = (s * np.float32(1.0 / block)).astype(np.float32)
-    return pack(codes), codes, ws
+    return (pack(codes) if bits == 4 else codes), codes, ws
 
 
 def gemm_i32(qa, qw):
@@ -199,11 +211,12 @@ def epilogue(acc, x_scale, w_scale, bias=None):
     return y, p
 
 
-def linear(X, W, bias, block, perm=None, clip_ratio=1.0):
-    """The whole W4A4 linear on the CPU.  Returns a dict with every
-    intermediate: xq, xcodes, x_scale, wq, wcodes, w_scale, acc, y64, p64."""
-    xq, xc, xs = quantize_act(X, block, perm)
-    wq, wc, ws = quantize_weights(W, block, perm, clip_ratio)
+def linear(X, W, bias, block, perm=None, clip_ratio=1.0, wbits=4, abits=4):
+    """The whole quantized linear on the CPU (W4A4 by default; W4A8 and W8A8
+    with wbits / abits = 8).  Returns a dict with every intermediate: xq,
+    xcodes, x_scale, wq, wcodes, w_scale, acc, y64, p64."""
+    xq, xc, xs = quantize_act(X, block, perm, abits)
+    wq, wc, ws = quantize_weights(W, block, perm, clip_ratio, wbits)
     acc = gemm_i32(xc, wc)
     y64, p64 = epilogue(acc, xs, ws, bias)
     return dict(xq=xq, xcodes=xc, x_scale=xs, wq=wq, wcodes=wc, w_scale=ws,

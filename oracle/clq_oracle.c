@@ -82,12 +82,14 @@ void clqo_rotate(const float *x, int64_t ldx, const int32_t *perm,
     }
 }
 
-/* ---- Sec. 3.1 Eq. (1): symmetric per-row int4 quantizer ----------------- */
+/* ---- Sec. 3.1 Eq. (1): symmetric per-row quantizer, n = 4 or 8 bits ------ */
 
-/* codes[r][k] in [-7, 7]; scale[r] = fl32(a_c / 7).  Returns nothing; the
- * number of clamped elements per row is written to nclamp[r] if non-NULL. */
-void clqo_quantize(const float *xr, int64_t rows, int64_t K, float alpha,
-                   int8_t *codes, float *scale, int32_t *nclamp)
+/* codes[r][k] in [-qmax, qmax] with qmax = 2^(n-1) - 1 (7 for n = 4 bits,
+ * 127 for n = 8); scale[r] = fl32(a_c / qmax), a_c = fl32(alpha * max|x|).
+ * The number of clamped elements per row is written to nclamp[r] if
+ * non-NULL. */
+void clqo_quantize_q(const float *xr, int64_t rows, int64_t K, float alpha, float qmax,
+                     int8_t *codes, float *scale, int32_t *nclamp)
 {
     #pragma omp parallel for schedule(static)
     for (int64_t r = 0; r < rows; ++r) {
@@ -104,13 +106,13 @@ void clqo_quantize(const float *xr, int64_t rows, int64_t K, float alpha,
             scale[r] = 0.0f;
             for (int64_t k = 0; k < K; ++k) q[k] = 0;
         } else {
-            float s = ac / 7.0f;
-            float rc = 7.0f / ac;
+            float s = ac / qmax;
+            float rc = qmax / ac;
             scale[r] = s;
             for (int64_t k = 0; k < K; ++k) {
                 double t = rint((double)x[k] * (double)rc); /* exact product, RNE */
-                if (t > 7.0) { t = 7.0; ++nc; }
-                if (t < -7.0) { t = -7.0; ++nc; }
+                if (t > qmax) { t = qmax; ++nc; }
+                if (t < -qmax) { t = -qmax; ++nc; }
                 q[k] = (int8_t)t;
             }
         }
@@ -118,7 +120,12 @@ void clqo_quantize(const float *xr, int64_t rows, int64_t K, float alpha,
     }
 }
 
-/* ---- nibble packing (two's complement, low nibble = even k) ------------- */
+/* The 4-bit quantizer of the W4A4 path: qmax = 7. */
+void clqo_quantize(const float *xr, int64_t rows, int64_t K, float alpha,
+                   int8_t *codes, float *scale, int32_t *nclamp)
+{
+    clqo_quantize_q(xr, rows, K, alpha, 7.0f, codes, scale, nclamp);
+}
 
 void clqo_pack(const int8_t *codes, int64_t rows, int64_t K, uint8_t *out)
 {
