@@ -58,7 +58,7 @@ typedef enum {
     CLQ_ERR_SHAPE = 2, /* M, N, K, ld* out of range or not multiples         */
     CLQ_ERR_BLOCK = 3, /* block not in {32, 64, 128} or K % block != 0       */
     CLQ_ERR_ALIGN = 4, /* a pointer is not aligned as required               */
-    CLQ_ERR_ARG = 5,   /* clip_ratio outside [2^-24, 1], or an unknown metric  */
+    CLQ_ERR_ARG = 5,   /* clip_ratio outside [2^-24, 1], unknown metric or wbits */
     CLQ_ERR_HIP = 6,   /* a HIP launch failed (see hipGetLastError)           */
     CLQ_ERR_WORKSPACE = 7 /* workspace smaller than the *_workspace_bytes() query */
 } clq_status;
@@ -154,6 +154,61 @@ clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K,
  * uint8 [M][K/2] (16-byte aligned), same nibble convention. */
 clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K,
                              void *Xq_canonical, hipStream_t stream);
+
+/* ---- 8-bit settings: W4A8 and W8A8 (Sec. 4.1 runs the method at W8A8,
+ * W4A8 and W4A4; Sec. 3.1 Eq. (1) with n = 8) -------------------------------
+ * The same rotation and quantizer with qmax = 127: q = clamp(rne(x~ * r),
+ * -127, 127), r = fl32(127 / (alpha * max|x~|)), scale = alpha * max|x~| /
+ * 127 (weights: / b as well).  Codes are int8 in an opaque layout shaped for
+ * the int8 matrix cores (clq_unswizzle_act8 / clq_unswizzle_weights8 give the
+ * row-major codes).  No workspace; the library allocates nothing. */
+
+/* Bytes of the int8 activation buffer: M rows padded to a multiple of 32,
+ * times K (0 for sizes out of range). */
+size_t clq_act8_bytes(int64_t M, int64_t K);
+
+/* Bytes of the int8 weight buffer: N rows padded to a multiple of 64, times
+ * K (0 for sizes out of range). */
+size_t clq_weight8_bytes(int64_t N, int64_t K);
+
+/* clq_rotate_quant_act with 8-bit codes: same arguments and rules, Xq8 of
+ * clq_act8_bytes(M, K) bytes, x_scale = max|x~| / 127. */
+clq_status clq_rotate_quant_act8(const void *X, int64_t ldx, const int32_t *perm,
+                                 int64_t M, int64_t K, int32_t block, void *Xq8,
+                                 float *x_scale, hipStream_t stream);
+
+/* clq_quantize_weights with 8-bit codes: same arguments and rules, Wq8 of
+ * clq_weight8_bytes(N, K) bytes, w_scale = (alpha * max|w~| / 127) / b. */
+clq_status clq_quantize_weights8(const void *W, const int32_t *perm, int64_t N,
+                                 int64_t K, int32_t block, float clip_ratio,
+                                 void *Wq8, float *w_scale, hipStream_t stream);
+
+/* W4A8 / W8A8 linear: Y = dequant(Xq8 . Wq^T) + bias as fp16.
+ *   Xq8, x_scale  from clq_rotate_quant_act8 (M rows, same K).
+ *   Wq, w_scale   wbits = 4: from clq_quantize_weights (W4A8);
+ *                 wbits = 8: from clq_quantize_weights8 (W8A8); else ARG.
+ *   bias          fp16 [N] or NULL (2-byte aligned).
+ *   Y             out, fp16 [M][N], row stride ldy (>= N, multiple of 8).
+ * y[m][n] = fp16(fl32(sum * x_scale[m]) * w_scale[n] + bias[n]) with the
+ * integer sum exact and the last multiply-add fused (as clq_w4a4_linear). */
+clq_status clq_a8_linear(const void *Xq8, const float *x_scale, const void *Wq,
+                         const float *w_scale, int32_t wbits, const void *bias,
+                         int64_t M, int64_t N, int64_t K, void *Y, int64_t ldy,
+                         hipStream_t stream);
+
+/* Diagnostic: the exact integer sums of clq_a8_linear as int32 [M][N], row
+ * stride ldacc (>= N, multiple of 4). */
+clq_status clq_a8_accum_i32(const void *Xq8, const void *Wq, int32_t wbits, int64_t M,
+                            int64_t N, int64_t K, int32_t *acc, int64_t ldacc,
+                            hipStream_t stream);
+
+/* Diagnostic: row-major int8 codes [M][K] of an int8 activation buffer. */
+clq_status clq_unswizzle_act8(const void *Xq8, int64_t M, int64_t K, void *codes,
+                              hipStream_t stream);
+
+/* Diagnostic: row-major int8 codes [N][K] of an int8 weight buffer. */
+clq_status clq_unswizzle_weights8(const void *Wq8, int64_t N, int64_t K, void *codes,
+                                  hipStream_t stream);
 
 /* ---- OBS calibration (Sec. 3.3 "Orthogonal-Based Smoothing", outlier
  * detection; Sec. 4.3 ablation of the outlier metric) ----------------------

@@ -12,6 +12,11 @@ carry the names of the C entry points declared in ``include/clq.h``:
     clq_unswizzle_act(Xq, M, K)                                -> canonical codes
     clq_obs_channel_scores(X, metric="absmax")                 -> scores [D]
     clq_obs_permutation(scores)                                -> perm [D]
+    clq_rotate_quant_act8(X, block, perm=None)                 -> (Xq8, x_scale)
+    clq_quantize_weights8(W, block, perm=None, clip_ratio=1.0) -> QWeight (8-bit)
+    clq_a8_linear(Xq8, x_scale, qw, bias=None)                 -> Y   (W4A8 / W8A8)
+    clq_a8_accum_i32(Xq8, x_scale, qw)                         -> acc
+    clq_unswizzle_act8(Xq8, M, K), clq_unswizzle_weights8(qw)  -> int8 codes
 
 Paper: "CLQ" (arXiv 2509.24416) -- Sec. 3.3 (online block-Hadamard rotation,
 weights absorb it offline) and Sec. 3.1 Eq. (1) (4-bit quantizer; dynamic
@@ -56,15 +61,29 @@ _lib.clq_obs_workspace_bytes.restype = ctypes.c_size_t
 _lib.clq_obs_workspace_bytes.argtypes = [_i64, _i64, _i32]
 _lib.clq_obs_channel_scores.argtypes = [_p, _i64, _i64, _i64, _i64, _i32, _p, ctypes.c_size_t, _p, _p]
 _lib.clq_obs_permutation.argtypes = [_p, _i64, _p, _p]
+_lib.clq_act8_bytes.restype = ctypes.c_size_t
+_lib.clq_act8_bytes.argtypes = [_i64, _i64]
+_lib.clq_weight8_bytes.restype = ctypes.c_size_t
+_lib.clq_weight8_bytes.argtypes = [_i64, _i64]
+_lib.clq_rotate_quant_act8.argtypes = [_p, _i64, _p, _i64, _i64, _i32, _p, _p, _p]
+_lib.clq_quantize_weights8.argtypes = [_p, _p, _i64, _i64, _i32, _f32, _p, _p, _p]
+_lib.clq_a8_linear.argtypes = [_p, _p, _p, _p, _i32, _p, _i64, _i64, _i64, _p, _i64, _p]
+_lib.clq_a8_accum_i32.argtypes = [_p, _p, _i32, _i64, _i64, _i64, _p, _i64, _p]
+_lib.clq_unswizzle_act8.argtypes = [_p, _i64, _i64, _p, _p]
+_lib.clq_unswizzle_weights8.argtypes = [_p, _i64, _i64, _p, _p]
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
-           "clq_obs_channel_scores", "clq_obs_permutation"):
+           "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
+           "clq_quantize_weights8", "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8",
+           "clq_unswizzle_weights8"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
            "clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_workspace_bytes",
            "clq_w4a4_linear", "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
-           "clq_obs_workspace_bytes", "clq_obs_channel_scores", "clq_obs_permutation")
+           "clq_obs_workspace_bytes", "clq_obs_channel_scores", "clq_obs_permutation",
+           "clq_act8_bytes", "clq_weight8_bytes", "clq_rotate_quant_act8", "clq_quantize_weights8",
+           "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8", "clq_unswizzle_weights8")
 
 OBS_METRICS = ("absmax", "range", "par", "topk_mean", "percentile")
 
@@ -136,6 +155,7 @@ class QWeight:
     block: int
     perm: torch.Tensor = None
     clip_ratio: float = 1.0
+    bits: int = 4           # 4: clq_quantize_weights, 8: clq_quantize_weights8
 
 
 def clq_quantize_weights(W, block, perm=None, clip_ratio=1.0, stream=None):
@@ -313,3 +333,109 @@ def clq_obs_permutation(scores, out=None, stream=None):
     _dev(perm, "perm", torch.int32)
     _check(_lib.clq_obs_permutation(_ptr(scores), D, _ptr(perm), _stream(stream)), "clq_obs_permutation")
     return perm
+
+
+# ---- 8-bit activations: W4A8 and W8A8 -------------------------------------------
+
+def clq_act8_bytes(M, K):
+    return int(_lib.clq_act8_bytes(M, K))
+
+
+def clq_weight8_bytes(N, K):
+    return int(_lib.clq_weight8_bytes(N, K))
+
+
+def clq_rotate_quant_act8(X, block, perm=None, out=None, scale_out=None, stream=None):
+    """clq_rotate_quant_act with 8-bit codes (x_scale = max|x~| / 127).
+    Returns (Xq8 uint8 [clq_act8_bytes(M, K)], x_scale fp32 [M])."""
+    _dev(X, "X", torch.float16)
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D [M, K] with unit column stride")
+    M, K = X.shape
+    perm = _perm(perm, K)
+    nbytes = clq_act8_bytes(M, K)
+    if nbytes == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_rotate_quant_act8")
+    Xq = out if out is not None else torch.empty(nbytes, dtype=torch.uint8, device=X.device)
+    xs = scale_out if scale_out is not None else torch.empty(M, dtype=torch.float32, device=X.device)
+    _dev(Xq, "Xq8", torch.uint8)
+    _dev(xs, "x_scale", torch.float32)
+    if Xq.numel() < nbytes or not Xq.is_contiguous() or xs.numel() < M:
+        raise ValueError("Xq8 / x_scale buffers are too small")
+    _check(_lib.clq_rotate_quant_act8(_ptr(X), X.stride(0), _ptr(perm), M, K, block, _ptr(Xq),
+                                      _ptr(xs), _stream(stream)), "clq_rotate_quant_act8")
+    return Xq, xs
+
+
+def clq_quantize_weights8(W, block, perm=None, clip_ratio=1.0, stream=None):
+    """clq_quantize_weights with 8-bit codes (w_scale = alpha max|w~| / 127 / b)."""
+    _dev(W, "W", torch.float16)
+    if W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be a contiguous 2-D [N, K] tensor")
+    N, K = W.shape
+    perm = _perm(perm, K)
+    nbytes = clq_weight8_bytes(N, K)
+    if nbytes == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_quantize_weights8")
+    wq = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
+    ws = torch.empty(N, dtype=torch.float32, device=W.device)
+    _check(_lib.clq_quantize_weights8(_ptr(W), _ptr(perm), N, K, block, clip_ratio, _ptr(wq), _ptr(ws),
+                                      _stream(stream)), "clq_quantize_weights8")
+    return QWeight(wq, ws, N, K, block, perm, clip_ratio, 8)
+
+
+def _check_xq8(Xq8, x_scale, K):
+    _dev(Xq8, "Xq8", torch.uint8)
+    _dev(x_scale, "x_scale", torch.float32)
+    M = x_scale.shape[0]
+    if not Xq8.is_contiguous() or Xq8.numel() < clq_act8_bytes(M, K):
+        raise ValueError("Xq8 must be the contiguous buffer clq_rotate_quant_act8 produced for "
+                         "these M and K")
+    return M
+
+
+def clq_a8_linear(Xq8, x_scale, qw, bias=None, out=None, stream=None):
+    """W4A8 (qw from clq_quantize_weights) or W8A8 (qw from
+    clq_quantize_weights8) linear: fp16 [M, N]."""
+    M = _check_xq8(Xq8, x_scale, qw.K)
+    if bias is not None:
+        _dev(bias, "bias", torch.float16)
+        if bias.shape != (qw.N,) or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous fp16 [N] tensor")
+    if out is None:
+        out = torch.empty((M, (qw.N + 7) // 8 * 8), dtype=torch.float16, device=Xq8.device)[:, :qw.N]
+    Y = out
+    _dev(Y, "Y", torch.float16)
+    if Y.dim() != 2 or Y.stride(1) != 1 or Y.shape != (M, qw.N):
+        raise ValueError("Y must be 2-D [M, N] with unit column stride")
+    _check(_lib.clq_a8_linear(_ptr(Xq8), _ptr(x_scale), _ptr(qw.wq), _ptr(qw.w_scale), qw.bits, _ptr(bias),
+                              M, qw.N, qw.K, _ptr(Y), Y.stride(0), _stream(stream)), "clq_a8_linear")
+    return Y
+
+
+def clq_a8_accum_i32(Xq8, x_scale, qw, out=None, stream=None):
+    """The exact integer sums of clq_a8_linear, int32 [M, N] (diagnostic)."""
+    M = _check_xq8(Xq8, x_scale, qw.K)
+    if out is None:
+        out = torch.empty((M, (qw.N + 3) // 4 * 4), dtype=torch.int32, device=Xq8.device)[:, :qw.N]
+    acc = out
+    _dev(acc, "acc", torch.int32)
+    _check(_lib.clq_a8_accum_i32(_ptr(Xq8), _ptr(qw.wq), qw.bits, M, qw.N, qw.K, _ptr(acc), acc.stride(0),
+                                 _stream(stream)), "clq_a8_accum_i32")
+    return acc
+
+
+def clq_unswizzle_act8(Xq8, M, K, stream=None):
+    """Row-major int8 codes [M, K] of an 8-bit activation buffer (diagnostic)."""
+    _dev(Xq8, "Xq8", torch.uint8)
+    out = torch.empty((M, K), dtype=torch.int8, device=Xq8.device)
+    _check(_lib.clq_unswizzle_act8(_ptr(Xq8), M, K, _ptr(out), _stream(stream)), "clq_unswizzle_act8")
+    return out
+
+
+def clq_unswizzle_weights8(qw, stream=None):
+    """Row-major int8 codes [N, K] of an 8-bit QWeight (diagnostic)."""
+    out = torch.empty((qw.N, qw.K), dtype=torch.int8, device=qw.wq.device)
+    _check(_lib.clq_unswizzle_weights8(_ptr(qw.wq), qw.N, qw.K, _ptr(out), _stream(stream)),
+           "clq_unswizzle_weights8")
+    return out

@@ -9,7 +9,7 @@
 
 namespace {
 
-constexpr int kVersion = 4;
+constexpr int kVersion = 5;
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxRows = 2147483647;
 
@@ -46,7 +46,7 @@ const char *clq_status_string(clq_status s) {
         case CLQ_ERR_SHAPE: return "CLQ_ERR_SHAPE: a size or row stride is out of range";
         case CLQ_ERR_BLOCK: return "CLQ_ERR_BLOCK: block must be 32, 64 or 128 and divide K";
         case CLQ_ERR_ALIGN: return "CLQ_ERR_ALIGN: a pointer is misaligned";
-        case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio outside [2^-24, 1], or an unknown metric";
+        case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio outside [2^-24, 1], or an unknown metric or wbits";
         case CLQ_ERR_HIP: return "CLQ_ERR_HIP: a HIP launch failed";
         case CLQ_ERR_WORKSPACE: return "CLQ_ERR_WORKSPACE: workspace smaller than the entry point's *_workspace_bytes()";
     }
@@ -185,6 +185,99 @@ clq_status clq_obs_permutation(const float *scores, int64_t D, int32_t *perm, hi
     if (D < 2 || D > 65536 || D % 2 != 0) return CLQ_ERR_SHAPE;
     if (!aligned(scores, 4) || !aligned(perm, 4)) return CLQ_ERR_ALIGN;
     return from_hip(clq::launch_obs_permutation(scores, (int)D, perm, stream));
+}
+
+/* ---- 8-bit activations (W4A8, W8A8) -------------------------------------- */
+
+size_t clq_act8_bytes(int64_t M, int64_t K) {
+    if (check_rows(M) != CLQ_OK || check_k(K) != CLQ_OK) return 0;
+    return (size_t)clq::padded_act_rows(M) * (size_t)K;
+}
+
+size_t clq_weight8_bytes(int64_t N, int64_t K) {
+    if (check_rows(N) != CLQ_OK || check_k(K) != CLQ_OK) return 0;
+    return (size_t)clq::padded_rows(N) * (size_t)K;
+}
+
+clq_status clq_rotate_quant_act8(const void *X, int64_t ldx, const int32_t *perm, int64_t M,
+                                 int64_t K, int32_t block, void *Xq8, float *x_scale,
+                                 hipStream_t stream) {
+    if (!X || !Xq8 || !x_scale) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (ldx < K || ldx % 8 != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(X, 16) || !aligned(Xq8, 16) || !aligned(x_scale, 4) || (perm && !aligned(perm, 4)))
+        return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_rotate_quant(
+        static_cast<const uint16_t *>(X), ldx, perm, M, clq::padded_act_rows(M), (int)K, block, 1.0f,
+        false, 1.0f, static_cast<uint8_t *>(Xq8), x_scale, stream, 8));
+}
+
+clq_status clq_quantize_weights8(const void *W, const int32_t *perm, int64_t N, int64_t K,
+                                 int32_t block, float clip_ratio, void *Wq8, float *w_scale,
+                                 hipStream_t stream) {
+    if (!W || !Wq8 || !w_scale) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (!(clip_ratio >= 0x1p-24f && clip_ratio <= 1.0f)) return CLQ_ERR_ARG;
+    if (!aligned(W, 16) || !aligned(Wq8, 16) || !aligned(w_scale, 4) || (perm && !aligned(perm, 4)))
+        return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_rotate_quant(
+        static_cast<const uint16_t *>(W), K, perm, N, clq::padded_rows(N), (int)K, block, clip_ratio,
+        true, 1.0f / (float)block, static_cast<uint8_t *>(Wq8), w_scale, stream, 8));
+}
+
+static clq_status check_a8(const void *Xq8, const void *Wq, int32_t wbits, int64_t M, int64_t N,
+                           int64_t K, const void *Y, int64_t ld, int64_t ld_mult) {
+    if (!Xq8 || !Wq || !Y) return CLQ_ERR_NULL;
+    if (wbits != 4 && wbits != 8) return CLQ_ERR_ARG;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (ld < N || ld % ld_mult != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(Xq8, 16) || !aligned(Wq, 16) || !aligned(Y, 16)) return CLQ_ERR_ALIGN;
+    return CLQ_OK;
+}
+
+clq_status clq_a8_linear(const void *Xq8, const float *x_scale, const void *Wq, const float *w_scale,
+                         int32_t wbits, const void *bias, int64_t M, int64_t N, int64_t K, void *Y,
+                         int64_t ldy, hipStream_t stream) {
+    if (!x_scale || !w_scale) return CLQ_ERR_NULL;
+    clq_status s = check_a8(Xq8, Wq, wbits, M, N, K, Y, ldy, 8);
+    if (s != CLQ_OK) return s;
+    if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2))) return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_a8_gemm(static_cast<const uint8_t *>(Xq8), x_scale,
+                                        static_cast<const uint8_t *>(Wq), wbits, w_scale,
+                                        static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy, false,
+                                        stream));
+}
+
+clq_status clq_a8_accum_i32(const void *Xq8, const void *Wq, int32_t wbits, int64_t M, int64_t N,
+                            int64_t K, int32_t *acc, int64_t ldacc, hipStream_t stream) {
+    clq_status s = check_a8(Xq8, Wq, wbits, M, N, K, acc, ldacc, 4);
+    if (s != CLQ_OK) return s;
+    return from_hip(clq::launch_a8_gemm(static_cast<const uint8_t *>(Xq8), nullptr,
+                                        static_cast<const uint8_t *>(Wq), wbits, nullptr, nullptr, M, N,
+                                        (int)K, acc, ldacc, true, stream));
+}
+
+clq_status clq_unswizzle_act8(const void *Xq8, int64_t M, int64_t K, void *codes, hipStream_t stream) {
+    if (!Xq8 || !codes) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (!aligned(Xq8, 16)) return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_unswizzle8(static_cast<const uint8_t *>(Xq8), M, (int)K, false,
+                                           static_cast<int8_t *>(codes), stream));
+}
+
+clq_status clq_unswizzle_weights8(const void *Wq8, int64_t N, int64_t K, void *codes, hipStream_t stream) {
+    if (!Wq8 || !codes) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (!aligned(Wq8, 16)) return CLQ_ERR_ALIGN;
+    return from_hip(clq::launch_unswizzle8(static_cast<const uint8_t *>(Wq8), N, (int)K, true,
+                                           static_cast<int8_t *>(codes), stream));
 }
 
 }  // extern "C"

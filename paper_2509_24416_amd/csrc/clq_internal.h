@@ -50,10 +50,43 @@ __host__ __device__ inline int64_t xq_chunk_offset(int64_t r, int64_t c, int64_t
     return (((r >> 5) * (K >> 6) + (c >> 1)) * 64 + (c & 1) * 32 + (r & 31)) * 16;
 }
 
+// int8 code layout (8-bit activations and weights, the W4A8 / W8A8 paths).
+// A unit is 32 rows x 64 codes (2 KB).  Its first KB holds the unit's first
+// 32x32x32 int8 matrix-core operand, its second KB the second: lane
+// l = 32h + rho (16 bytes) of operand q carries codes 32h + 16q + t,
+// t = 0..15, of fragment row rho, the even t in bytes 0..7 and the odd t in
+// bytes 8..15 -- the byte order in which 4-bit operands are widened, so that
+// 8-bit and 4-bit operands pair code for code.  Units are stored [row unit]
+// [k unit].  Activations: rho = row % 32, rows padded to a multiple of 32.
+// Weights: the fragment-row order of the 4-bit weights (wq_rho), rows padded
+// to a multiple of 64.
+__host__ __device__ inline int wq_rho(int w) {
+    const int h = w >> 4, g = (w >> 2) & 3, i = w & 3;
+    return 8 * g + 4 * h + i;
+}
+
+// Byte offset of the 16-byte operand piece q (0 or 1) of 32-code chunk c of
+// fragment row rho in row unit u.
+__host__ __device__ inline int64_t q8_piece_offset(int64_t u, int rho, int64_t c, int q, int64_t K) {
+    return ((u * (K >> 6) + (c >> 1)) * 2 + q) * 1024 + (32 * (c & 1) + rho) * 16;
+}
+
+// bits: 4 (packed int4 layouts above) or 8 (int8 layout).
 hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
                                int64_t rows, int64_t rows_alloc, int K, int block,
                                float alpha, bool weight_mode, float post_scale,
-                               uint8_t *out, float *scale, hipStream_t stream);
+                               uint8_t *out, float *scale, hipStream_t stream, int bits = 4);
+
+// canonical int8 codes [rows][K] of an int8-layout buffer (weights: the
+// fragment-row order undone)
+hipError_t launch_unswizzle8(const uint8_t *q8, int64_t rows, int K, bool weights, int8_t *out,
+                             hipStream_t stream);
+
+// W4A8 (wbits 4: Wq in the packed int4 weight layout) or W8A8 (wbits 8: Wq
+// in the int8 layout) GEMM with int8 activations; no workspace.
+hipError_t launch_a8_gemm(const uint8_t *Xq8, const float *xs, const uint8_t *Wq, int wbits,
+                          const float *ws, const uint16_t *bias, int64_t M, int64_t N, int K,
+                          void *Y, int64_t ldy, bool i32out, hipStream_t stream);
 
 hipError_t launch_unswizzle(const uint8_t *Wq, int64_t N, int K, uint8_t *out,
                             hipStream_t stream);

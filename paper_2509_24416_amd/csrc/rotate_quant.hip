@@ -37,6 +37,16 @@ namespace {
 
 constexpr float kMagic = 12582920.0f;  // 1.5 * 2^23 + 8
 
+// n-bit grid of Eq. (1): codes in [-qmax, qmax], qmax = 2^(n-1) - 1; the
+// magic constant 1.5 * 2^23 + 2^(n-1) leaves code + 2^(n-1) in the low n
+// bits of the fma result (bits n..21 clear).
+template <int QB>
+struct Grid {
+    static_assert(QB == 4 || QB == 8, "4- or 8-bit codes");
+    static constexpr float qmax = QB == 4 ? 7.0f : 127.0f;
+    static constexpr float magic = QB == 4 ? 12582920.0f : 12583040.0f;
+};
+
 // Slot of 16-byte chunk i of Hadamard block j inside its block's span in
 // LDS.  Eight consecutive lanes own eight consecutive blocks and read chunk i
 // at the same time; the XOR spreads those reads over distinct banks.
@@ -79,13 +89,52 @@ __device__ __forceinline__ uint32_t pack8(const uint32_t *w) {
     return __builtin_amdgcn_perm(q47, q03, 0x05040100u) ^ 0x88888888u;
 }
 
+// Sixteen quantized words (code + 128 in bits 0..7, bits 8..21 clear) into
+// one 16-byte int8 operand piece: codes 0, 2, ..., 14 in bytes 0..7, codes 1,
+// 3, ..., 15 in bytes 8..15 (the order of the widened 4-bit operands), two's
+// complement.
+__device__ __forceinline__ uint4 pack16_q8(const uint32_t *w) {
+    auto four = [](uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+        const uint32_t ab = __builtin_amdgcn_perm(b, a, 0x0c0c0400u);
+        const uint32_t cd = __builtin_amdgcn_perm(d, c, 0x0c0c0400u);
+        return __builtin_amdgcn_perm(cd, ab, 0x05040100u) ^ 0x80808080u;
+    };
+    return make_uint4(four(w[0], w[2], w[4], w[6]), four(w[8], w[10], w[12], w[14]),
+                      four(w[1], w[3], w[5], w[7]), four(w[9], w[11], w[13], w[15]));
+}
+
+// The int8 codes of one lane's b-element block (codes 32c .. of the row's
+// 32-code chunks j * b/32 + c): two 16-byte operand pieces per chunk.
+template <int B, bool WEIGHT>
+__device__ __forceinline__ void store_q8(const float *x, float rc, int64_t grow, int j, int K,
+                                         uint8_t *__restrict__ out) {
+    constexpr float M = Grid<8>::magic, Q = Grid<8>::qmax;
+    const int64_t u = grow >> 5;
+    const int rho = WEIGHT ? wq_rho((int)(grow & 31)) : (int)(grow & 31);
+#pragma unroll
+    for (int c = 0; c < B / 32; ++c) {
+        const int64_t c32 = (int64_t)j * (B / 32) + c;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            uint32_t w[16];
+#pragma unroll
+            for (int t = 0; t < 16; ++t) {
+                float v = __builtin_fmaf(x[32 * c + 16 * q + t], rc, M);
+                if constexpr (WEIGHT) v = __builtin_amdgcn_fmed3f(v, M - Q, M + Q);
+                w[t] = __float_as_uint(v);
+            }
+            *reinterpret_cast<uint4 *>(out + q8_piece_offset(u, rho, c32, q, K)) = pack16_q8(w);
+        }
+    }
+}
+
 // Lanes per workgroup never exceed 512 for b >= 64 (at most 512 blocks per
 // row, and rows are only batched up to 512 lanes), which lets the compiler
 // keep a 128-element block in registers.
 template <int B>
 constexpr int rq_max_threads() { return B == 32 ? 1024 : 512; }
 
-template <int B, bool WEIGHT>
+template <int B, bool WEIGHT, int QB>
 __global__ void __launch_bounds__(rq_max_threads<B>())
 rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
                     const int32_t *__restrict__ perm, int64_t rows_valid,
@@ -179,9 +228,13 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
     // 3. per-row scale and codes
     const float a = __uint_as_float(rowmax[r]);
     const float ac = WEIGHT ? alpha * a : a;
-    const float rc = (ac == 0.0f) ? 0.0f : 7.0f / ac;
+    const float rc = (ac == 0.0f) ? 0.0f : Grid<QB>::qmax / ac;
     const int64_t grow = row0 + r;
-    if (j == 0 && grow < rows_valid) scale_out[grow] = (ac / 7.0f) * post_scale;
+    if (j == 0 && grow < rows_valid) scale_out[grow] = (ac / Grid<QB>::qmax) * post_scale;
+    if constexpr (QB == 8) {
+        store_q8<B, WEIGHT>(x, rc, grow, j, K, out);
+        return;
+    }
 
     uint32_t words[B / 8];
 #pragma unroll
@@ -222,7 +275,7 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
 // barrier per batch: before it, block maxima meet in rowmax[i % 3]; after it,
 // codes are formed and stored.  The third rowmax buffer is cleared one batch
 // after its use, when no lane can still be reading it.
-template <int B>
+template <int B, int QB>
 __global__ void __launch_bounds__(256)
 rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__restrict__ perm,
               int64_t rows_valid, int64_t rows_alloc, int64_t nbatch, int K, int R,
@@ -347,10 +400,14 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
         if (t < R) rowmax[((i + 2) % 3) * R + t] = 0u;
         if (!active) continue;
         const float a = __uint_as_float(rm[r]);
-        const float rc = (a == 0.0f) ? 0.0f : 7.0f / a;
+        const float rc = (a == 0.0f) ? 0.0f : Grid<QB>::qmax / a;
         const int64_t grow = b * R + r;
         if (grow >= rows_alloc) continue;   // past the padded rows
-        if (j == 0 && grow < rows_valid) scale_out[grow] = a / 7.0f;
+        if (j == 0 && grow < rows_valid) scale_out[grow] = a / Grid<QB>::qmax;
+        if constexpr (QB == 8) {
+            store_q8<B, false>(x, rc, grow, j, K, out);
+            continue;
+        }
         uint32_t words[B / 8];
 #pragma unroll
         for (int g = 0; g < B / 8; ++g) {
@@ -384,7 +441,7 @@ int pick_rows(int K, int block) {
     return best;
 }
 
-template <int B, bool WEIGHT>
+template <int B, bool WEIGHT, int QB>
 hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
                      int64_t rows_valid, int64_t rows_alloc, int K, float alpha,
                      float post_scale, uint8_t *out, float *scale, hipStream_t stream) {
@@ -395,13 +452,13 @@ hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
     const size_t lds = (size_t)R * K * 2 + (size_t)R * 4;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)rotate_quant_kernel<B, WEIGHT>,
+        hipError_t e = hipFuncSetAttribute((const void *)rotate_quant_kernel<B, WEIGHT, QB>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 65536 + 4096);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const int64_t grid = (rows_alloc + R - 1) / R;
-    hipLaunchKernelGGL((rotate_quant_kernel<B, WEIGHT>), dim3((unsigned)grid), dim3(T), lds,
+    hipLaunchKernelGGL((rotate_quant_kernel<B, WEIGHT, QB>), dim3((unsigned)grid), dim3(T), lds,
                        stream, X, ldx, perm, rows_valid, rows_alloc, K, R, alpha, post_scale,
                        out, scale);
     return hipGetLastError();
@@ -422,7 +479,7 @@ int pick_act_rows(int K, int block) {
     return best;
 }
 
-template <int B>
+template <int B, int QB>
 hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, int64_t rows_valid,
                          int64_t rows_alloc, int K, uint8_t *out, float *scale, hipStream_t stream) {
     const int R = pick_act_rows(K, B);
@@ -431,7 +488,7 @@ hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, in
     const size_t lds = (size_t)2 * R * K * 2 + (size_t)3 * R * 4;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)rq_act_kernel<B>,
+        hipError_t e = hipFuncSetAttribute((const void *)rq_act_kernel<B, QB>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 65536 + 4096);
         if (e != hipSuccess) return e;
         attr_set = true;
@@ -444,11 +501,11 @@ hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, in
             cus = 256;
     }
     if ((int64_t)R * ldx > INT32_MAX)   // 32-bit in-batch offsets: very wide strides take the one-shot kernel
-        return launch_rq<B, false>(X, ldx, perm, rows_valid, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
+        return launch_rq<B, false, QB>(X, ldx, perm, rows_valid, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
     const int64_t nbatch = (rows_alloc + R - 1) / R;
     const int per_cu = (int)std::min<size_t>(4, (160 * 1024) / lds);
     const int64_t grid = std::min<int64_t>(nbatch, (int64_t)cus * per_cu);
-    hipLaunchKernelGGL((rq_act_kernel<B>), dim3((unsigned)grid), dim3(T), lds, stream, X, ldx, perm,
+    hipLaunchKernelGGL((rq_act_kernel<B, QB>), dim3((unsigned)grid), dim3(T), lds, stream, X, ldx, perm,
                        rows_valid, rows_alloc, nbatch, K, R, out, scale);
     return hipGetLastError();
 }
@@ -473,25 +530,66 @@ __global__ void unswizzle_act_kernel(const uint8_t *__restrict__ Xq, int64_t M, 
     *reinterpret_cast<uint4 *>(out + r * (K / 2) + c * 16) = v;
 }
 
+// one 16-byte operand piece per thread, scattered back to canonical codes
+__global__ void unswizzle8_kernel(const uint8_t *__restrict__ q8, int64_t rows, int K, bool weights,
+                                  int8_t *__restrict__ out) {
+    const int64_t cpr = K / 32;   // 32-code chunks per row
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= rows * cpr * 2) return;
+    const int q = (int)(idx & 1);
+    const int64_t rc = idx >> 1, r = rc / cpr, c = rc - r * cpr;
+    const int rho = weights ? wq_rho((int)(r & 31)) : (int)(r & 31);
+    const uint4 v = *reinterpret_cast<const uint4 *>(q8 + q8_piece_offset(r >> 5, rho, c, q, K));
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    int8_t *dst = out + r * K + c * 32 + q * 16;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+        const int byte = (t & 1) * 8 + (t >> 1);
+        dst[t] = (int8_t)(w[byte >> 2] >> (8 * (byte & 3)));
+    }
+}
+
 }  // namespace
+
+hipError_t launch_unswizzle8(const uint8_t *q8, int64_t rows, int K, bool weights, int8_t *out,
+                             hipStream_t stream) {
+    const int64_t total = rows * (K / 32) * 2;
+    hipLaunchKernelGGL(unswizzle8_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                       q8, rows, K, weights, out);
+    return hipGetLastError();
+}
+
+template <int QB>
+hipError_t launch_rq_bits(const uint16_t *X, int64_t ldx, const int32_t *perm,
+                          int64_t rows, int64_t rows_alloc, int K, int block,
+                          float alpha, bool weight_mode, float post_scale,
+                          uint8_t *out, float *scale, hipStream_t stream) {
+    if (weight_mode) {
+        switch (block) {
+            case 32: return launch_rq<32, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
+            case 64: return launch_rq<64, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
+            case 128: return launch_rq<128, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
+        }
+    } else {
+        switch (block) {
+            case 32: return launch_rq_act<32, QB>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
+            case 64: return launch_rq_act<64, QB>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
+            case 128: return launch_rq_act<128, QB>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
+        }
+    }
+    return hipErrorInvalidValue;
+}
 
 hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
                                int64_t rows, int64_t rows_alloc, int K, int block,
                                float alpha, bool weight_mode, float post_scale,
-                               uint8_t *out, float *scale, hipStream_t stream) {
-    if (weight_mode) {
-        switch (block) {
-            case 32: return launch_rq<32, true>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
-            case 64: return launch_rq<64, true>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
-            case 128: return launch_rq<128, true>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
-        }
-    } else {
-        switch (block) {
-            case 32: return launch_rq_act<32>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
-            case 64: return launch_rq_act<64>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
-            case 128: return launch_rq_act<128>(X, ldx, perm, rows, rows_alloc, K, out, scale, stream);
-        }
-    }
+                               uint8_t *out, float *scale, hipStream_t stream, int bits) {
+    if (bits == 8)
+        return launch_rq_bits<8>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
+                                 out, scale, stream);
+    if (bits == 4)
+        return launch_rq_bits<4>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
+                                 out, scale, stream);
     return hipErrorInvalidValue;
 }
 

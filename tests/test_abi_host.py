@@ -49,12 +49,22 @@ def lib():
     L.clq_obs_workspace_bytes.argtypes = [i64, i64, i32]
     L.clq_obs_channel_scores.argtypes = [p, i64, i64, i64, i64, i32, p, ctypes.c_size_t, p, p]
     L.clq_obs_permutation.argtypes = [p, i64, p, p]
+    L.clq_act8_bytes.restype = ctypes.c_size_t
+    L.clq_act8_bytes.argtypes = [i64, i64]
+    L.clq_weight8_bytes.restype = ctypes.c_size_t
+    L.clq_weight8_bytes.argtypes = [i64, i64]
+    L.clq_rotate_quant_act8.argtypes = [p, i64, p, i64, i64, i32, p, p, p]
+    L.clq_quantize_weights8.argtypes = [p, p, i64, i64, i32, f32, p, p, p]
+    L.clq_a8_linear.argtypes = [p, p, p, p, i32, p, i64, i64, i64, p, i64, p]
+    L.clq_a8_accum_i32.argtypes = [p, p, i32, i64, i64, i64, p, i64, p]
+    L.clq_unswizzle_act8.argtypes = [p, i64, i64, p, p]
+    L.clq_unswizzle_weights8.argtypes = [p, i64, i64, p, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 22, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -66,7 +76,7 @@ def test_binding_names_match_header():
 
 
 def test_version_and_strings(lib):
-    assert lib.clq_version() == 4
+    assert lib.clq_version() == 5
     for code in range(8):
         s = lib.clq_status_string(code).decode()
         assert s.startswith("CLQ")
@@ -221,3 +231,39 @@ def test_obs_validation(lib):
     assert g(A, 0, A, None) == SHAPE
     assert g(A, 65538, A, None) == SHAPE
     assert g(A + 2, 64, A, None) == ALIGN
+
+
+def test_8bit_sizes(lib):
+    assert lib.clq_act8_bytes(1, 64) == 32 * 64
+    assert lib.clq_act8_bytes(8192, 1152) == 8192 * 1152
+    assert lib.clq_act8_bytes(33, 1152) == 64 * 1152
+    assert lib.clq_weight8_bytes(1, 64) == 64 * 64
+    assert lib.clq_weight8_bytes(3456, 1152) == 3456 * 1152
+    assert lib.clq_act8_bytes(0, 1152) == 0 and lib.clq_weight8_bytes(8, 100) == 0
+
+
+def test_8bit_validation(lib):
+    f = lib.clq_rotate_quant_act8
+    assert f(None, 1152, None, 4, 1152, 64, A, A, None) == NULL
+    assert f(A, 1152, None, 4, 1152, 48, A, A, None) == BLOCK
+    assert f(A, 1000, None, 4, 1152, 64, A, A, None) == SHAPE
+    assert f(A, 1152, None, 4, 1000, 64, A, A, None) == SHAPE
+    assert f(A + 8, 1152, None, 4, 1152, 64, A, A, None) == ALIGN
+    g = lib.clq_quantize_weights8
+    assert g(A, None, 8, 1152, 64, 0.0, A, A, None) == ARG
+    assert g(A, None, 8, 1152, 64, 1.5, A, A, None) == ARG
+    assert g(A, None, 8, 1152, 64, 1.0, A + 4, A, None) == ALIGN
+    h = lib.clq_a8_linear
+    assert h(A, A, A, A, 4, None, 4, 8, 1152, None, 8, None) == NULL
+    assert h(A, None, A, A, 4, None, 4, 8, 1152, A, 8, None) == NULL
+    assert h(A, A, A, A, 5, None, 4, 8, 1152, A, 8, None) == ARG
+    assert h(A, A, A, A, 8, None, 0, 8, 1152, A, 8, None) == SHAPE
+    assert h(A, A, A, A, 8, None, 4, 8, 1100, A, 8, None) == SHAPE
+    assert h(A, A, A, A, 8, None, 4, 12, 1152, A, 12, None) == SHAPE       # ldy % 8
+    assert h(A, A, A, A, 4, None, 4, 8, 1152, A + 8, 8, None) == ALIGN
+    assert h(A, A, A, A, 4, A + 1, 4, 8, 1152, A, 8, None) == ALIGN        # bias
+    k = lib.clq_a8_accum_i32
+    assert k(A, A, 4, 4, 8, 1152, A, 6, None) == SHAPE                     # ldacc % 4
+    assert k(A, A, 0, 4, 8, 1152, A, 8, None) == ARG
+    assert lib.clq_unswizzle_act8(None, 4, 1152, A, None) == NULL
+    assert lib.clq_unswizzle_weights8(A, 4, 100, A, None) == SHAPE
