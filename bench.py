@@ -41,10 +41,11 @@ HBM_PEAK_GBPS = 8000.0       # HBM3E, MI355X
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic_pixart_block_m8192.txt")
 
 
-def rq_bytes(l):
+def rq_bytes(l, abits=4):
     """Algorithmic HBM bytes of one rotate+quant launch: read M*K fp16, write
-    M*K/2 packed codes and M fp32 scales."""
-    return l.M * (2 * l.K + l.K // 2 + 4)
+    M*K/2 packed int4 codes (M*K int8 codes for 8-bit activations) and M fp32
+    scales."""
+    return l.M * (2 * l.K + (l.K // 2 if abits == 4 else l.K) + 4)
 
 
 def gemm_ops(l):
@@ -77,7 +78,7 @@ def kernel_sha():
     return h.hexdigest()[:16]
 
 
-def cpu_baseline(layers, inputs, budget_s=15.0):
+def cpu_baseline(layers, inputs, budget_s=15.0, wbits=4, abits=4):
     """Times the CPU oracle's online path (rotate + quantize the activations,
     integer GEMM, fp64 epilogue) on a sample of token rows of every layer,
     sized to roughly budget_s seconds; returns TOPS on that sample."""
@@ -86,14 +87,14 @@ def cpu_baseline(layers, inputs, budget_s=15.0):
     wq = {}
     for l in layers:  # offline step, not timed (as on the GPU)
         _, W, b = inputs[l.name]
-        wq[l.name] = oracle.quantize_weights(W, l.block)
+        wq[l.name] = oracle.quantize_weights(W, l.block, bits=wbits)
 
     def run(rows):
         ops = 0
         t0 = time.perf_counter()
         for l in layers:
             X, _, b = inputs[l.name]
-            _, xc, xs = oracle.quantize_act(X[:rows], l.block)
+            _, xc, xs = oracle.quantize_act(X[:rows], l.block, bits=abits)
             _, wc, ws = wq[l.name]
             acc = oracle.gemm_i32(xc, wc)
             oracle.epilogue(acc, xs, ws, b)
@@ -206,8 +207,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--cold-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", default="pixart_block", choices=["pixart_block", "obs_calibration"],
-                    help="pixart_block: the W4A4 linear hot path (default); obs_calibration: the OBS "
+    ap.add_argument("--workload", default="pixart_block",
+                    choices=["pixart_block", "pixart_block_w4a8", "pixart_block_w8a8", "obs_calibration"],
+                    help="pixart_block: the W4A4 linear hot path (default); pixart_block_w4a8 / _w8a8: the "
+                         "same block at 8-bit activations (and weights); obs_calibration: the OBS "
                          "channel-score pass over a calibration batch")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (reference for the HBM "
@@ -240,15 +243,23 @@ def main():
     wl = workloads.C2
     layers = list(wl.layers)
     inputs = {l.name: workloads.layer_inputs(l) for l in layers}
+    # bit setting (Sec. 4.1: W4A4, W4A8, W8A8)
+    wbits, abits = {"pixart_block": (4, 4), "pixart_block_w4a8": (4, 8),
+                    "pixart_block_w8a8": (8, 8)}[args.workload]
+    quant_w = clq.clq_quantize_weights if wbits == 4 else clq.clq_quantize_weights8
+    if abits == 4:
+        act_bytes, rq_fn, lin_fn = clq.clq_act_bytes, clq.clq_rotate_quant_act, clq.clq_w4a4_linear
+    else:
+        act_bytes, rq_fn, lin_fn = clq.clq_act8_bytes, clq.clq_rotate_quant_act8, clq.clq_a8_linear
 
     # resident device data; weights quantized once (offline step)
     state = []
     for l in layers:
         X, W, b = inputs[l.name]
         Xd = torch.from_numpy(X).to(dev)
-        qw = clq.clq_quantize_weights(torch.from_numpy(W).to(dev), l.block)
+        qw = quant_w(torch.from_numpy(W).to(dev), l.block)
         bd = torch.from_numpy(b).to(dev)
-        Xq = torch.empty(clq.clq_act_bytes(l.M, l.K), dtype=torch.uint8, device=dev)
+        Xq = torch.empty(act_bytes(l.M, l.K), dtype=torch.uint8, device=dev)
         xs = torch.empty(l.M, dtype=torch.float32, device=dev)
         Y = torch.empty((l.M, l.N), dtype=torch.float16, device=dev)
         state.append((l, Xd, qw, bd, Xq, xs, Y))
@@ -259,10 +270,10 @@ def main():
         for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
             if events is not None:
                 events[i][0].record(stream)
-            clq.clq_rotate_quant_act(Xd, l.block, out=Xq, scale_out=xs)
+            rq_fn(Xd, l.block, out=Xq, scale_out=xs)
             if events is not None:
                 events[i][1].record(stream)
-            clq.clq_w4a4_linear(Xq, xs, qw, bd, out=Y)
+            lin_fn(Xq, xs, qw, bd, out=Y)
             if events is not None:
                 events[i][2].record(stream)
 
@@ -303,8 +314,8 @@ def main():
     gemm_avg_ms = float(gemm_ms.mean())
     gemm_ops_per_launch = total_ops / len(layers)
     achieved = gemm_ops_per_launch / (gemm_avg_ms * 1e-3) / 1e12
-    rq_gbps = [rq_bytes(l) / (rq_ms[i] * 1e-3) / 1e9 for i, l in enumerate(layers)]
-    rq_avg_bytes = sum(rq_bytes(l) for l in layers) / len(layers)
+    rq_gbps = [rq_bytes(l, abits) / (rq_ms[i] * 1e-3) / 1e9 for i, l in enumerate(layers)]
+    rq_avg_bytes = sum(rq_bytes(l, abits) for l in layers) / len(layers)
     rq_achieved = rq_avg_bytes / (float(rq_ms.mean()) * 1e-3) / 1e9
 
     # rotate+quant and GEMM with the Infinity Cache flushed before each launch
@@ -319,13 +330,13 @@ def main():
         for _ in range(args.cold_reps):
             flush.sum()
             e0.record(stream)
-            clq.clq_rotate_quant_act(Xd, l.block, out=Xq, scale_out=xs)
+            rq_fn(Xd, l.block, out=Xq, scale_out=xs)
             e1.record(stream)
             e1.synchronize()
             t_rq.append(e0.elapsed_time(e1))
             flush.sum()
             e0.record(stream)
-            clq.clq_w4a4_linear(Xq, xs, qw, bd, out=Y)
+            lin_fn(Xq, xs, qw, bd, out=Y)
             e1.record(stream)
             e1.synchronize()
             t_g.append(e0.elapsed_time(e1))
@@ -333,9 +344,10 @@ def main():
         cold_gemm[i] = np.median(t_g)
     del flush
 
-    traffic = load_traffic(kernel_sha())
+    traffic = load_traffic(kernel_sha()) if (wbits, abits) == (4, 4) else None
+    setting = f"W{wbits}A{abits}"
     out = {
-        "metric": "W4A4 linear effective TOPS + % int8-MFMA peak; rotate+quant HBM GB/s",
+        "metric": f"{setting} linear effective TOPS + % int8-MFMA peak; rotate+quant HBM GB/s",
         "value": round(value, 2),
         "unit": "TOPS",
         "n_gpus": 1,
@@ -345,23 +357,26 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int4",
+        "dtype": "int4" if (wbits, abits) == (4, 4) else ("int4 x int8" if wbits == 4 else "int8"),
         "data": "synthetic",
-        "config": {"workload": wl.name, "M": layers[0].M, "hidden": 1152, "mlp": 4608,
+        "config": {"workload": wl.name + ("" if abits == 4 else f"_{setting.lower()}"), "M": layers[0].M,
+                   "hidden": 1152, "mlp": 4608,
                    "block": 64, "layers": {l.name.split(".")[1]: [l.K, l.N] for l in layers},
                    "parallelism": "none (one GPU)"},
         "pct_int8_peak": round(100 * value / INT8_PEAK_TOPS, 2),
-        "roofline": {"kernel": "w4a4_gemm_kernel (128 ch x 256 tok tiles, 2 per CU)", "bound": "mfma", "achieved": round(achieved, 1),
+        "roofline": {"kernel": ("w4a4_gemm_kernel (128 ch x 256 tok tiles, 2 per CU)" if abits == 4 else
+                                f"a8_gemm_kernel<{wbits}> (128 ch x 128 tok tiles)"),
+                     "bound": "mfma", "achieved": round(achieved, 1),
                      "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / INT8_PEAK_TOPS, 4),
                      "traffic": traffic, "avg_launch_us": round(gemm_avg_ms * 1e3, 2),
                      "ops_per_launch": gemm_ops_per_launch},
-        "rotate_quant": {"kernel": "rq_act_kernel<64>", "bound": "hbm",
+        "rotate_quant": {"kernel": f"rq_act_kernel<64, {abits}>", "bound": "hbm",
                          "achieved": round(rq_achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": round(rq_achieved / HBM_PEAK_GBPS, 4),
                          "avg_launch_us": round(float(rq_ms.mean()) * 1e3, 2),
                          "bytes_per_launch": rq_avg_bytes,
-                         "cold_cache_GBps": {l.name: round(rq_bytes(l) / (cold_rq[i] * 1e-3) / 1e9, 1)
+                         "cold_cache_GBps": {l.name: round(rq_bytes(l, abits) / (cold_rq[i] * 1e-3) / 1e9, 1)
                                              for i, l in enumerate(layers)}},
         "per_layer": {l.name: {"gemm_us": round(gemm_ms[i] * 1e3, 2), "gemm_TOPS": round(gemm_tops[i], 1),
                                "gemm_cold_us": round(cold_gemm[i] * 1e3, 2),
@@ -371,7 +386,7 @@ def main():
         "gpu": torch.cuda.get_device_name(dev),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers, inputs)
+        out["cpu_baseline"] = cpu_baseline(layers, inputs, wbits=wbits, abits=abits)
     print(json.dumps(out), flush=True)
 
 
