@@ -58,7 +58,7 @@ typedef enum {
     CLQ_ERR_SHAPE = 2, /* M, N, K, ld* out of range or not multiples         */
     CLQ_ERR_BLOCK = 3, /* block not in {32, 64, 128} or K % block != 0       */
     CLQ_ERR_ALIGN = 4, /* a pointer is not aligned as required               */
-    CLQ_ERR_ARG = 5,   /* clip_ratio outside [2^-24, 1], unknown metric or wbits */
+    CLQ_ERR_ARG = 5,   /* clip_ratio, metric, wbits, gamma or grid out of range */
     CLQ_ERR_HIP = 6,   /* a HIP launch failed (see hipGetLastError)           */
     CLQ_ERR_WORKSPACE = 7 /* workspace smaller than the *_workspace_bytes() query */
 } clq_status;
@@ -261,6 +261,42 @@ clq_status clq_obs_channel_scores(const void *X, int64_t ldx, int64_t B, int64_t
  *           ascending order (x'[k] = x[perm[k]]). */
 clq_status clq_obs_permutation(const float *scores, int64_t D, int32_t *perm,
                                hipStream_t stream);
+
+/* ---- CLPS single-layer clip search (Sec. 3.4 "Cross-Layer Parameter
+ * Searching", Eq. (2); Sec. 4.1: beta = 0, gamma = 0.01, one percentile for
+ * all channels of a matrix) -------------------------------------------------
+ * Grid search of the weight clip ratio alpha (row bound alpha * max|w~|)
+ * that minimises ||Y0 - Yhat_alpha||_F^2 on calibration activations, with
+ * the layer's own unquantised output as the target (the cross-layer target
+ * needs a model).  W4A4, all on the GPU, no host synchronisation:
+ *   window   alpha_lo = min over rows of Q / max|w~_row|, Q the order
+ *            statistic of |w~_row| with floor(gamma (K - 1)) values above
+ *            it (the product in fp64 of gamma and K - 1); rows of zeros
+ *            count as 1.
+ *   grid     alpha_i = 1 - ((1 - alpha_lo)(G - 1 - i)) / (G - 1) in fp32,
+ *            i = 0 .. G-1 (alpha_{G-1} = 1; G = 1 gives alpha = 1).
+ *   error    e_i = sum over m, n of (Y0[m][n] - acc * x_scale[m] *
+ *            w_scale[n])^2 in fp64 (acc the exact integer sums; a bias
+ *            cancels), summed in a fixed order (deterministic).
+ *   choice   best = the smallest e_i, ties to the lower i. */
+
+/* Workspace bytes of clq_clps_search (0 for sizes out of range). */
+size_t clq_clps_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*   X          fp16 [M][K] calibration activations, row stride ldx (>= K,
+ *              multiple of 8), 16-byte aligned.
+ *   W          fp16 [N][K] weights, contiguous, 16-byte aligned; K <= 16384.
+ *   Y0         fp32 [M][N] target output X W^T (no bias), row stride ldy0.
+ *   perm       the gather vector s (int32 [K]) or NULL, as for the hot path.
+ *   gamma      in [0, 1) (0.01 in the paper); grid: 1 .. 256 candidates.
+ *   workspace  clq_clps_workspace_bytes(M, N, K) bytes, 16-byte aligned.
+ *   alphas     out, device fp32 [grid]; errors: out, device fp64 [grid];
+ *   best       out, device int32 [1]. */
+clq_status clq_clps_search(const void *X, int64_t ldx, const void *W, const float *Y0,
+                           int64_t ldy0, const int32_t *perm, int64_t M, int64_t N,
+                           int64_t K, int32_t block, float gamma, int32_t grid,
+                           void *workspace, size_t workspace_bytes, float *alphas,
+                           double *errors, int32_t *best, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -33,8 +33,9 @@ import oracle
 
 def order_index(K, gamma):
     """Position (ascending, 0-based) of the upper gamma order statistic of K
-    values: l = floor(gamma (K - 1)) values lie above it."""
-    return K - 1 - int(math.floor(gamma * (K - 1)))
+    values: l = floor(gamma (K - 1)) values lie above it, gamma taken as an
+    fp32 value and the product formed in fp64."""
+    return K - 1 - int(math.floor(float(np.float32(gamma)) * (K - 1)))
 
 
 def alpha_floor(W, block, perm=None, gamma=0.01):

@@ -17,6 +17,8 @@ carry the names of the C entry points declared in ``include/clq.h``:
     clq_a8_linear(Xq8, x_scale, qw, bias=None)                 -> Y   (W4A8 / W8A8)
     clq_a8_accum_i32(Xq8, x_scale, qw)                         -> acc
     clq_unswizzle_act8(Xq8, M, K), clq_unswizzle_weights8(qw)  -> int8 codes
+    clq_clps_search(X, W, Y0, block, perm=None, gamma=0.01, grid=20)
+                                                               -> (alphas, errors, best)
 
 Paper: "CLQ" (arXiv 2509.24416) -- Sec. 3.3 (online block-Hadamard rotation,
 weights absorb it offline) and Sec. 3.1 Eq. (1) (4-bit quantizer; dynamic
@@ -71,11 +73,15 @@ _lib.clq_a8_linear.argtypes = [_p, _p, _p, _p, _i32, _p, _i64, _i64, _i64, _p, _
 _lib.clq_a8_accum_i32.argtypes = [_p, _p, _i32, _i64, _i64, _i64, _p, _i64, _p]
 _lib.clq_unswizzle_act8.argtypes = [_p, _i64, _i64, _p, _p]
 _lib.clq_unswizzle_weights8.argtypes = [_p, _i64, _i64, _p, _p]
+_lib.clq_clps_workspace_bytes.restype = ctypes.c_size_t
+_lib.clq_clps_workspace_bytes.argtypes = [_i64, _i64, _i64]
+_lib.clq_clps_search.argtypes = [_p, _i64, _p, _p, _i64, _p, _i64, _i64, _i64, _i32, _f32, _i32, _p,
+                                 ctypes.c_size_t, _p, _p, _p, _p]
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
            "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
            "clq_quantize_weights8", "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8",
-           "clq_unswizzle_weights8"):
+           "clq_unswizzle_weights8", "clq_clps_search"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -83,7 +89,8 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_w4a4_linear", "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
            "clq_obs_workspace_bytes", "clq_obs_channel_scores", "clq_obs_permutation",
            "clq_act8_bytes", "clq_weight8_bytes", "clq_rotate_quant_act8", "clq_quantize_weights8",
-           "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8", "clq_unswizzle_weights8")
+           "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8", "clq_unswizzle_weights8",
+           "clq_clps_workspace_bytes", "clq_clps_search")
 
 OBS_METRICS = ("absmax", "range", "par", "topk_mean", "percentile")
 
@@ -439,3 +446,39 @@ def clq_unswizzle_weights8(qw, stream=None):
     _check(_lib.clq_unswizzle_weights8(_ptr(qw.wq), qw.N, qw.K, _ptr(out), _stream(stream)),
            "clq_unswizzle_weights8")
     return out
+
+
+# ---- CLPS single-layer clip search ------------------------------------------------
+
+def clq_clps_workspace_bytes(M, N, K):
+    return int(_lib.clq_clps_workspace_bytes(M, N, K))
+
+
+def clq_clps_search(X, W, Y0, block, perm=None, gamma=0.01, grid=20, workspace=None, stream=None):
+    """Grid search of the weight clip ratio (W4A4) minimising ||Y0 - Yhat||_F^2
+    on calibration activations X fp16 [M, K]; W fp16 [N, K]; Y0 fp32 [M, N]
+    the unquantised output.  Returns device tensors (alphas fp32 [grid],
+    errors fp64 [grid], best int32 [1]); nothing is synchronised."""
+    _dev(X, "X", torch.float16)
+    _dev(W, "W", torch.float16)
+    _dev(Y0, "Y0", torch.float32)
+    if X.dim() != 2 or X.stride(1) != 1 or W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("X must be [M, K] with unit column stride and W contiguous [N, K]")
+    M, K = X.shape
+    N = W.shape[0]
+    if W.shape[1] != K or Y0.dim() != 2 or Y0.shape != (M, N) or Y0.stride(1) != 1:
+        raise ValueError("shapes: X [M, K], W [N, K], Y0 [M, N]")
+    perm = _perm(perm, K)
+    need = clq_clps_workspace_bytes(M, N, K)
+    if need == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_clps_search")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    _dev(workspace, "workspace", torch.uint8)
+    alphas = torch.empty(grid, dtype=torch.float32, device=X.device)
+    errors = torch.empty(grid, dtype=torch.float64, device=X.device)
+    best = torch.empty(1, dtype=torch.int32, device=X.device)
+    _check(_lib.clq_clps_search(_ptr(X), X.stride(0), _ptr(W), _ptr(Y0), Y0.stride(0), _ptr(perm), M, N, K,
+                                block, gamma, grid, _ptr(workspace), workspace.numel(), _ptr(alphas),
+                                _ptr(errors), _ptr(best), _stream(stream)), "clq_clps_search")
+    return alphas, errors, best

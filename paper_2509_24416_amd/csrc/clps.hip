@@ -1,0 +1,228 @@
+// Single-layer CLPS clip search on the GPU (CLQ, arXiv 2509.24416, Sec. 3.4:
+// a grid search of the quantizer bounds between quantiles of the layer's
+// weights that minimises the squared Frobenius norm of the output error,
+// Eq. (2); Sec. 4.1: beta = 0, gamma = 0.01, one percentile for every
+// channel of a matrix).  The target is the layer's own unquantised output;
+// the searched quantity is the weight clip ratio alpha of the hot path
+// (row bound alpha * max|w~_row|).
+//
+// Steps, all on the caller's stream with no host synchronisation:
+//   clps_row_ratio_kernel  per weight row: gather, block FWHT in LDS (the
+//                          same fp32 butterflies as the quantizer), |.|,
+//                          bitonic sort, ratio of the order statistic with
+//                          floor(gamma (K-1)) values above it to the max.
+//   clps_grid_kernel       alpha_lo = min of the row ratios; the G candidates
+//                          alpha_i = 1 - ((1 - alpha_lo)(G-1-i)) / (G-1).
+//   per candidate          the hot path's weight quantizer with alpha_i read
+//                          from device memory, the W4A4 GEMM's exact integer
+//                          sums, then clps_error_kernel: sum over the
+//                          outputs of (Y0 - acc * x_scale * w_scale)^2 in fp64
+//                          (per-workgroup partials in a fixed order, then
+//                          clps_sum_kernel), so results are deterministic.
+//   clps_argmin_kernel     the smallest error, ties to the lower index.
+// The activations are rotated and quantized once.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "clq_internal.h"
+
+namespace clq {
+namespace {
+
+constexpr int kRatioThreads = 256;
+constexpr int kErrBlocks = 1024;
+constexpr int kErrThreads = 256;
+
+// one workgroup per row; LDS holds the row padded to P = 2^ceil(log2 K)
+__global__ void __launch_bounds__(kRatioThreads)
+clps_row_ratio_kernel(const uint16_t *__restrict__ W, const int32_t *__restrict__ perm, int K, int block,
+                      int P, int order_idx, float *__restrict__ ratio)
+{
+    extern __shared__ float w[];   // [P]
+    const int row = blockIdx.x, t = threadIdx.x;
+    const uint16_t *src = W + (int64_t)row * K;
+    for (int i = t; i < P; i += kRatioThreads)
+        w[i] = i < K ? __half2float(__ushort_as_half(src[perm ? perm[i] : i])) : 0.0f;
+    __syncthreads();
+    // block FWHT: stage h pairs (i, i + h) with (i mod 2h) < h, ascending h
+    for (int h = 1; h < block; h <<= 1) {
+        for (int p = t; p < K / 2; p += kRatioThreads) {
+            const int i = (p / h) * 2 * h + (p % h);
+            const float u = w[i], v = w[i + h];
+            w[i] = u + v;
+            w[i + h] = u - v;
+        }
+        __syncthreads();
+    }
+    // magnitudes; padding below every magnitude so it sorts first
+    for (int i = t; i < P; i += kRatioThreads) w[i] = i < K ? fabsf(w[i]) : -1.0f;
+    __syncthreads();
+    for (int k = 2; k <= P; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = t; i < P; i += kRatioThreads) {
+                const int l = i ^ j;
+                if (l > i) {
+                    const float a = w[i], b = w[l];
+                    if ((a > b) == ((i & k) == 0)) {
+                        w[i] = b;
+                        w[l] = a;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    if (t == 0) {
+        const float mx = w[P - 1], q = w[P - K + order_idx];
+        ratio[row] = mx == 0.0f ? 1.0f : q / mx;
+    }
+}
+
+__global__ void __launch_bounds__(256)
+clps_grid_kernel(const float *__restrict__ ratio, int64_t N, int G, float *__restrict__ alphas)
+{
+    __shared__ float red[256];
+    float m = 1.0f;
+    for (int64_t i = threadIdx.x; i < N; i += 256) m = fminf(m, ratio[i]);
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) red[threadIdx.x] = fminf(red[threadIdx.x], red[threadIdx.x + s]);
+        __syncthreads();
+    }
+    const float lo = red[0];
+    for (int i = threadIdx.x; i < G; i += 256) {
+        if (G == 1) {
+            alphas[i] = 1.0f;
+        } else {
+            const float tt = 1.0f - lo;
+            const float u = tt * (float)(G - 1 - i);
+            const float v = u / (float)(G - 1);
+            alphas[i] = 1.0f - v;
+        }
+    }
+}
+
+// partial sums of (Y0 - acc * xs * ws)^2 over a grid-stride slice of the
+// M x N outputs, fp64, tree-reduced in a fixed order
+__global__ void __launch_bounds__(kErrThreads)
+clps_error_kernel(const float *__restrict__ Y0, int64_t ldy0, const int32_t *__restrict__ acc, int64_t ldacc,
+                  const float *__restrict__ xs, const float *__restrict__ ws, int64_t M, int64_t N,
+                  double *__restrict__ partial)
+{
+    __shared__ double red[kErrThreads];
+    double s = 0.0;
+    const int64_t total = M * N;
+    for (int64_t e = (int64_t)blockIdx.x * kErrThreads + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * kErrThreads) {
+        const int64_t m = e / N, n = e - m * N;
+        const double p = (double)acc[m * ldacc + n] * (double)xs[m] * (double)ws[n];
+        const double d = (double)Y0[m * ldy0 + n] - p;
+        s += d * d;
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int k = kErrThreads / 2; k > 0; k >>= 1) {
+        if ((int)threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partial[blockIdx.x] = red[0];
+}
+
+__global__ void __launch_bounds__(256)
+clps_sum_kernel(const double *__restrict__ partial, int n, double *__restrict__ out)
+{
+    __shared__ double red[256];
+    double s = 0.0;
+    for (int i = threadIdx.x; i < n; i += 256) s += partial[i];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int k = 128; k > 0; k >>= 1) {
+        if ((int)threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *out = red[0];
+}
+
+__global__ void clps_argmin_kernel(const double *__restrict__ errors, int G, int32_t *__restrict__ best)
+{
+    if (threadIdx.x != 0) return;
+    int b = 0;
+    for (int i = 1; i < G; ++i)
+        if (errors[i] < errors[b]) b = i;
+    *best = b;
+}
+
+struct ClpsLayout {
+    size_t ratio, xq, xs, wq, ws, acc, partial, total;
+    int64_t ldacc;
+};
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+ClpsLayout clps_layout(int64_t M, int64_t N, int64_t K) {
+    ClpsLayout l{};
+    l.ldacc = (N + 3) / 4 * 4;
+    size_t off = 0;
+    l.ratio = off;   off += align256((size_t)N * 4);
+    l.xq = off;      off += align256((size_t)padded_act_rows(M) * (size_t)(K / 2));
+    l.xs = off;      off += align256((size_t)M * 4);
+    l.wq = off;      off += align256((size_t)padded_rows(N) * (size_t)(K / 2));
+    l.ws = off;      off += align256((size_t)N * 4);
+    l.acc = off;     off += align256((size_t)M * (size_t)l.ldacc * 4);
+    l.partial = off; off += align256((size_t)kErrBlocks * 8);
+    l.total = off;
+    return l;
+}
+
+}  // namespace
+
+size_t clps_workspace_bytes(int64_t M, int64_t N, int64_t K) { return clps_layout(M, N, K).total; }
+
+hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const float *Y0, int64_t ldy0,
+                       const int32_t *perm, int64_t M, int64_t N, int K, int block, int order_idx,
+                       int grid, void *workspace, float *alphas, double *errors, int32_t *best,
+                       hipStream_t stream) {
+    const ClpsLayout l = clps_layout(M, N, K);
+    uint8_t *base = static_cast<uint8_t *>(workspace);
+    float *ratio = reinterpret_cast<float *>(base + l.ratio);
+    uint8_t *xq = base + l.xq;
+    float *xs = reinterpret_cast<float *>(base + l.xs);
+    uint8_t *wq = base + l.wq;
+    float *wsc = reinterpret_cast<float *>(base + l.ws);
+    int32_t *acc = reinterpret_cast<int32_t *>(base + l.acc);
+    double *partial = reinterpret_cast<double *>(base + l.partial);
+
+    int P = 1;
+    while (P < K) P <<= 1;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void *)clps_row_ratio_kernel,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 16384 * 4);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    hipLaunchKernelGGL(clps_row_ratio_kernel, dim3((unsigned)N), dim3(kRatioThreads), (size_t)P * 4, stream,
+                       W, perm, K, block, P, order_idx, ratio);
+    hipLaunchKernelGGL(clps_grid_kernel, dim3(1), dim3(256), 0, stream, ratio, N, grid, alphas);
+    hipError_t e = launch_rotate_quant(X, ldx, perm, M, padded_act_rows(M), K, block, 1.0f, false, 1.0f, xq, xs,
+                                       stream);
+    if (e != hipSuccess) return e;
+    for (int i = 0; i < grid; ++i) {
+        e = launch_rotate_quant(W, K, perm, N, padded_rows(N), K, block, 1.0f, true, 1.0f / (float)block, wq, wsc,
+                                stream, 4, alphas + i);
+        if (e != hipSuccess) return e;
+        e = launch_gemm(xq, xs, wq, wsc, nullptr, M, N, K, acc, l.ldacc, true, nullptr, stream);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(clps_error_kernel, dim3(kErrBlocks), dim3(kErrThreads), 0, stream, Y0, ldy0, acc,
+                           l.ldacc, xs, wsc, M, N, partial);
+        hipLaunchKernelGGL(clps_sum_kernel, dim3(1), dim3(256), 0, stream, partial, kErrBlocks, errors + i);
+    }
+    hipLaunchKernelGGL(clps_argmin_kernel, dim3(1), dim3(64), 0, stream, errors, grid, best);
+    return hipGetLastError();
+}
+
+}  // namespace clq

@@ -2,6 +2,7 @@
 // Every entry point checks its arguments before enqueuing anything and
 // returns a status code; kernels run on the caller's stream.
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 #include "../../include/clq.h"
@@ -9,7 +10,7 @@
 
 namespace {
 
-constexpr int kVersion = 5;
+constexpr int kVersion = 6;
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxRows = 2147483647;
 
@@ -46,7 +47,7 @@ const char *clq_status_string(clq_status s) {
         case CLQ_ERR_SHAPE: return "CLQ_ERR_SHAPE: a size or row stride is out of range";
         case CLQ_ERR_BLOCK: return "CLQ_ERR_BLOCK: block must be 32, 64 or 128 and divide K";
         case CLQ_ERR_ALIGN: return "CLQ_ERR_ALIGN: a pointer is misaligned";
-        case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio outside [2^-24, 1], or an unknown metric or wbits";
+        case CLQ_ERR_ARG: return "CLQ_ERR_ARG: clip_ratio, metric, wbits, gamma or grid out of range";
         case CLQ_ERR_HIP: return "CLQ_ERR_HIP: a HIP launch failed";
         case CLQ_ERR_WORKSPACE: return "CLQ_ERR_WORKSPACE: workspace smaller than the entry point's *_workspace_bytes()";
     }
@@ -278,6 +279,35 @@ clq_status clq_unswizzle_weights8(const void *Wq8, int64_t N, int64_t K, void *c
     if (!aligned(Wq8, 16)) return CLQ_ERR_ALIGN;
     return from_hip(clq::launch_unswizzle8(static_cast<const uint8_t *>(Wq8), N, (int)K, true,
                                            static_cast<int8_t *>(codes), stream));
+}
+
+/* ---- CLPS single-layer clip search ------------------------------------------ */
+
+size_t clq_clps_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (check_rows(M) != CLQ_OK || check_rows(N) != CLQ_OK || check_k(K) != CLQ_OK || K > 16384) return 0;
+    return clq::clps_workspace_bytes(M, N, K);
+}
+
+clq_status clq_clps_search(const void *X, int64_t ldx, const void *W, const float *Y0, int64_t ldy0,
+                           const int32_t *perm, int64_t M, int64_t N, int64_t K, int32_t block,
+                           float gamma, int32_t grid, void *workspace, size_t workspace_bytes,
+                           float *alphas, double *errors, int32_t *best, hipStream_t stream) {
+    if (!X || !W || !Y0 || !workspace || !alphas || !errors || !best) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (K > 16384) return CLQ_ERR_SHAPE;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (ldx < K || ldx % 8 != 0 || ldy0 < N) return CLQ_ERR_SHAPE;
+    if (!(gamma >= 0.0f && gamma < 1.0f) || grid < 1 || grid > 256) return CLQ_ERR_ARG;
+    if (!aligned(X, 16) || !aligned(W, 16) || !aligned(Y0, 4) || !aligned(workspace, 16) ||
+        !aligned(alphas, 4) || !aligned(errors, 8) || !aligned(best, 4) || (perm && !aligned(perm, 4)))
+        return CLQ_ERR_ALIGN;
+    if (workspace_bytes < clq::clps_workspace_bytes(M, N, K)) return CLQ_ERR_WORKSPACE;
+    // l = floor(gamma (K - 1)) weights above the order statistic
+    const int l = (int)floor((double)gamma * (double)(K - 1));
+    return from_hip(clq::launch_clps(static_cast<const uint16_t *>(X), ldx, static_cast<const uint16_t *>(W), Y0,
+                                     ldy0, perm, M, N, (int)K, block, (int)(K - 1 - l), grid, workspace, alphas,
+                                     errors, best, stream));
 }
 
 }  // extern "C"

@@ -71,11 +71,21 @@ __host__ __device__ inline int64_t q8_piece_offset(int64_t u, int rho, int64_t c
     return ((u * (K >> 6) + (c >> 1)) * 2 + q) * 1024 + (32 * (c & 1) + rho) * 16;
 }
 
-// bits: 4 (packed int4 layouts above) or 8 (int8 layout).
+// bits: 4 (packed int4 layouts above) or 8 (int8 layout).  alpha_dev, when
+// given, holds the weights' clip ratio in device memory (alpha is then unused).
 hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
                                int64_t rows, int64_t rows_alloc, int K, int block,
                                float alpha, bool weight_mode, float post_scale,
-                               uint8_t *out, float *scale, hipStream_t stream, int bits = 4);
+                               uint8_t *out, float *scale, hipStream_t stream, int bits = 4,
+                               const float *alpha_dev = nullptr);
+
+// Single-layer clip search (CLPS): workspace bytes and the whole search.
+size_t clps_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const float *Y0, int64_t ldy0,
+                       const int32_t *perm, int64_t M, int64_t N, int K, int block, int order_idx,
+                       int grid, void *workspace, float *alphas, double *errors, int32_t *best,
+                       hipStream_t stream);
 
 // canonical int8 codes [rows][K] of an int8-layout buffer (weights: the
 // fragment-row order undone)

@@ -138,8 +138,8 @@ template <int B, bool WEIGHT, int QB>
 __global__ void __launch_bounds__(rq_max_threads<B>())
 rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
                     const int32_t *__restrict__ perm, int64_t rows_valid,
-                    int64_t rows_alloc, int K, int R, float alpha, float post_scale,
-                    uint8_t *__restrict__ out, float *__restrict__ scale_out)
+                    int64_t rows_alloc, int K, int R, float alpha, const float *__restrict__ alpha_dev,
+                    float post_scale, uint8_t *__restrict__ out, float *__restrict__ scale_out)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int CPB = B / 8;            // 16-byte chunks per block
@@ -227,7 +227,10 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
 
     // 3. per-row scale and codes
     const float a = __uint_as_float(rowmax[r]);
-    const float ac = WEIGHT ? alpha * a : a;
+    // the clip ratio: a launch argument, or read from device memory (a
+    // search that picks it on the GPU)
+    const float al = alpha_dev != nullptr ? *alpha_dev : alpha;
+    const float ac = WEIGHT ? al * a : a;
     const float rc = (ac == 0.0f) ? 0.0f : Grid<QB>::qmax / ac;
     const int64_t grow = row0 + r;
     if (j == 0 && grow < rows_valid) scale_out[grow] = (ac / Grid<QB>::qmax) * post_scale;
@@ -444,7 +447,8 @@ int pick_rows(int K, int block) {
 template <int B, bool WEIGHT, int QB>
 hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
                      int64_t rows_valid, int64_t rows_alloc, int K, float alpha,
-                     float post_scale, uint8_t *out, float *scale, hipStream_t stream) {
+                     float post_scale, uint8_t *out, float *scale, hipStream_t stream,
+                     const float *alpha_dev = nullptr) {
     const int R = pick_rows(K, B);
     const int nb = K / B;
     const int T = (R * nb + 63) / 64 * 64;
@@ -459,7 +463,7 @@ hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
     }
     const int64_t grid = (rows_alloc + R - 1) / R;
     hipLaunchKernelGGL((rotate_quant_kernel<B, WEIGHT, QB>), dim3((unsigned)grid), dim3(T), lds,
-                       stream, X, ldx, perm, rows_valid, rows_alloc, K, R, alpha, post_scale,
+                       stream, X, ldx, perm, rows_valid, rows_alloc, K, R, alpha, alpha_dev, post_scale,
                        out, scale);
     return hipGetLastError();
 }
@@ -563,12 +567,12 @@ template <int QB>
 hipError_t launch_rq_bits(const uint16_t *X, int64_t ldx, const int32_t *perm,
                           int64_t rows, int64_t rows_alloc, int K, int block,
                           float alpha, bool weight_mode, float post_scale,
-                          uint8_t *out, float *scale, hipStream_t stream) {
+                          uint8_t *out, float *scale, hipStream_t stream, const float *alpha_dev) {
     if (weight_mode) {
         switch (block) {
-            case 32: return launch_rq<32, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
-            case 64: return launch_rq<64, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
-            case 128: return launch_rq<128, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream);
+            case 32: return launch_rq<32, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev);
+            case 64: return launch_rq<64, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev);
+            case 128: return launch_rq<128, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev);
         }
     } else {
         switch (block) {
@@ -583,13 +587,14 @@ hipError_t launch_rq_bits(const uint16_t *X, int64_t ldx, const int32_t *perm,
 hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
                                int64_t rows, int64_t rows_alloc, int K, int block,
                                float alpha, bool weight_mode, float post_scale,
-                               uint8_t *out, float *scale, hipStream_t stream, int bits) {
+                               uint8_t *out, float *scale, hipStream_t stream, int bits,
+                               const float *alpha_dev) {
     if (bits == 8)
         return launch_rq_bits<8>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
-                                 out, scale, stream);
+                                 out, scale, stream, alpha_dev);
     if (bits == 4)
         return launch_rq_bits<4>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
-                                 out, scale, stream);
+                                 out, scale, stream, alpha_dev);
     return hipErrorInvalidValue;
 }
 

@@ -59,12 +59,16 @@ def lib():
     L.clq_a8_accum_i32.argtypes = [p, p, i32, i64, i64, i64, p, i64, p]
     L.clq_unswizzle_act8.argtypes = [p, i64, i64, p, p]
     L.clq_unswizzle_weights8.argtypes = [p, i64, i64, p, p]
+    L.clq_clps_workspace_bytes.restype = ctypes.c_size_t
+    L.clq_clps_workspace_bytes.argtypes = [i64, i64, i64]
+    L.clq_clps_search.argtypes = [p, i64, p, p, i64, p, i64, i64, i64, i32, f32, i32, p, ctypes.c_size_t,
+                                  p, p, p, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 22, names
+    assert len(names) == 24, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -76,7 +80,7 @@ def test_binding_names_match_header():
 
 
 def test_version_and_strings(lib):
-    assert lib.clq_version() == 5
+    assert lib.clq_version() == 6
     for code in range(8):
         s = lib.clq_status_string(code).decode()
         assert s.startswith("CLQ")
@@ -267,3 +271,24 @@ def test_8bit_validation(lib):
     assert k(A, A, 0, 4, 8, 1152, A, 8, None) == ARG
     assert lib.clq_unswizzle_act8(None, 4, 1152, A, None) == NULL
     assert lib.clq_unswizzle_weights8(A, 4, 100, A, None) == SHAPE
+
+
+def test_clps_validation(lib):
+    need = lib.clq_clps_workspace_bytes(64, 48, 1152)
+    assert need > 64 * 48 * 4
+    assert lib.clq_clps_workspace_bytes(64, 48, 32768) == 0          # K <= 16384
+    f = lib.clq_clps_search
+
+    def cs(X=A, ldx=1152, W=A, Y0=A, ldy0=48, M=64, N=48, K=1152, block=64, gamma=0.01, grid=20,
+           ws=A, wsb=need, al=A, er=A, best=A):
+        return f(X, ldx, W, Y0, ldy0, None, M, N, K, block, gamma, grid, ws, wsb, al, er, best, None)
+    assert cs(X=None) == NULL and cs(Y0=None) == NULL and cs(best=None) == NULL and cs(ws=None) == NULL
+    assert cs(K=32768, ldx=32768) == SHAPE
+    assert cs(block=48) == BLOCK
+    assert cs(ldy0=40) == SHAPE
+    assert cs(ldx=1156) == SHAPE
+    assert cs(gamma=1.0) == ARG and cs(gamma=-0.1) == ARG
+    assert cs(grid=0) == ARG and cs(grid=257) == ARG
+    assert cs(er=A + 4) == ALIGN
+    assert cs(Y0=A + 2) == ALIGN
+    assert cs(wsb=need - 1) == WORKSPACE
