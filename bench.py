@@ -200,6 +200,63 @@ def bench_obs(args, clq, torch, dev):
     print(json.dumps(out), flush=True)
 
 
+def bench_clps(args, clq, torch, dev):
+    """CLPS single-layer clip search (Sec. 3.4): the PixArt qkv layer (1152 ->
+    3456) on 4096 calibration tokens, 20 candidate clip ratios.  value =
+    effective TOPS of the search (20 quantized GEMMs of 2 M N K each, plus the
+    window, weight quantization and error passes, over the search time)."""
+    M, K, N, b, G = 4096, 1152, 3456, 64, 20
+    X = workloads.activations(M, K, "L1", 2101)
+    W = workloads.weights(N, K, 2102)
+    Xd, Wd = torch.from_numpy(X).to(dev), torch.from_numpy(W).to(dev)
+    # the target output X W^T in fp32 (input to the search, computed once)
+    Y0 = (Xd.float() @ Wd.float().T).contiguous()
+    ws = torch.empty(clq.clq_clps_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        return clq.clq_clps_search(Xd, Wd, Y0, b, grid=G, workspace=ws)
+
+    for _ in range(max(1, args.warmup // 10)):
+        step()
+    torch.cuda.synchronize()
+    steps = max(3, args.steps // 10)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        al, er, best = step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    ev_ms = e0.elapsed_time(e1) / steps
+    ops = G * 2.0 * M * N * K
+    value = ops / (ms * 1e-3) / 1e12
+    out = {
+        "metric": "CLPS single-layer clip search, effective TOPS (20 candidates)",
+        "value": round(value, 2), "unit": "TOPS", "n_gpus": 1, "steps": steps, "warmup": max(1, args.warmup // 10),
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int4", "data": "synthetic",
+        "config": {"workload": "clps_pixart_qkv_m4096_k1152_n3456_g20", "M": M, "K": K, "N": N, "block": b,
+                   "grid": G, "gamma": 0.01, "parallelism": "none (one GPU)"},
+        "search_ms_events": round(ev_ms, 4),
+        "best_alpha": float(al[int(best.item())].item()),
+        "errors_first_last": [float(er[0].item()), float(er[-1].item())],
+        "gpu": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline:
+        # the oracle's search on the first 256 tokens, 4 candidates
+        from oracle import clps as oclps
+        t0 = time.perf_counter()
+        Y0h = Y0[:256].cpu().numpy()
+        oclps.search(X[:256], W, Y0h, b, G=4)
+        t = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(4 * 2.0 * 256 * N * K / t / 1e12, 4), "unit": "TOPS",
+                               "cores": 16, "kind": "oracle",
+                               "sample": f"256 of the 4096 tokens, 4 of the 20 candidates ({t:.1f} s)"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -208,7 +265,8 @@ def main():
     ap.add_argument("--cold-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default="pixart_block",
-                    choices=["pixart_block", "pixart_block_w4a8", "pixart_block_w8a8", "obs_calibration"],
+                    choices=["pixart_block", "pixart_block_w4a8", "pixart_block_w8a8", "obs_calibration",
+                             "clps_search"],
                     help="pixart_block: the W4A4 linear hot path (default); pixart_block_w4a8 / _w8a8: the "
                          "same block at 8-bit activations (and weights); obs_calibration: the OBS "
                          "channel-score pass over a calibration batch")
@@ -238,6 +296,9 @@ def main():
 
     if args.workload == "obs_calibration":
         bench_obs(args, clq, torch, dev)
+        return
+    if args.workload == "clps_search":
+        bench_clps(args, clq, torch, dev)
         return
 
     wl = workloads.C2

@@ -8,9 +8,10 @@
 //
 // Steps, all on the caller's stream with no host synchronisation:
 //   clps_row_ratio_kernel  per weight row: gather, block FWHT in LDS (the
-//                          same fp32 butterflies as the quantizer), |.|,
-//                          bitonic sort, ratio of the order statistic with
-//                          floor(gamma (K-1)) values above it to the max.
+//                          same fp32 butterflies as the quantizer), then the
+//                          order statistic of |.| with floor(gamma (K-1))
+//                          values above it (walked down from the max) over
+//                          the max.
 //   clps_grid_kernel       alpha_lo = min of the row ratios; the G candidates
 //                          alpha_i = 1 - ((1 - alpha_lo)(G-1-i)) / (G-1).
 //   per candidate          the hot path's weight quantizer with alpha_i read
@@ -36,16 +37,16 @@ constexpr int kRatioThreads = 256;
 constexpr int kErrBlocks = 1024;
 constexpr int kErrThreads = 256;
 
-// one workgroup per row; LDS holds the row padded to P = 2^ceil(log2 K)
+// one workgroup per row; LDS holds the row
 __global__ void __launch_bounds__(kRatioThreads)
 clps_row_ratio_kernel(const uint16_t *__restrict__ W, const int32_t *__restrict__ perm, int K, int block,
-                      int P, int order_idx, float *__restrict__ ratio)
+                      int order_idx, float *__restrict__ ratio)
 {
-    extern __shared__ float w[];   // [P]
+    extern __shared__ float w[];   // [K]
     const int row = blockIdx.x, t = threadIdx.x;
     const uint16_t *src = W + (int64_t)row * K;
-    for (int i = t; i < P; i += kRatioThreads)
-        w[i] = i < K ? __half2float(__ushort_as_half(src[perm ? perm[i] : i])) : 0.0f;
+    for (int i = t; i < K; i += kRatioThreads)
+        w[i] = __half2float(__ushort_as_half(src[perm ? perm[i] : i]));
     __syncthreads();
     // block FWHT: stage h pairs (i, i + h) with (i mod 2h) < h, ascending h
     for (int h = 1; h < block; h <<= 1) {
@@ -57,28 +58,42 @@ clps_row_ratio_kernel(const uint16_t *__restrict__ W, const int32_t *__restrict_
         }
         __syncthreads();
     }
-    // magnitudes; padding below every magnitude so it sorts first
-    for (int i = t; i < P; i += kRatioThreads) w[i] = i < K ? fabsf(w[i]) : -1.0f;
-    __syncthreads();
-    for (int k = 2; k <= P; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = t; i < P; i += kRatioThreads) {
-                const int l = i ^ j;
-                if (l > i) {
-                    const float a = w[i], b = w[l];
-                    if ((a > b) == ((i & k) == 0)) {
-                        w[i] = b;
-                        w[l] = a;
-                    }
-                }
-            }
-            __syncthreads();
+    // the order statistic with l = K-1-order_idx values above it, by walking
+    // down the distinct magnitudes: m = the largest magnitude below the last
+    // one, c = how many are >= m; the first m with c > l is the answer (exact
+    // with repeated values; at most l + 1 steps).  The first m is the max.
+    __shared__ float redf[kRatioThreads / 64];
+    __shared__ int redi[kRatioThreads / 64];
+    const int l = K - 1 - order_idx;
+    const int lane = t & 63, wv = t >> 6;
+    float top = __builtin_inff(), mx = 0.0f, q = 0.0f;
+    for (int it = 0;; ++it) {
+        float m = -1.0f;
+        for (int i = t; i < K; i += kRatioThreads) {
+            const float v = fabsf(w[i]);
+            if (v < top) m = fmaxf(m, v);
         }
+        for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+        if (lane == 0) redf[wv] = m;
+        __syncthreads();
+        m = redf[0];
+        for (int k = 1; k < kRatioThreads / 64; ++k) m = fmaxf(m, redf[k]);
+        int c = 0;
+        for (int i = t; i < K; i += kRatioThreads) c += fabsf(w[i]) >= m;
+        for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+        if (lane == 0) redi[wv] = c;
+        __syncthreads();
+        c = 0;
+        for (int k = 0; k < kRatioThreads / 64; ++k) c += redi[k];
+        __syncthreads();   // redf / redi are rewritten in the next step
+        if (it == 0) mx = m;
+        if (c > l) {
+            q = m;
+            break;
+        }
+        top = m;
     }
-    if (t == 0) {
-        const float mx = w[P - 1], q = w[P - K + order_idx];
-        ratio[row] = mx == 0.0f ? 1.0f : q / mx;
-    }
+    if (t == 0) ratio[row] = mx == 0.0f ? 1.0f : q / mx;
 }
 
 __global__ void __launch_bounds__(256)
@@ -106,8 +121,9 @@ clps_grid_kernel(const float *__restrict__ ratio, int64_t N, int G, float *__res
     }
 }
 
-// partial sums of (Y0 - acc * xs * ws)^2 over a grid-stride slice of the
-// M x N outputs, fp64, tree-reduced in a fixed order
+// partial sums of (Y0 - acc * xs * ws)^2: workgroup g takes rows g, g + G,
+// ..., a thread the columns t, t + 256, ...; fp64, tree-reduced in a fixed
+// order
 __global__ void __launch_bounds__(kErrThreads)
 clps_error_kernel(const float *__restrict__ Y0, int64_t ldy0, const int32_t *__restrict__ acc, int64_t ldacc,
                   const float *__restrict__ xs, const float *__restrict__ ws, int64_t M, int64_t N,
@@ -115,13 +131,14 @@ clps_error_kernel(const float *__restrict__ Y0, int64_t ldy0, const int32_t *__r
 {
     __shared__ double red[kErrThreads];
     double s = 0.0;
-    const int64_t total = M * N;
-    for (int64_t e = (int64_t)blockIdx.x * kErrThreads + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * kErrThreads) {
-        const int64_t m = e / N, n = e - m * N;
-        const double p = (double)acc[m * ldacc + n] * (double)xs[m] * (double)ws[n];
-        const double d = (double)Y0[m * ldy0 + n] - p;
-        s += d * d;
+    for (int64_t m = blockIdx.x; m < M; m += gridDim.x) {
+        const double xm = (double)xs[m];
+        const int32_t *ar = acc + m * ldacc;
+        const float *yr = Y0 + m * ldy0;
+        for (int64_t n = threadIdx.x; n < N; n += kErrThreads) {
+            const double d = (double)yr[n] - (double)ar[n] * xm * (double)ws[n];
+            s += d * d;
+        }
     }
     red[threadIdx.x] = s;
     __syncthreads();
@@ -196,8 +213,6 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
     int32_t *acc = reinterpret_cast<int32_t *>(base + l.acc);
     double *partial = reinterpret_cast<double *>(base + l.partial);
 
-    int P = 1;
-    while (P < K) P <<= 1;
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void *)clps_row_ratio_kernel,
@@ -205,8 +220,8 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL(clps_row_ratio_kernel, dim3((unsigned)N), dim3(kRatioThreads), (size_t)P * 4, stream,
-                       W, perm, K, block, P, order_idx, ratio);
+    hipLaunchKernelGGL(clps_row_ratio_kernel, dim3((unsigned)N), dim3(kRatioThreads), (size_t)K * 4, stream,
+                       W, perm, K, block, order_idx, ratio);
     hipLaunchKernelGGL(clps_grid_kernel, dim3(1), dim3(256), 0, stream, ratio, N, grid, alphas);
     hipError_t e = launch_rotate_quant(X, ldx, perm, M, padded_act_rows(M), K, block, 1.0f, false, 1.0f, xq, xs,
                                        stream);
@@ -217,9 +232,10 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
         if (e != hipSuccess) return e;
         e = launch_gemm(xq, xs, wq, wsc, nullptr, M, N, K, acc, l.ldacc, true, nullptr, stream);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(clps_error_kernel, dim3(kErrBlocks), dim3(kErrThreads), 0, stream, Y0, ldy0, acc,
+        const int eb = (int)std::min<int64_t>(M, kErrBlocks);
+        hipLaunchKernelGGL(clps_error_kernel, dim3(eb), dim3(kErrThreads), 0, stream, Y0, ldy0, acc,
                            l.ldacc, xs, wsc, M, N, partial);
-        hipLaunchKernelGGL(clps_sum_kernel, dim3(1), dim3(256), 0, stream, partial, kErrBlocks, errors + i);
+        hipLaunchKernelGGL(clps_sum_kernel, dim3(1), dim3(256), 0, stream, partial, eb, errors + i);
     }
     hipLaunchKernelGGL(clps_argmin_kernel, dim3(1), dim3(64), 0, stream, errors, grid, best);
     return hipGetLastError();
