@@ -69,12 +69,11 @@ def load_traffic(kernel_src_sha):
 
 
 def kernel_sha():
+    """Hash of the GEMM kernel's source (the kernel the traffic figures
+    describe)."""
     import hashlib
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2509_24416_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h")):
-            h.update(open(os.path.join(csrc, f), "rb").read())
+    h.update(open(os.path.join(ROOT, "paper_2509_24416_amd", "csrc", "w4a4_gemm.hip"), "rb").read())
     return h.hexdigest()[:16]
 
 
