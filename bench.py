@@ -256,6 +256,61 @@ def bench_clps(args, clq, torch, dev):
     print(json.dumps(out), flush=True)
 
 
+def bench_stack(args, clq, torch, dev):
+    """The multi-layer path: 28 PixArt-width DiT blocks (112 linears, 223 MB
+    of resident int4 weights), rotate+quant + W4A4 GEMM per linear, replayed
+    as one HIP graph.  value = effective TOPS at M = 4096 tokens; the eager
+    (launch-by-launch) step and M = 1024 / 16384 are reported beside it."""
+    from paper_2509_24416_amd.stack import DiTStack
+    nb, b = 28, 64
+    # weights are generated once (at the largest M; shapes do not depend on M)
+    wl = workloads.dit_stack(nb, 4096, b)
+    weights = []
+    for j in range(nb):
+        blk = {}
+        for l in wl.layers[4 * j:4 * j + 4]:
+            blk[l.name.split(".")[1]] = (torch.from_numpy(workloads.weights(l.N, l.K, l.seed + 1)).to(dev),
+                                         torch.from_numpy(workloads.bias(l.N, l.seed + 2)).to(dev))
+        weights.append(blk)
+    res = {}
+    for M in (4096, 1024, 16384):
+        st = DiTStack(weights, M, b)
+        x = torch.from_numpy(workloads.activations(M, 1152, "L1", 500)).to(dev)
+        st.forward(x)
+        st.capture()
+        steps = args.steps if M == 4096 else max(5, args.steps // 4)
+        for _ in range(3):
+            st.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            st.replay()
+        torch.cuda.synchronize()
+        g_ms = (time.perf_counter() - t0) * 1e3 / steps
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            st.forward()
+        torch.cuda.synchronize()
+        e_ms = (time.perf_counter() - t0) * 1e3 / steps
+        res[M] = (g_ms, e_ms, st.ops)
+        del st
+        torch.cuda.synchronize()
+    g_ms, e_ms, ops = res[4096]
+    out = {
+        "metric": "DiT stack (28 blocks x 4 W4A4 linears) effective TOPS, one HIP graph per step",
+        "value": round(ops / (g_ms * 1e-3) / 1e12, 2), "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": 3, "ms_per_step": round(g_ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int4", "data": "synthetic",
+        "config": {"workload": "dit_stack_28x4_m4096_h1152_b64", "blocks": nb, "M": 4096, "block": b,
+                   "launches_per_step": 2 * 4 * nb, "parallelism": "none (one GPU)"},
+        "per_M": {str(M): {"graph_ms": round(v[0], 4), "eager_ms": round(v[1], 4),
+                           "graph_TOPS": round(v[2] / (v[0] * 1e-3) / 1e12, 1),
+                           "eager_TOPS": round(v[2] / (v[1] * 1e-3) / 1e12, 1)} for M, v in res.items()},
+        "gpu": torch.cuda.get_device_name(dev),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -265,7 +320,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default="pixart_block",
                     choices=["pixart_block", "pixart_block_w4a8", "pixart_block_w8a8", "obs_calibration",
-                             "clps_search"],
+                             "clps_search", "dit_stack"],
                     help="pixart_block: the W4A4 linear hot path (default); pixart_block_w4a8 / _w8a8: the "
                          "same block at 8-bit activations (and weights); obs_calibration: the OBS "
                          "channel-score pass over a calibration batch")
@@ -298,6 +353,9 @@ def main():
         return
     if args.workload == "clps_search":
         bench_clps(args, clq, torch, dev)
+        return
+    if args.workload == "dit_stack":
+        bench_stack(args, clq, torch, dev)
         return
 
     wl = workloads.C2

@@ -69,6 +69,24 @@ C4 = Workload("video_block_m43200_h1152_b64",
 WORKLOADS = {w.name: w for w in (C1, C2, C3, C4)}
 
 
+def dit_stack(nblocks=28, M=4096, block=64, hidden=1152, mlp=4608):
+    """A stack of DiT blocks' linears (qkv, proj, fc1, fc2 per block) for the
+    multi-layer path: layer i (block i // 4) draws its weights with seed
+    500 + 10 i + 1 and bias with 500 + 10 i + 2; the stack input is L1 with
+    seed 500.  Between layers the previous output feeds the next input (proj
+    reads the first `hidden` columns of the qkv output, standing in for the
+    attention that is not part of this path), so only the stack input has
+    planted outliers."""
+    shapes = [("qkv", hidden, 3 * hidden), ("proj", hidden, hidden),
+              ("fc1", hidden, mlp), ("fc2", mlp, hidden)]
+    layers = []
+    for j in range(nblocks):
+        for t, (n, K, N) in enumerate(shapes):
+            i = 4 * j + t
+            layers.append(Layer(f"blk{j}.{n}", M, K, N, block, "L1", 500 + 10 * i))
+    return Workload(f"dit_stack_{nblocks}x4_m{M}_h{hidden}_b{block}", tuple(layers))
+
+
 def law_params(law):
     if law == "L1":
         return dict(frac=0.01, lo=20.0, hi=100.0, token_sigma=0.0)
