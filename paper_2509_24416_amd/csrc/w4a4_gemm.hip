@@ -50,6 +50,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "clq_internal.h"
@@ -629,6 +630,7 @@ int full_grid() { return (device_cus() * TCfg::WGS + 7) / 8 * 8; }
 // summed from at most nks / kSplitMinShare + 1 pieces).
 constexpr int kSplitMinSaved = 16;
 constexpr int kSplitMinShare = 8;
+constexpr int kSplitMinLong = 32;   // k-stages (K >= 2048) for the few-tile split
 
 template <class C, bool I32OUT, bool RAGGED, bool BIAS>
 hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
@@ -636,6 +638,22 @@ hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
     int grid = full_grid();
     g.dp = ntiles;
     g.sk = 0;
+    if (may_split && ntiles < grid && nks >= kSplitMinLong) {
+        // fewer tiles than workgroup slots and a long k loop: every tile is
+        // cut along k over as many workgroups as keep shares of
+        // kSplitMinShare stages or more, when that at least doubles the
+        // workgroups at work (all of them fit on the chip at once, so an
+        // owner never waits for one not started).  With short k loops the
+        // partial-sum exchange costs more than the shorter chains save.
+        const int64_t units = (int64_t)ntiles * nks;
+        const int g2 = (int)std::min<int64_t>(grid, units / kSplitMinShare) / 8 * 8;
+        if (g2 >= 2 * ntiles) {
+            g.dp = 0;
+            g.sk = (int)units;
+            hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS>), dim3((unsigned)g2), dim3(C::NT), 0, stream, g);
+            return hipGetLastError();
+        }
+    }
     if (may_split && ntiles % grid != 0) {
         // whole tiles for all but the last one or two rounds; the rest is
         // spread over every workgroup in k-stage units (1 to 2 tiles each)

@@ -148,7 +148,9 @@ def test_accum_i32_bitexact(clq, M, N, K, workspace):
 
 # Shapes whose last tile round is split along k over every workgroup (few
 # tiles, long k): each tile is summed from the partials of many workgroups.
-SPLIT_SHAPES = [(2048, 1152, 4608), (2000, 1000, 4608), (2048, 640, 8192)]
+# The last two have fewer tiles than workgroup slots and a long k loop:
+# every tile is cut along k over a smaller grid.
+SPLIT_SHAPES = [(2048, 1152, 4608), (2000, 1000, 4608), (2048, 640, 8192), (1024, 1152, 4608), (300, 520, 8192)]
 
 
 @pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
