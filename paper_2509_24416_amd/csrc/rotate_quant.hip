@@ -428,6 +428,177 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
     }
 }
 
+// Activations with long rows (K >= 2048): batches of exactly 8 token rows,
+// aligned to 8, so that with the rows-fastest lane order every 128-byte line
+// of the code layout (8 rows x 16 bytes, or 8 rows x 16 bytes of an int8
+// operand piece) is written whole by one store instruction -- partial lines
+// written by several batches cost long-row launches about 40% at full HBM
+// rate.  One workgroup per CU with one LDS buffer of 8 rows; the next batch
+// waits in registers.  Two barriers per batch: after the block reads (the
+// buffer may be refilled) and after the block maxima (codes may be formed).
+// Codes of batch i are formed at the top of iteration i+1, from the
+// registers that still hold its rotated blocks.
+// at most 8 x 80 lanes (b = 64, K <= 5120)
+template <int B>
+constexpr int rows8_threads() { return 640; }
+
+template <int B, int QB>
+__global__ void __launch_bounds__(rows8_threads<B>())
+rq_rows8_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__restrict__ perm,
+                int64_t rows_valid, int64_t rows_alloc, int64_t nbatch, int K,
+                uint8_t *__restrict__ out, float *__restrict__ scale_out)
+{
+    constexpr int R = 8;
+    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int CPB = B / 8;
+    constexpr int LPT = CPB;
+    const int cpr = K >> 3;
+    const int nb = K / B;
+    const int chunks = R * cpr;
+    uint4 *tile = reinterpret_cast<uint4 *>(smem);
+    unsigned *rowmax = reinterpret_cast<unsigned *>(tile + chunks);   // [2][R]
+
+    const int t = threadIdx.x, T = blockDim.x;
+    const int64_t G = gridDim.x;
+
+    // this lane's chunks: source offset, and LDS slot | row << 16 | valid << 19
+    // in one register (slots < 8 * 640)
+    int lsrc[LPT], lmeta[LPT];
+#pragma unroll
+    for (int k = 0; k < LPT; ++k) {
+        const int c = t + k * T;
+        const int r = c / cpr, cc = c - r * cpr;
+        lsrc[k] = r * (int)ldx + cc * 8;
+        const int jj = cc / CPB, ii = cc - jj * CPB;
+        const int slot = r * cpr + jj * CPB + (ii ^ r);   // key (jj * 8 + r) & 7 = r
+        lmeta[k] = c < chunks ? slot | (r << 16) | (1 << 19) : 0;
+    }
+    uint4 ld[LPT];
+    auto load = [&](int64_t batch) {
+        const int64_t row0 = batch * R;
+        const uint16_t *base = X + row0 * ldx;
+#pragma unroll
+        for (int k = 0; k < LPT; ++k) {
+            ld[k] = make_uint4(0u, 0u, 0u, 0u);
+            if ((lmeta[k] >> 19) && row0 + ((lmeta[k] >> 16) & 7) < rows_valid)
+                ld[k] = *reinterpret_cast<const uint4 *>(base + lsrc[k]);
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int k = 0; k < LPT; ++k)
+            if (lmeta[k] >> 19) tile[lmeta[k] & 0xFFFF] = ld[k];
+    };
+
+    const int j = t >> 3, r = t & 7;   // rows fastest
+    const bool active = j < nb;
+    int64_t b = blockIdx.x;
+    if (b >= nbatch) return;
+    if (t < 2 * R) rowmax[t] = 0u;
+    load(b);
+    stash();
+    if (b + G < nbatch) load(b + G);
+    __syncthreads();
+
+    float x[B];
+#pragma unroll
+    for (int e = 0; e < B; ++e) x[e] = 0.0f;
+    int64_t prev = -1;   // batch whose rotated blocks x holds, codes pending
+    int i = 0;
+    auto codes = [&](int64_t pb, int pi) {
+        const float a = __uint_as_float(rowmax[(pi & 1) * R + r]);
+        const float rc = (a == 0.0f) ? 0.0f : Grid<QB>::qmax / a;
+        const int64_t grow = pb * R + r;
+        if (!active || grow >= rows_alloc) return;
+        if (j == 0 && grow < rows_valid) scale_out[grow] = a / Grid<QB>::qmax;
+        if constexpr (QB == 8) {
+            store_q8<B, false>(x, rc, grow, j, K, out);
+        } else {
+            uint32_t words[B / 8];
+#pragma unroll
+            for (int g = 0; g < B / 8; ++g) {
+                uint32_t w[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) w[e] = __float_as_uint(__builtin_fmaf(x[8 * g + e], rc, kMagic));
+                words[g] = pack8(w);
+            }
+#pragma unroll
+            for (int c = 0; c < B / 32; ++c) {
+                const int64_t c32 = (int64_t)j * (B / 32) + c;
+                *reinterpret_cast<uint4 *>(out + xq_chunk_offset(grow, c32, K)) =
+                    make_uint4(words[4 * c], words[4 * c + 1], words[4 * c + 2], words[4 * c + 3]);
+            }
+        }
+    };
+
+    for (; b < nbatch; ++i, b += G) {
+        // codes of the previous batch (its maxima are complete), then this
+        // batch's blocks into registers
+        if (prev >= 0) codes(prev, i - 1);
+        if (t < R) rowmax[((i + 1) & 1) * R + t] = 0u;   // read last at the previous codes
+        if (active) {
+            if (perm == nullptr) {
+                const uint4 *src = tile + r * cpr + j * CPB;
+#pragma unroll
+                for (int ii = 0; ii < CPB; ++ii) {
+                    const uint4 v = src[ii ^ r];
+                    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float u = half_lo(w[e]), s = half_hi(w[e]);
+                        x[8 * ii + 2 * e] = u + s;       // stage h = 1
+                        x[8 * ii + 2 * e + 1] = u - s;
+                    }
+                }
+            } else {
+                const uint16_t *rowh = reinterpret_cast<const uint16_t *>(tile + r * cpr);
+                const int32_t *p = perm + j * B;
+#pragma unroll
+                for (int e = 0; e < B; e += 2) {
+                    const int k0 = p[e], k1 = p[e + 1];
+                    const int c0 = k0 >> 3, c1 = k1 >> 3;
+                    const int s0 = (c0 / CPB) * CPB + ((c0 % CPB) ^ r);
+                    const int s1 = (c1 / CPB) * CPB + ((c1 % CPB) ^ r);
+                    const float u = __half2float(__ushort_as_half(rowh[s0 * 8 + (k0 & 7)]));
+                    const float s = __half2float(__ushort_as_half(rowh[s1 * 8 + (k1 & 7)]));
+                    x[e] = u + s;
+                    x[e + 1] = u - s;
+                }
+            }
+        }
+        __syncthreads();   // every block read: the buffer may be refilled
+        if (b + G < nbatch) stash();
+        if (b + 2 * G < nbatch) load(b + 2 * G);
+        if (active) {
+#pragma unroll
+            for (int h = 2; h < B; h <<= 1) {
+#pragma unroll
+                for (int ii = 0; ii < B; ++ii) {
+                    if ((ii & h) == 0) {
+                        const float u = x[ii], v = x[ii + h];
+                        x[ii] = u + v;
+                        x[ii + h] = u - v;
+                    }
+                }
+            }
+            float bmax = 0.0f;
+#pragma unroll
+            for (int ii = 0; ii < B; ii += 2) bmax = fmaxf(bmax, fmaxf(fabsf(x[ii]), fabsf(x[ii + 1])));
+            atomicMax(&rowmax[(i & 1) * R + r], __float_as_uint(bmax));
+        }
+        __syncthreads();   // maxima complete, next batch staged
+        prev = b;
+    }
+    if (prev >= 0) codes(prev, i - 1);
+}
+
+// Long rows (b = 64, 2048 <= K <= 5120: one buffer of 8 rows within 80 KB,
+// at most 640 lanes) take the 8-row kernel.
+template <int B>
+bool use_rows8(int K) {
+    return B == 64 && K >= 2048 && K <= 5120;
+}
+
 // Rows per workgroup: the largest lane utilisation R*nb / roundup(R*nb, 64)
 // with at most 512 lanes (unless one row alone needs more) and at most 64 KB
 // of staged fp16 rows.
@@ -506,6 +677,22 @@ hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, in
     }
     if ((int64_t)R * ldx > INT32_MAX)   // 32-bit in-batch offsets: very wide strides take the one-shot kernel
         return launch_rq<B, false, QB>(X, ldx, perm, rows_valid, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
+    if constexpr (B == 64) if (use_rows8<B>(K) && (int64_t)8 * ldx <= INT32_MAX) {
+        static bool attr8 = false;
+        if (!attr8) {
+            hipError_t e = hipFuncSetAttribute((const void *)rq_rows8_kernel<B, QB>,
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, 80 * 1024 + 64);
+            if (e != hipSuccess) return e;
+            attr8 = true;
+        }
+        const int T8 = (8 * (K / B) + 63) / 64 * 64;
+        const size_t lds8 = (size_t)8 * K * 2 + 2 * 8 * 4;
+        const int64_t nb8 = (rows_alloc + 7) / 8;
+        const int64_t grid8 = std::min<int64_t>(nb8, (int64_t)cus);
+        hipLaunchKernelGGL((rq_rows8_kernel<B, QB>), dim3((unsigned)grid8), dim3(T8), lds8, stream, X, ldx, perm,
+                           rows_valid, rows_alloc, nb8, K, out, scale);
+        return hipGetLastError();
+    }
     const int64_t nbatch = (rows_alloc + R - 1) / R;
     const int per_cu = (int)std::min<size_t>(4, (160 * 1024) / lds);
     const int64_t grid = std::min<int64_t>(nbatch, (int64_t)cus * per_cu);

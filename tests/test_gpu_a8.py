@@ -66,6 +66,17 @@ def test_rotate_quant_act8_perm_and_stride(clq):
     assert np.array_equal(host(clq.clq_unswizzle_act8(Xq8, M, K)), ref_c)
 
 
+@pytest.mark.parametrize("M,K,with_perm", [(1000, 4608, False), (777, 4608, True), (13, 2048, False)])
+def test_rotate_quant_act8_long_rows(clq, M, K, with_perm):
+    # the 8-aligned-row batches of long rows (b = 64), int8 codes
+    X = workloads.activations(M, K, "L2", seed=M + K)
+    perm = workloads.random_perm(K, seed=M + 1) if with_perm else None
+    Xq8, xs = clq.clq_rotate_quant_act8(dev(X), 64, perm=None if perm is None else dev(perm))
+    _, ref_c, ref_s = oracle.quantize_act(X, 64, perm, bits=8)
+    assert np.array_equal(host(xs), ref_s)
+    assert np.array_equal(host(clq.clq_unswizzle_act8(Xq8, M, K)), ref_c)
+
+
 @pytest.mark.parametrize("N,K,block,clip", [
     (1, 64, 32, 1.0), (65, 1152, 64, 1.0), (200, 1152, 64, 0.8), (96, 3072, 128, 0.9),
     (40, 4608, 64, 0.5)])

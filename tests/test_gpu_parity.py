@@ -59,6 +59,22 @@ def test_rotate_quant_bitexact(clq, M, K, block, law):
     assert Xq.numel() == clq.clq_act_bytes(M, K)
 
 
+# Long rows (b = 64, 2048 <= K <= 5120) are handled in batches of 8 aligned
+# rows; ragged row counts, a gather vector and a wider row stride included.
+@pytest.mark.parametrize("M,K,ld,with_perm", [
+    (1000, 4608, 4608, False), (777, 4608, 4672, True), (9, 2048, 2048, True), (1001, 5120, 5120, False),
+    (8, 4608, 4608, False)])
+def test_rotate_quant_long_rows(clq, M, K, ld, with_perm):
+    X = workloads.activations(M, K, "L1", seed=M + K + 11)
+    wide = np.zeros((M, ld), np.float16)
+    wide[:, :K] = X
+    perm = workloads.random_perm(K, seed=M) if with_perm else None
+    Xq, xs = clq.clq_rotate_quant_act(dev(wide)[:, :K], 64, perm=None if perm is None else dev(perm))
+    ref_q, _, ref_s = oracle.quantize_act(X, 64, perm)
+    assert np.array_equal(host(xs), ref_s)
+    assert np.array_equal(host(clq.clq_unswizzle_act(Xq, M, K)), ref_q)
+
+
 @pytest.mark.parametrize("block", [32, 64, 128])
 def test_rotate_quant_perm_and_stride(clq, block):
     M, K, ld = 37, 1152 if block != 128 else 1536, 2048
