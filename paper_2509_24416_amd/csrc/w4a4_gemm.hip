@@ -369,48 +369,106 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __hip_atomic_store(a.flags + rank * C::NW + wave, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     };
+    // Partials are read two contributors at a time (16 loads in flight per
+    // wave), so a tile split many ways pays half as many memory round trips.
+    auto wait_flag = [&](int r2) {
+        int *fl = a.flags + r2 * C::NW + wave;
+        for (int spin = 0; spin < kSpinLimit; ++spin) {
+            if (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
+            __builtin_amdgcn_s_sleep(8);
+        }
+    };
+    auto part_base = [&](int r2) -> const uint8_t * {
+        uint32_t lo = (uint32_t)lane * 16;
+        asm volatile("" : "+v"(lo));
+        return reinterpret_cast<const uint8_t *>(a.part + (size_t)r2 * C::PART_INTS + wave * WPART) + lo;
+    };
+    auto add8 = [&](int fn, v4i q0, v4i q1, v4i q2, v4i q3, v4i q4, v4i q5, v4i q6, v4i q7) {
+        acc[fn][0] += __builtin_shufflevector(__builtin_shufflevector(q0, q1, 0, 1, 2, 3, 4, 5, 6, 7),
+                                              __builtin_shufflevector(q2, q3, 0, 1, 2, 3, 4, 5, 6, 7),
+                                              0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+        acc[fn][1] += __builtin_shufflevector(__builtin_shufflevector(q4, q5, 0, 1, 2, 3, 4, 5, 6, 7),
+                                              __builtin_shufflevector(q6, q7, 0, 1, 2, 3, 4, 5, 6, 7),
+                                              0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+    };
+    auto add_one = [&](int r2) {
+        const uint8_t *base = part_base(r2);
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn) {
+            const uint8_t *p0 = base + (fn * C::FM) * 4096, *p1 = p0 + 4096;
+            v4i q0, q1, q2, q3, q4, q5, q6, q7;
+            asm volatile(
+                "global_load_dwordx4 %0, %8, off sc1\n\t"
+                "global_load_dwordx4 %1, %8, off offset:1024 sc1\n\t"
+                "global_load_dwordx4 %2, %8, off offset:2048 sc1\n\t"
+                "global_load_dwordx4 %3, %8, off offset:3072 sc1\n\t"
+                "global_load_dwordx4 %4, %9, off sc1\n\t"
+                "global_load_dwordx4 %5, %9, off offset:1024 sc1\n\t"
+                "global_load_dwordx4 %6, %9, off offset:2048 sc1\n\t"
+                "global_load_dwordx4 %7, %9, off offset:3072 sc1\n\t"
+                "s_waitcnt vmcnt(0)"
+                : "=&v"(q0), "=&v"(q1), "=&v"(q2), "=&v"(q3), "=&v"(q4), "=&v"(q5), "=&v"(q6), "=&v"(q7)
+                : "v"(p0), "v"(p1)
+                : "memory");
+            add8(fn, q0, q1, q2, q3, q4, q5, q6, q7);
+        }
+    };
+    auto add_two = [&](int r2, int r3) {
+        const uint8_t *base = part_base(r2), *bas2 = part_base(r3);
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn) {
+            const uint8_t *p0 = base + (fn * C::FM) * 4096, *p1 = p0 + 4096;
+            const uint8_t *p2 = bas2 + (fn * C::FM) * 4096, *p3 = p2 + 4096;
+            v4i q0, q1, q2, q3, q4, q5, q6, q7, t0, t1, t2, t3, t4, t5, t6, t7;
+            asm volatile(
+                "global_load_dwordx4 %0, %16, off sc1\n\t"
+                "global_load_dwordx4 %1, %16, off offset:1024 sc1\n\t"
+                "global_load_dwordx4 %2, %16, off offset:2048 sc1\n\t"
+                "global_load_dwordx4 %3, %16, off offset:3072 sc1\n\t"
+                "global_load_dwordx4 %4, %17, off sc1\n\t"
+                "global_load_dwordx4 %5, %17, off offset:1024 sc1\n\t"
+                "global_load_dwordx4 %6, %17, off offset:2048 sc1\n\t"
+                "global_load_dwordx4 %7, %17, off offset:3072 sc1\n\t"
+                "global_load_dwordx4 %8, %18, off sc1\n\t"
+                "global_load_dwordx4 %9, %18, off offset:1024 sc1\n\t"
+                "global_load_dwordx4 %10, %18, off offset:2048 sc1\n\t"
+                "global_load_dwordx4 %11, %18, off offset:3072 sc1\n\t"
+                "global_load_dwordx4 %12, %19, off sc1\n\t"
+                "global_load_dwordx4 %13, %19, off offset:1024 sc1\n\t"
+                "global_load_dwordx4 %14, %19, off offset:2048 sc1\n\t"
+                "global_load_dwordx4 %15, %19, off offset:3072 sc1\n\t"
+                "s_waitcnt vmcnt(0)"
+                : "=&v"(q0), "=&v"(q1), "=&v"(q2), "=&v"(q3), "=&v"(q4), "=&v"(q5), "=&v"(q6), "=&v"(q7),
+                  "=&v"(t0), "=&v"(t1), "=&v"(t2), "=&v"(t3), "=&v"(t4), "=&v"(t5), "=&v"(t6), "=&v"(t7)
+                : "v"(p0), "v"(p1), "v"(p2), "v"(p3)
+                : "memory");
+            add8(fn, q0, q1, q2, q3, q4, q5, q6, q7);
+            add8(fn, t0, t1, t2, t3, t4, t5, t6, t7);
+        }
+    };
     auto fixup = [&](int L) {
         static_assert(C::FM == 2, "two token fragments per load group");
         const int u = L - dp;
         const int beg = u * nks, end = beg + nks;
+        int pending = -1;
         for (int r2 = rank + 1; r2 < G; ++r2) {
             const int st = r2 * S / G;
             if (st >= end) break;
             const int en = (r2 + 1) * S / G;
             if (en <= st || st <= beg) continue;
-            int *fl = a.flags + r2 * C::NW + wave;
-            for (int spin = 0; spin < kSpinLimit; ++spin) {
-                if (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
-                __builtin_amdgcn_s_sleep(8);
+            wait_flag(r2);
+            if (pending < 0) {
+                pending = r2;
+                continue;
             }
-            uint32_t lo = (uint32_t)lane * 16;
-            asm volatile("" : "+v"(lo));
-            const uint8_t *base = reinterpret_cast<const uint8_t *>(a.part + (size_t)r2 * C::PART_INTS + wave * WPART) + lo;
-#pragma unroll
-            for (int fn = 0; fn < C::FN; ++fn) {
-                const uint8_t *p0 = base + (fn * C::FM) * 4096, *p1 = p0 + 4096;
-                v4i q0, q1, q2, q3, q4, q5, q6, q7;
-                asm volatile(
-                    "global_load_dwordx4 %0, %8, off sc1\n\t"
-                    "global_load_dwordx4 %1, %8, off offset:1024 sc1\n\t"
-                    "global_load_dwordx4 %2, %8, off offset:2048 sc1\n\t"
-                    "global_load_dwordx4 %3, %8, off offset:3072 sc1\n\t"
-                    "global_load_dwordx4 %4, %9, off sc1\n\t"
-                    "global_load_dwordx4 %5, %9, off offset:1024 sc1\n\t"
-                    "global_load_dwordx4 %6, %9, off offset:2048 sc1\n\t"
-                    "global_load_dwordx4 %7, %9, off offset:3072 sc1\n\t"
-                    "s_waitcnt vmcnt(0)"
-                    : "=&v"(q0), "=&v"(q1), "=&v"(q2), "=&v"(q3), "=&v"(q4), "=&v"(q5), "=&v"(q6), "=&v"(q7)
-                    : "v"(p0), "v"(p1)
-                    : "memory");
-                acc[fn][0] += __builtin_shufflevector(__builtin_shufflevector(q0, q1, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                      __builtin_shufflevector(q2, q3, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                      0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
-                acc[fn][1] += __builtin_shufflevector(__builtin_shufflevector(q4, q5, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                      __builtin_shufflevector(q6, q7, 0, 1, 2, 3, 4, 5, 6, 7),
-                                                      0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
-            }
-            __hip_atomic_store(fl, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            add_two(pending, r2);
+            __hip_atomic_store(a.flags + pending * C::NW + wave, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.flags + r2 * C::NW + wave, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            pending = -1;
+        }
+        if (pending >= 0) {
+            add_one(pending);
+            __hip_atomic_store(a.flags + pending * C::NW + wave, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     };
 
