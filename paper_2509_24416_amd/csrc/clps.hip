@@ -15,11 +15,13 @@
 //   clps_grid_kernel       alpha_lo = min of the row ratios; the G candidates
 //                          alpha_i = 1 - ((1 - alpha_lo)(G-1-i)) / (G-1).
 //   per candidate          the hot path's weight quantizer with alpha_i read
-//                          from device memory, the W4A4 GEMM's exact integer
-//                          sums, then clps_error_kernel: sum over the
-//                          outputs of (Y0 - acc * x_scale * w_scale)^2 in fp64
-//                          (per-workgroup partials in a fixed order, then
-//                          clps_sum_kernel), so results are deterministic.
+//                          from device memory, then the W4A4 GEMM in its
+//                          squared-error mode: the epilogue forms
+//                          (Y0 - sum * x_scale * w_scale)^2 in fp64 from the
+//                          exact integer sums and keeps one partial per wave
+//                          of each output tile (no product is stored);
+//                          clps_sum_kernel adds the partials in index order,
+//                          so results are deterministic.
 //   clps_argmin_kernel     the smallest error, ties to the lower index.
 // The activations are rotated and quantized once.
 #include <hip/hip_fp16.h>
@@ -34,8 +36,6 @@ namespace clq {
 namespace {
 
 constexpr int kRatioThreads = 256;
-constexpr int kErrBlocks = 1024;
-constexpr int kErrThreads = 256;
 
 // one workgroup per row; LDS holds the row
 __global__ void __launch_bounds__(kRatioThreads)
@@ -121,34 +121,6 @@ clps_grid_kernel(const float *__restrict__ ratio, int64_t N, int G, float *__res
     }
 }
 
-// partial sums of (Y0 - acc * xs * ws)^2: workgroup g takes rows g, g + G,
-// ..., a thread the columns t, t + 256, ...; fp64, tree-reduced in a fixed
-// order
-__global__ void __launch_bounds__(kErrThreads)
-clps_error_kernel(const float *__restrict__ Y0, int64_t ldy0, const int32_t *__restrict__ acc, int64_t ldacc,
-                  const float *__restrict__ xs, const float *__restrict__ ws, int64_t M, int64_t N,
-                  double *__restrict__ partial)
-{
-    __shared__ double red[kErrThreads];
-    double s = 0.0;
-    for (int64_t m = blockIdx.x; m < M; m += gridDim.x) {
-        const double xm = (double)xs[m];
-        const int32_t *ar = acc + m * ldacc;
-        const float *yr = Y0 + m * ldy0;
-        for (int64_t n = threadIdx.x; n < N; n += kErrThreads) {
-            const double d = (double)yr[n] - (double)ar[n] * xm * (double)ws[n];
-            s += d * d;
-        }
-    }
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int k = kErrThreads / 2; k > 0; k >>= 1) {
-        if ((int)threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) partial[blockIdx.x] = red[0];
-}
-
 __global__ void __launch_bounds__(256)
 clps_sum_kernel(const double *__restrict__ partial, int n, double *__restrict__ out)
 {
@@ -174,23 +146,20 @@ __global__ void clps_argmin_kernel(const double *__restrict__ errors, int G, int
 }
 
 struct ClpsLayout {
-    size_t ratio, xq, xs, wq, ws, acc, partial, total;
-    int64_t ldacc;
+    size_t ratio, xq, xs, wq, ws, partial, total;
 };
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
 ClpsLayout clps_layout(int64_t M, int64_t N, int64_t K) {
     ClpsLayout l{};
-    l.ldacc = (N + 3) / 4 * 4;
     size_t off = 0;
     l.ratio = off;   off += align256((size_t)N * 4);
     l.xq = off;      off += align256((size_t)padded_act_rows(M) * (size_t)(K / 2));
     l.xs = off;      off += align256((size_t)M * 4);
     l.wq = off;      off += align256((size_t)padded_rows(N) * (size_t)(K / 2));
     l.ws = off;      off += align256((size_t)N * 4);
-    l.acc = off;     off += align256((size_t)M * (size_t)l.ldacc * 4);
-    l.partial = off; off += align256((size_t)kErrBlocks * 8);
+    l.partial = off; off += align256((size_t)gemm_err_partials(M, N) * 8);
     l.total = off;
     return l;
 }
@@ -210,7 +179,6 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
     float *xs = reinterpret_cast<float *>(base + l.xs);
     uint8_t *wq = base + l.wq;
     float *wsc = reinterpret_cast<float *>(base + l.ws);
-    int32_t *acc = reinterpret_cast<int32_t *>(base + l.acc);
     double *partial = reinterpret_cast<double *>(base + l.partial);
 
     static bool attr_set = false;
@@ -230,12 +198,10 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
         e = launch_rotate_quant(W, K, perm, N, padded_rows(N), K, block, 1.0f, true, 1.0f / (float)block, wq, wsc,
                                 stream, 4, alphas + i);
         if (e != hipSuccess) return e;
-        e = launch_gemm(xq, xs, wq, wsc, nullptr, M, N, K, acc, l.ldacc, true, nullptr, stream);
+        e = launch_gemm_err(xq, xs, wq, wsc, M, N, K, Y0, ldy0, partial, stream);
         if (e != hipSuccess) return e;
-        const int eb = (int)std::min<int64_t>(M, kErrBlocks);
-        hipLaunchKernelGGL(clps_error_kernel, dim3(eb), dim3(kErrThreads), 0, stream, Y0, ldy0, acc,
-                           l.ldacc, xs, wsc, M, N, partial);
-        hipLaunchKernelGGL(clps_sum_kernel, dim3(1), dim3(256), 0, stream, partial, eb, errors + i);
+        hipLaunchKernelGGL(clps_sum_kernel, dim3(1), dim3(256), 0, stream, partial, (int)gemm_err_partials(M, N),
+                           errors + i);
     }
     hipLaunchKernelGGL(clps_argmin_kernel, dim3(1), dim3(64), 0, stream, errors, grid, best);
     return hipGetLastError();

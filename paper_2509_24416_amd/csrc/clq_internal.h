@@ -115,6 +115,14 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
                        int K, void *Y, int64_t ldy, bool i32out, void *workspace,
                        hipStream_t stream);
 
+// The same product, reduced to the squared error against an fp32 target:
+// partials[t] (t < gemm_err_partials(M, N)) receives the fp64 sum of
+// (Y0 - sum * x_scale * w_scale)^2 over one wave's part of one output tile.
+int64_t gemm_err_partials(int64_t M, int64_t N);
+hipError_t launch_gemm_err(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                           int64_t M, int64_t N, int K, const float *Y0, int64_t ldy0, double *partials,
+                           hipStream_t stream);
+
 // OBS calibration (batch mean, channel outlier scores, column swap).
 // metric: 0 abs-max, 1 range, 2 peak-to-average ratio, 3 top-k mean,
 // 4 percentile spread.

@@ -130,11 +130,20 @@ struct GemmArgs {
     int sk;        // k-stages of the remaining tiles, split evenly over the grid
     int32_t *part; // partial accumulators, one tile per workgroup
     int *flags;    // one per wave of every workgroup
+    // squared-error mode: target Y0 fp32 [M][ldy0]; one fp64 partial per
+    // wave of every tile, at errp[tile * waves + wave]
+    const float *y0;
+    int64_t ldy0;
+    double *errp;
 };
 
-template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+// ERR: instead of storing Y, the epilogue sums (Y0 - sum * x_scale * w_scale)^2
+// over the tile in fp64 (the integer sum exact, the products in the order
+// written) and stores one partial per wave.
+template <class C, bool I32OUT, bool RAGGED, bool BIAS, bool ERR>
 __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
 {
+    static_assert(!ERR || (!I32OUT && !BIAS), "the error mode has no output and no bias");
     constexpr int NS = kStages;
     constexpr bool BIAS_CH = BIAS && !RAGGED && !I32OUT;
     constexpr int E_CH = I32OUT ? 0 : C::XS_CH + C::WS_CH + (BIAS_CH ? C::B_CH : 0);
@@ -486,6 +495,7 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
         const uint32_t axs = sb + E_XS + lx, aws = sb + E_WS + lw, ab = sb + E_B + lw / 2;
         float xsm[C::FM];
         int mrow[C::FM];
+        double esum = 0.0;
         if constexpr (!I32OUT) {
             static_assert(C::FM == 2, "two token scales per lane");
             asm volatile("ds_read_b32 %0, %2\n\tds_read_b32 %1, %2 offset:128\n\ts_waitcnt lgkmcnt(0)"
@@ -559,6 +569,32 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
                                 if (n0 + v < N) dst[v] = x[v] >> 8;
                         }
                     }
+                } else if constexpr (ERR) {
+                    // the exact integer sum is x >> 8; d = Y0 - ((sum * x_scale) * w_scale)
+                    if (m < M && n0 < N) {
+                        const float *yr = a.y0 + (int64_t)m * a.ldy0 + n0;
+                        float yv[16];
+                        if constexpr (!RAGGED) {   // 16-byte aligned rows of whole 16-channel pieces
+#pragma unroll
+                            for (int q4 = 0; q4 < 4; ++q4) {
+                                const v4f t = reinterpret_cast<const v4f *>(yr)[q4];
+                                yv[4 * q4] = t[0];
+                                yv[4 * q4 + 1] = t[1];
+                                yv[4 * q4 + 2] = t[2];
+                                yv[4 * q4 + 3] = t[3];
+                            }
+                        } else {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v) yv[v] = n0 + v < N ? yr[v] : 0.0f;
+                        }
+                        const double xm = (double)xsm[fm];
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            if (RAGGED && n0 + v >= N) continue;
+                            const double d = (double)yv[v] - (double)(x[v] >> 8) * xm * (double)wsv[v];
+                            esum += d * d;
+                        }
+                    }
                 } else {
                     uint32_t hv[8];
                     const float xsc = xsm[fm] * (1.0f / 256.0f);   // accumulators hold 256 * sum
@@ -585,6 +621,11 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
             }
             __builtin_amdgcn_sched_barrier(0);
         });
+        if constexpr (ERR) {
+            // fixed butterfly over the wave; lane 0 holds the wave's partial
+            for (int off = 32; off > 0; off >>= 1) esum += __shfl_xor(esum, off);
+            if (lane == 0) a.errp[(int64_t)L * C::NW + wave] = esum;
+        }
     };
 
     // Stage s+1 has landed once at most the VMEM instructions issued after
@@ -690,7 +731,7 @@ constexpr int kSplitMinSaved = 16;
 constexpr int kSplitMinShare = 8;
 constexpr int kSplitMinLong = 32;   // k-stages (K >= 2048) for the few-tile split
 
-template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+template <class C, bool I32OUT, bool RAGGED, bool BIAS, bool ERR = false>
 hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
     const int ntiles = g.tiles_m * g.tiles_n, nks = g.K >> 6;
     int grid = full_grid();
@@ -708,7 +749,7 @@ hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
         if (g2 >= 2 * ntiles) {
             g.dp = 0;
             g.sk = (int)units;
-            hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS>), dim3((unsigned)g2), dim3(C::NT), 0, stream, g);
+            hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS, ERR>), dim3((unsigned)g2), dim3(C::NT), 0, stream, g);
             return hipGetLastError();
         }
     }
@@ -725,7 +766,7 @@ hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
         }
     }
     if (g.sk == 0) grid = max(8, (min(ntiles, grid) + 7) / 8 * 8);
-    hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS>), dim3((unsigned)grid), dim3(C::NT), 0, stream, g);
+    hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS, ERR>), dim3((unsigned)grid), dim3(C::NT), 0, stream, g);
     return hipGetLastError();
 }
 
@@ -768,6 +809,32 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
                     : launch_cfg<TCfg, false, true, false>(g, may_split, stream);
     return bias ? launch_cfg<TCfg, false, false, true>(g, may_split, stream)
                 : launch_cfg<TCfg, false, false, false>(g, may_split, stream);
+}
+
+int64_t gemm_err_partials(int64_t M, int64_t N) {
+    return ((M + TCfg::BM - 1) / TCfg::BM) * ((N + TCfg::BN - 1) / TCfg::BN) * TCfg::NW;
+}
+
+hipError_t launch_gemm_err(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                           int64_t M, int64_t N, int K, const float *Y0, int64_t ldy0, double *partials,
+                           hipStream_t stream) {
+    GemmArgs g{};
+    g.Xq = Xq;
+    g.xs = xs;
+    g.Wq = Wq;
+    g.ws = ws;
+    g.M = (int)M;
+    g.N = (int)N;
+    g.K = K;
+    g.tiles_m = (int)((M + TCfg::BM - 1) / TCfg::BM);
+    g.tiles_n = (int)((N + TCfg::BN - 1) / TCfg::BN);
+    g.y0 = Y0;
+    g.ldy0 = ldy0;
+    g.errp = partials;
+    // whole tiles (no workspace): each tile's partials come from its one epilogue
+    const bool ragged = N % 16 != 0 || ldy0 % 4 != 0 || reinterpret_cast<uintptr_t>(Y0) % 16 != 0;
+    return ragged ? launch_cfg<TCfg, false, true, false, true>(g, false, stream)
+                  : launch_cfg<TCfg, false, false, false, true>(g, false, stream);
 }
 
 }  // namespace clq
