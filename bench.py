@@ -295,6 +295,27 @@ def bench_stack(args, clq, torch, dev):
         res[M] = (g_ms, e_ms, st.ops)
         del st
         torch.cuda.synchronize()
+    # one swap vector per layer input (random stand-ins for OBS outputs):
+    # gathered by every rotate+quant, or folded into the producing layers
+    from paper_2509_24416_amd.stack import LAYERS
+    perms = [{name: torch.from_numpy(workloads.random_perm(weights[j][name][0].shape[1], 1000 + 4 * j + i)).to(dev)
+              for i, name in enumerate(LAYERS)} for j in range(nb)]
+    swap = {}
+    for fold in (False, True):
+        st = DiTStack(weights, 4096, b, perms=perms, fold=fold)
+        x = torch.from_numpy(workloads.activations(4096, 1152, "L1", 500)).to(dev)
+        st.forward(x)
+        st.capture()
+        for _ in range(3):
+            st.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            st.replay()
+        torch.cuda.synchronize()
+        swap["folded_ms" if fold else "gather_ms"] = round((time.perf_counter() - t0) * 1e3 / args.steps, 4)
+        del st
+        torch.cuda.synchronize()
     g_ms, e_ms, ops = res[4096]
     out = {
         "metric": "DiT stack (28 blocks x 4 W4A4 linears) effective TOPS, one HIP graph per step",
@@ -306,6 +327,7 @@ def bench_stack(args, clq, torch, dev):
         "per_M": {str(M): {"graph_ms": round(v[0], 4), "eager_ms": round(v[1], 4),
                            "graph_TOPS": round(v[2] / (v[0] * 1e-3) / 1e12, 1),
                            "eager_TOPS": round(v[2] / (v[1] * 1e-3) / 1e12, 1)} for M, v in res.items()},
+        "swap_vectors_m4096": swap,
         "gpu": torch.cuda.get_device_name(dev),
     }
     print(json.dumps(out), flush=True)

@@ -10,6 +10,14 @@ stay resident; activation buffers are allocated once and reused by every
 block, so a captured graph replays the whole stack (2 launches per linear)
 with no host work and no allocation.
 
+Swap vectors (the `s` of G = S.H, Sec. 3.3, one per layer input) are either
+gathered by each rotate+quant, or folded upstream: the layer that produces an
+input gets its output channels (weight rows and bias) reordered by that
+input's `s` once, at construction, so its output already comes out gathered
+and the consumer's rotate+quant reads it in order.  Each output channel is
+computed independently, so the folded stack produces the same bits.  The
+stack's first input has no producer inside the stack and keeps its gather.
+
 Paper: "CLQ" (arXiv 2509.24416) -- the method quantizes every linear of the
 DiT blocks (Sec. 4.1, W4A4), with the online rotation of Sec. 3.3 in front of
 each.
@@ -24,22 +32,50 @@ LAYERS = ("qkv", "proj", "fc1", "fc2")
 class DiTStack:
     """weights: one dict per block, {"qkv": (W, b), "proj": ..., "fc1": ...,
     "fc2": ...}, fp16 device tensors in torch Linear layout (b may be None).
-    M tokens per step, Hadamard block size `block`."""
+    M tokens per step, Hadamard block size `block`.  perm: one swap vector
+    (int32 [K]) for every layer input, or perms: one dict per block mapping a
+    layer name to its input's swap vector (or None).  fold: reorder each
+    producer's output channels by its consumer's swap vector instead of
+    gathering in the consumer's rotate+quant."""
 
-    def __init__(self, weights, M, block=64, perm=None):
+    def __init__(self, weights, M, block=64, perm=None, perms=None, fold=False):
         self.M, self.block = M, block
         W0 = weights[0]["qkv"][0]
         self.hidden = W0.shape[1]
         self.mlp = weights[0]["fc1"][0].shape[0]
         dev = W0.device
+        nb = len(weights)
+        if perms is None:
+            perms = [{name: perm for name in LAYERS} for _ in range(nb)]
+        self.fold = fold
+        # the swap vector each layer's rotate+quant still gathers by
+        self.gather = [{name: perms[j][name] for name in LAYERS} for j in range(nb)]
+        # output-channel order of each layer (None: natural)
+        rows = [{name: None for name in LAYERS} for _ in range(nb)]
+        if fold:
+            for j in range(nb):
+                for name in LAYERS:
+                    s = perms[j][name]
+                    if s is None or (j == 0 and name == "qkv"):
+                        continue
+                    pj, pname = self._producer(j, name)
+                    if pname == "qkv":   # proj reads the first `hidden` qkv columns
+                        rest = torch.arange(self.hidden, 3 * self.hidden, dtype=s.dtype, device=s.device)
+                        rows[pj][pname] = torch.cat([s, rest])
+                    else:
+                        rows[pj][pname] = s
+                    self.gather[j][name] = None
         self.blocks = []
-        for blk in weights:
+        for j, blk in enumerate(weights):
             q = {}
             for name in LAYERS:
                 W, b = blk[name]
-                q[name] = (clq_quantize_weights(W, block, perm=perm), b)
+                r = rows[j][name]
+                if r is not None:   # one-time reorder of the layer's parameters
+                    W = W.index_select(0, r.long()).contiguous()
+                    b = None if b is None else b.index_select(0, r.long()).contiguous()
+                q[name] = (clq_quantize_weights(W, block, perm=perms[j][name]), b)
             self.blocks.append(q)
-        self.perm = perm
         h, f = self.hidden, self.mlp
         f16 = dict(dtype=torch.float16, device=dev)
         self.x_in = torch.empty((M, h), **f16)
@@ -49,6 +85,13 @@ class DiTStack:
                    f: torch.empty(clq_act_bytes(M, f), dtype=torch.uint8, device=dev)}
         self.xs = torch.empty(M, dtype=torch.float32, device=dev)
         self.graph = None
+
+    @staticmethod
+    def _producer(j, name):
+        """The layer whose output is the input of (j, name) (j >= 0)."""
+        if name == "qkv":
+            return j - 1, "fc2"
+        return j, {"proj": "qkv", "fc1": "proj", "fc2": "fc1"}[name]
 
     def _input(self, j, name):
         if name == "qkv":
@@ -65,7 +108,7 @@ class DiTStack:
                 qw, b = blk[name]
                 x = self._input(j, name)
                 xq = self.xq[qw.K]
-                clq_rotate_quant_act(x, self.block, perm=self.perm, out=xq, scale_out=self.xs)
+                clq_rotate_quant_act(x, self.block, perm=self.gather[j][name], out=xq, scale_out=self.xs)
                 clq_w4a4_linear(xq, self.xs, qw, b, out=self.out[name])
                 if taps is not None and (j, name) in taps:
                     taps[(j, name)] = (x.clone(), self.out[name].clone())

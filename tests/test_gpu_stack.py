@@ -98,3 +98,35 @@ def test_full_depth_stack_is_finite_and_replays(clq):
     st.capture()
     got = host(st.replay())
     assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
+
+
+@pytest.mark.parametrize("M,block", [(300, 64), (256, 128)])
+def test_swap_folded_upstream_matches_gather(clq, M, block):
+    # one swap vector per layer input (Sec. 3.3's s): gathering it in every
+    # rotate+quant and folding it into the producing layer's output channels
+    # give the same bits; the folded producers' outputs come out gathered
+    from paper_2509_24416_amd.stack import DiTStack, LAYERS
+    nb = 3
+    wl = workloads.dit_stack(nb, M, block)
+    x = workloads.activations(M, wl.layers[0].K, "L1", wl.layers[0].seed)
+    weights = [{} for _ in range(nb)]
+    for j in range(nb):
+        for l in wl.layers[4 * j:4 * j + 4]:
+            weights[j][l.name.split(".")[1]] = (dev(workloads.weights(l.N, l.K, l.seed + 1)),
+                                                dev(workloads.bias(l.N, l.seed + 2)))
+    perms = [{name: dev(workloads.random_perm(weights[j][name][0].shape[1], 100 * j + i))
+              for i, name in enumerate(LAYERS)} for j in range(nb)]
+    a = DiTStack(weights, M, block, perms=perms, fold=False)
+    f = DiTStack(weights, M, block, perms=perms, fold=True)
+    ta = {(j, n): None for j in range(nb) for n in LAYERS}
+    tf = dict(ta)
+    ya = host(a.forward(dev(x), taps=ta)).copy()
+    yf = host(f.forward(dev(x), taps=tf)).copy()
+    assert np.array_equal(ya.view(np.uint16), yf.view(np.uint16))
+    for (j, name), (xa, _) in ta.items():
+        xf = host(tf[(j, name)][0])
+        s = host(perms[j][name]).astype(np.int64)
+        want = host(xa) if (j, name) == (0, "qkv") else host(xa)[:, s]
+        assert np.array_equal(xf.view(np.uint16), want.view(np.uint16)), (j, name)
+    # the folded stack gathers only at its first input
+    assert [f.gather[j][n] is None for j in range(nb) for n in LAYERS].count(False) == 1
