@@ -280,7 +280,10 @@ clq_status clq_obs_permutation(const float *scores, int64_t D, int32_t *perm,
  *            cancels), summed in a fixed order (deterministic).
  *   choice   best = the smallest e_i, ties to the lower i. */
 
-/* Workspace bytes of clq_clps_search (0 for sizes out of range). */
+/* Workspace bytes of clq_clps_search (0 for sizes out of range): the
+ * rotated and quantized activations and weights, the row ratios, and 8 bytes
+ * per wave of every 128 x 256 output tile for each of up to 256 candidates
+ * (their error partials). */
 size_t clq_clps_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 /*   X          fp16 [M][K] calibration activations, row stride ldx (>= K,

@@ -20,8 +20,9 @@
 //                          (Y0 - sum * x_scale * w_scale)^2 in fp64 from the
 //                          exact integer sums and keeps one partial per wave
 //                          of each output tile (no product is stored);
-//                          clps_sum_kernel adds the partials in index order,
-//                          so results are deterministic.
+//   clps_sum_kernel        one workgroup per candidate adds that candidate's
+//                          partials in index order, so results are
+//                          deterministic.
 //   clps_argmin_kernel     the smallest error, ties to the lower index.
 // The activations are rotated and quantized once.
 #include <hip/hip_fp16.h>
@@ -36,6 +37,7 @@ namespace clq {
 namespace {
 
 constexpr int kRatioThreads = 256;
+constexpr int kMaxGrid = 256;   // candidates per search (checked by the caller)
 
 // one workgroup per row; LDS holds the row
 __global__ void __launch_bounds__(kRatioThreads)
@@ -121,10 +123,14 @@ clps_grid_kernel(const float *__restrict__ ratio, int64_t N, int G, float *__res
     }
 }
 
+// workgroup g: errors[g] = the sum of partial[g * n .. g * n + n) (thread t
+// takes t, t + 256, ... in order, then a fixed tree)
 __global__ void __launch_bounds__(256)
 clps_sum_kernel(const double *__restrict__ partial, int n, double *__restrict__ out)
 {
     __shared__ double red[256];
+    partial += (int64_t)blockIdx.x * n;
+    out += blockIdx.x;
     double s = 0.0;
     for (int i = threadIdx.x; i < n; i += 256) s += partial[i];
     red[threadIdx.x] = s;
@@ -159,7 +165,8 @@ ClpsLayout clps_layout(int64_t M, int64_t N, int64_t K) {
     l.xs = off;      off += align256((size_t)M * 4);
     l.wq = off;      off += align256((size_t)padded_rows(N) * (size_t)(K / 2));
     l.ws = off;      off += align256((size_t)N * 4);
-    l.partial = off; off += align256((size_t)gemm_err_partials(M, N) * 8);
+    // room for every candidate's partials (the grid is at most kMaxGrid)
+    l.partial = off; off += align256((size_t)kMaxGrid * (size_t)gemm_err_partials(M, N) * 8);
     l.total = off;
     return l;
 }
@@ -180,6 +187,8 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
     uint8_t *wq = base + l.wq;
     float *wsc = reinterpret_cast<float *>(base + l.ws);
     double *partial = reinterpret_cast<double *>(base + l.partial);
+    const int64_t P = gemm_err_partials(M, N);
+    if (grid < 1 || grid > kMaxGrid || P > INT32_MAX) return hipErrorInvalidValue;
 
     static bool attr_set = false;
     if (!attr_set) {
@@ -198,11 +207,10 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
         e = launch_rotate_quant(W, K, perm, N, padded_rows(N), K, block, 1.0f, true, 1.0f / (float)block, wq, wsc,
                                 stream, 4, alphas + i);
         if (e != hipSuccess) return e;
-        e = launch_gemm_err(xq, xs, wq, wsc, M, N, K, Y0, ldy0, partial, stream);
+        e = launch_gemm_err(xq, xs, wq, wsc, M, N, K, Y0, ldy0, partial + (int64_t)i * P, stream);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(clps_sum_kernel, dim3(1), dim3(256), 0, stream, partial, (int)gemm_err_partials(M, N),
-                           errors + i);
     }
+    hipLaunchKernelGGL(clps_sum_kernel, dim3((unsigned)grid), dim3(256), 0, stream, partial, (int)P, errors);
     hipLaunchKernelGGL(clps_argmin_kernel, dim3(1), dim3(64), 0, stream, errors, grid, best);
     return hipGetLastError();
 }
