@@ -679,7 +679,9 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
         interleave(IC<GB>{}, IC<VH2>{}, IC<-1>{});
         __builtin_amdgcn_sched_barrier(0);
         if (cc.k == cc.ke - 1) {
-            if (cc.kb != 0) {
+            if constexpr (ERR) {   // launched with whole tiles only: no split code
+                epilogue(cc.L, cc.j, qc);
+            } else if (cc.kb != 0) {
                 contribute();
             } else {
                 if (cc.ke != nks) fixup(cc.L);
