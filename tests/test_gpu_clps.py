@@ -93,3 +93,21 @@ def test_calibration_sized_layer(clq):
     W = workloads.weights(N, K, seed=12)
     b, al = check(clq, X, W, 64, G=20)
     assert b < len(al) - 1     # clipping helps Gaussian weight rows
+
+
+@pytest.mark.parametrize("pad", [4, 3])   # aligned rows (vector loads), misaligned rows (element loads)
+def test_search_strided_target(clq, pad):
+    # the target as a column slice of a wider fp32 tensor: the fused error
+    # epilogue reads it through its row stride
+    M, N, K, b = 96, 256, 1152, 64
+    X = workloads.activations(M, K, "L1", seed=41)
+    W = workloads.weights(N, K, seed=42)
+    Y0 = oracle.linear_fp64(X, W).astype(np.float32)
+    wide = np.full((M, N + pad), np.nan, np.float32)
+    wide[:, :N] = Y0
+    al, er, best = clq.clq_clps_search(dev(X), dev(W), dev(wide)[:, :N], b, grid=8)
+    ral, rer, rbest = clps.search(X, W, Y0, b, G=8)
+    assert np.array_equal(host(al), ral)
+    assert np.allclose(host(er), rer, rtol=1e-12, atol=0)
+    bb = int(host(best)[0])
+    assert bb == rbest or abs(rer[bb] - rer[rbest]) <= 1e-12 * rer[rbest]
