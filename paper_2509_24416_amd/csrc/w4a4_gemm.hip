@@ -46,6 +46,10 @@
 // equal shares of stages for every workgroup (integer sums are exact in any
 // order); the workgroup that computes a split tile's first stages owns it
 // and adds the others' partial accumulators before its epilogue.
+//
+// With at most one tile per compute unit a second kernel runs instead
+// (w4a4_gemm_halves_kernel, below): eight waves per tile, the two halves of
+// the k loop on two waves per SIMD, summed in LDS.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -704,6 +708,263 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// each half of the eight-wave workgroup: the tile geometry of TCfg
+using TileHalf = Tile<1, 4, 4, 2, 2>;
+
+// ---- few tiles: two waves per SIMD on one tile ---------------------------------
+// With at most one tile per compute unit, a lone workgroup's k loop is bound
+// by the instruction stream of its one wave per SIMD (matrix-core work and
+// the ~180 other instructions of a stage run mostly in series).  This kernel
+// gives each tile a workgroup of eight waves: waves 0-3 run the first half of
+// the k-stages and waves 4-7 the second half, each half through its own LDS
+// ring, in lockstep on the workgroup barrier, so two waves share each SIMD.
+// The halves' integer sums meet in LDS (exact), and waves 0-3 run the
+// epilogue with the same arithmetic as the persistent kernel.
+constexpr int kHalfStages = 4;   // ring depth per half
+
+template <bool I32OUT, bool RAGGED, bool BIAS>
+__global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
+{
+    static_assert(!(I32OUT && BIAS), "no bias on the integer output");
+    using C = TileHalf;
+    constexpr int NS = kHalfStages;
+    constexpr int SLOT = C::STAGE_BYTES;
+    __shared__ __align__(16) uint8_t ring[2][NS][SLOT];
+    // the tile's epilogue operands, staged at the start: channel scales,
+    // biases (fp16), token scales
+    __shared__ float ep_ws[C::BN], ep_xs[C::BM];
+    __shared__ _Float16 ep_b[C::BN];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w8 = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = w8 >> 2, wm = w8 & 3;   // one channel panel per tile: wn = 0
+    const int M = a.M, N = a.N, nks = a.K >> 6;
+    const int L = blockIdx.x;
+    int tm, tn;
+    {
+        const int gsz = kGroupM * a.tiles_n;
+        const int g = L / gsz, r = L - g * gsz;
+        const int m0 = g * kGroupM;
+        const int gm = min(a.tiles_m - m0, kGroupM);
+        tn = r / gm;
+        tm = m0 + (r - tn * gm);
+    }
+    const int h0 = (nks + 1) >> 1;
+    const int kb = half ? h0 : 0, len = half ? nks - h0 : h0;   // len >= 1 (nks >= 2)
+    const int wunits_total = (int)(padded_rows(N) >> 5);
+    const int xunits_total = (int)(padded_act_rows(M) >> 5);
+    const uint8_t *usrc[C::UPW];
+#pragma unroll
+    for (int j = 0; j < C::UPW; ++j) {
+        const int u = wm * C::UPW + j;
+        if (u < C::W_UNITS) {
+            const int ug = min(tn * C::W_UNITS + u, wunits_total - 1);
+            usrc[j] = a.Wq + ((int64_t)ug * nks + kb) * 1024;
+        } else {
+            const int ux = min(tm * C::X_UNITS + (u - C::W_UNITS), xunits_total - 1);
+            usrc[j] = a.Xq + ((int64_t)ux * nks + kb) * 1024;
+        }
+    }
+    // stage k of this half into slot q; past the end the last stage is
+    // loaded again (into a free slot, never read), so every wave issues the
+    // same transfers and the wait counts stay fixed
+    auto produce = [&](int q, int k) {
+        const uint32_t voff = (uint32_t)(min(k, len - 1) * 1024 + lane * 16);
+        uint8_t *dst = &ring[half][q][0];
+#pragma unroll
+        for (int j = 0; j < C::UPW; ++j) {
+            const uint8_t *sp = usrc[j] + voff;
+            __builtin_amdgcn_global_load_lds(sp, (CLQ_LDS void *)(dst + (wm * C::UPW + j) * 1024), 16, 0, 0);
+        }
+    };
+    v4u pa[C::FN], pb[C::FM];
+    v4i a0[C::FN], b0[C::FM], a1[C::FN], b1[C::FM];
+    const uint32_t wl0 = (uint32_t)(lane * 16);
+    const uint32_t xl0 = (uint32_t)((C::W_UNITS + wm * C::FM) * 1024 + lane * 16);
+    auto read_packed = [&](int q) {
+        uint32_t wl = wl0, xl = xl0;
+        asm volatile("" : "+v"(wl), "+v"(xl));
+        wl += lds_addr(&ring[half][q][0]);
+        xl += lds_addr(&ring[half][q][0]);
+        static_for<0, C::FN>([&](auto f) { pa[f] = lds_read16<decltype(f)::value * 1024>(wl); });
+        static_for<0, C::FM>([&](auto f) { pb[f] = lds_read16<decltype(f)::value * 1024>(xl); });
+    };
+    auto operands_ready = [&]() {
+        static_assert(C::FN == 4 && C::FM == 2, "operand list below");
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(pa[0]), "+v"(pa[1]), "+v"(pa[2]), "+v"(pa[3]), "+v"(pb[0]), "+v"(pb[1]));
+    };
+    auto widen_half0 = [&]() {
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn) a0[fn] = widen16(pa[fn][0], pa[fn][1]);
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) b0[fm] = widen16(pb[fm][0], pb[fm][1]);
+    };
+    auto widen_half1 = [&]() {
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn) a1[fn] = widen16(pa[fn][2], pa[fn][3]);
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) b1[fm] = widen16(pb[fm][2], pb[fm][3]);
+    };
+    v16i acc[C::FN][C::FM];
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) acc[fn][fm] = v16i{};
+    auto mma = [&](const v4i (&x)[C::FN], const v4i (&y)[C::FM]) {
+#pragma unroll
+        for (int fn = 0; fn < C::FN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < C::FM; ++fm)
+                acc[fn][fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(x[fn], y[fm], acc[fn][fm], 0, 0, 0);
+    };
+    // stage i+1 has landed once only the transfers of stage i+2 (NS - 3
+    // later productions of UPW each) may be outstanding
+    static_assert(NS == 4, "wait count below");
+    auto landed_wait = [&]() {
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 3) * C::UPW) : "memory");
+    };
+
+    // epilogue operands first (one value per thread, clamped indices), then
+    // the first stages; the LDS writes land before the first barrier
+    static_assert(2 * C::BN + C::BM == 512, "one operand per thread below");
+    // (branch-free loads, so that the waits for them stay exact)
+    const int ec = tid & (C::BN - 1), er = max(tid - 2 * C::BN, 0);
+    const float *esrc = tid < 2 * C::BN ? a.ws + min(tn * C::BN + ec, N - 1) : a.xs + min(tm * C::BM + er, M - 1);
+    const float epv = *esrc;
+    _Float16 epb = (_Float16)0.0f;
+    if constexpr (BIAS) epb = reinterpret_cast<const _Float16 *>(a.bias)[min(tn * C::BN + ec, N - 1)];
+    for (int q = 0; q < NS - 1; ++q) produce(q, q);
+    if (tid < C::BN) ep_ws[ec] = epv;
+    else if (tid < 2 * C::BN) ep_b[ec] = epb;
+    else ep_xs[er] = epv;
+    landed_wait();
+    read_packed(0);
+    operands_ready();
+    widen_half0();
+    // both halves take h0 steps; a second half one stage shorter idles on
+    // its last step (wave-uniform)
+    int i = 0;
+    auto iter = [&](auto qc) -> bool {
+        constexpr int q = decltype(qc)::value;
+        constexpr int nq = (q + 1) % NS, pq = (q + NS - 1) % NS;
+        const bool active = i < len;
+        landed_wait();
+        produce(pq, i + NS - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        widen_half1();
+        if (active) mma(a0, b0);
+        read_packed(nq);
+        __builtin_amdgcn_sched_barrier(0);
+        operands_ready();
+        widen_half0();
+        if (active) mma(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        return ++i < h0;
+    };
+    while (iter(IC<0>{}) && iter(IC<1>{}) && iter(IC<2>{}) && iter(IC<3>{})) {
+    }
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    // the second half's sums into the first half's, through the (now idle)
+    // rings: two rounds of two channel fragments (64 KB each), 16-byte
+    // pieces with lanes consecutive
+    v4i *red = reinterpret_cast<v4i *>(&ring[0][0][0]);
+    static_for<0, 2>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        if (half == 1) {
+            static_for<0, 2>([&](auto fc) {
+                constexpr int f = decltype(fc)::value;
+#pragma unroll
+                for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const v16i &x = acc[2 * r + f][fm];
+                        red[(((wm * 2 + f) * C::FM + fm) * 4 + c) * 64 + lane] =
+                            v4i{x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]};
+                    }
+            });
+        }
+        __syncthreads();
+        if (half == 0) {
+            static_for<0, 2>([&](auto fc) {
+                constexpr int f = decltype(fc)::value;
+#pragma unroll
+                for (int fm = 0; fm < C::FM; ++fm)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const v4i t = red[(((wm * 2 + f) * C::FM + fm) * 4 + c) * 64 + lane];
+                        acc[2 * r + f][fm][4 * c] += t[0];
+                        acc[2 * r + f][fm][4 * c + 1] += t[1];
+                        acc[2 * r + f][fm][4 * c + 2] += t[2];
+                        acc[2 * r + f][fm][4 * c + 3] += t[3];
+                    }
+            });
+        }
+        __syncthreads();
+    });
+    if (half != 0) return;
+
+    // epilogue (waves 0-3): lane owns token m and 16 consecutive channels
+    const int h16 = (lane >> 5) * 16;
+#pragma unroll
+    for (int fn = 0; fn < C::FN; ++fn) {
+        const int c0 = fn * 32 + h16, n0 = tn * C::BN + c0;
+        float wsv[16];
+        h2v bw[8];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) wsv[v] = ep_ws[c0 + v];
+        if constexpr (BIAS) {
+#pragma unroll
+            for (int v = 0; v < 16; v += 2) bw[v / 2] = h2v{ep_b[c0 + v], ep_b[c0 + v + 1]};
+        } else {
+#pragma unroll
+            for (int v = 0; v < 8; ++v) bw[v] = h2v{(_Float16)0.0f, (_Float16)0.0f};
+        }
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) {
+            const int r0 = (wm * C::FM + fm) * 32 + (lane & 31), m = tm * C::BM + r0;
+            const v16i &x = acc[fn][fm];
+            if constexpr (I32OUT) {   // the exact integer sums
+                int32_t *dst = reinterpret_cast<int32_t *>(a.Y) + (int64_t)m * a.ldy + n0;
+                if (m < M && n0 < N) {
+                    if (!RAGGED || n0 + 16 <= N) {
+#pragma unroll
+                        for (int q4 = 0; q4 < 4; ++q4)
+                            reinterpret_cast<v4i *>(dst)[q4] =
+                                v4i{x[4 * q4] >> 8, x[4 * q4 + 1] >> 8, x[4 * q4 + 2] >> 8, x[4 * q4 + 3] >> 8};
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 16; ++v)
+                            if (n0 + v < N) dst[v] = x[v] >> 8;
+                    }
+                }
+                continue;
+            }
+            uint32_t hv[8];
+            const float xsc = ep_xs[r0] * (1.0f / 256.0f);   // accumulators hold 256 * sum
+#pragma unroll
+            for (int v = 0; v < 16; v += 2) {
+                const float p0 = (float)x[v] * xsc, p1 = (float)x[v + 1] * xsc;
+                h2v hh;
+                hh[0] = (_Float16)__builtin_fmaf(p0, wsv[v], (float)bw[v / 2][0]);
+                hh[1] = (_Float16)__builtin_fmaf(p1, wsv[v + 1], (float)bw[v / 2][1]);
+                hv[v / 2] = __builtin_bit_cast(uint32_t, hh);
+            }
+            uint16_t *dst = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)m * a.ldy + n0;
+            if (m < M && n0 < N) {
+                if (!RAGGED || n0 + 16 <= N) {
+                    reinterpret_cast<v4u *>(dst)[0] = v4u{hv[0], hv[1], hv[2], hv[3]};
+                    reinterpret_cast<v4u *>(dst)[1] = v4u{hv[4], hv[5], hv[6], hv[7]};
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v)
+                        if (n0 + v < N) dst[v] = (uint16_t)(hv[v >> 1] >> (16 * (v & 1)));
+                }
+            }
+        }
+    }
+}
+
 // four waves of 128 channels x 64 tokens: 128 channels x 256 tokens per
 // workgroup, two workgroups per compute unit
 using TCfg = Tile<1, 4, 4, 2, 2>;
@@ -731,7 +992,7 @@ int full_grid() { return (device_cus() * TCfg::WGS + 7) / 8 * 8; }
 // summed from at most nks / kSplitMinShare + 1 pieces).
 constexpr int kSplitMinSaved = 16;
 constexpr int kSplitMinShare = 8;
-constexpr int kSplitMinLong = 32;   // k-stages (K >= 2048) for the few-tile split
+constexpr int kHalvesMinStages = 4;   // k-stages for the eight-wave kernel
 
 template <class C, bool I32OUT, bool RAGGED, bool BIAS, bool ERR = false>
 hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
@@ -739,22 +1000,6 @@ hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
     int grid = full_grid();
     g.dp = ntiles;
     g.sk = 0;
-    if (may_split && ntiles < grid && nks >= kSplitMinLong) {
-        // fewer tiles than workgroup slots and a long k loop: every tile is
-        // cut along k over as many workgroups as keep shares of
-        // kSplitMinShare stages or more, when that at least doubles the
-        // workgroups at work (all of them fit on the chip at once, so an
-        // owner never waits for one not started).  With short k loops the
-        // partial-sum exchange costs more than the shorter chains save.
-        const int64_t units = (int64_t)ntiles * nks;
-        const int g2 = (int)std::min<int64_t>(grid, units / kSplitMinShare) / 8 * 8;
-        if (g2 >= 2 * ntiles) {
-            g.dp = 0;
-            g.sk = (int)units;
-            hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS, ERR>), dim3((unsigned)g2), dim3(C::NT), 0, stream, g);
-            return hipGetLastError();
-        }
-    }
     if (may_split && ntiles % grid != 0) {
         // whole tiles for all but the last one or two rounds; the rest is
         // spread over every workgroup in k-stage units (1 to 2 tiles each)
@@ -800,6 +1045,26 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
     g.part = workspace ? reinterpret_cast<int32_t *>(reinterpret_cast<uint8_t *>(workspace) + G * TCfg::NW * sizeof(int))
                        : nullptr;
     const bool may_split = workspace != nullptr;
+    // at most one tile per compute unit and a k loop worth halving: eight
+    // waves per tile
+    const int ntiles = g.tiles_m * g.tiles_n;
+    if (ntiles <= device_cus() && (K >> 6) >= kHalvesMinStages) {
+        const bool rag = N % 16 != 0;
+        const dim3 grid((unsigned)ntiles), block(512);
+        if (i32out && rag)
+            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<true, true, false>), grid, block, 0, stream, g);
+        else if (i32out)
+            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<true, false, false>), grid, block, 0, stream, g);
+        else if (bias && rag)
+            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, true, true>), grid, block, 0, stream, g);
+        else if (bias)
+            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, false, true>), grid, block, 0, stream, g);
+        else if (rag)
+            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, true, false>), grid, block, 0, stream, g);
+        else
+            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, false, false>), grid, block, 0, stream, g);
+        return hipGetLastError();
+    }
     // ragged channel edges, and biases not 4-byte aligned (the fast path
     // moves them in channel pairs), use element-wise epilogue accesses
     const bool ragged = N % 16 != 0 || (bias && reinterpret_cast<uintptr_t>(bias) % 4 != 0);

@@ -144,8 +144,11 @@ def test_quantize_weights_perm(clq):
 
 # ---- GEMM: exact accumulators and the fp16 epilogue ------------------------------
 
+# few tiles and at least 4 k-stages go through the eight-wave kernel (its two
+# halves of the k loop summed in LDS), including odd stage counts (one half a
+# stage shorter) and ragged channels
 GEMM_SHAPES = [(1, 1, 64), (7, 8, 128), (129, 72, 192), (257, 200, 1152), (64, 1152, 1152),
-               (300, 130, 640), (128, 128, 128), (513, 264, 4608)]
+               (300, 130, 640), (128, 128, 128), (513, 264, 4608), (257, 200, 576), (100, 1001, 320)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
@@ -162,10 +165,8 @@ def test_accum_i32_bitexact(clq, M, N, K, workspace):
     assert np.array_equal(host(acc), oracle.gemm_i32(xc, wc))
 
 
-# Shapes whose last tile round is split along k over every workgroup (few
-# tiles, long k): each tile is summed from the partials of many workgroups.
-# The last two have fewer tiles than workgroup slots and a long k loop:
-# every tile is cut along k over a smaller grid.
+# Few tiles and a long k loop (the eight-wave kernel at these sizes), called
+# repeatedly with a shared workspace.
 SPLIT_SHAPES = [(2048, 1152, 4608), (2000, 1000, 4608), (2048, 640, 8192), (1024, 1152, 4608), (300, 520, 8192)]
 
 
@@ -186,6 +187,27 @@ def test_split_k_exact_and_repeatable(clq, M, N, K):
         assert oracle.err_metric(host(Y).astype(np.float64), ref["y64"], ref["p64"], b) <= TOL, rep
     groups = clq.clq_w4a4_workspace_bytes() // (128 * 256 * 4 + 4 * 4)
     assert not host(ws[:groups * 4 * 4]).any()     # every flag back at zero
+
+
+def test_persistent_tail_split_exact(clq):
+    # more tiles than compute units (the persistent kernel), a last round
+    # split along k over every workgroup: the split sums equal the
+    # whole-tile sums bit for bit and the oracle's on sampled rows
+    M, N, K, block = 4352, 2048, 2432, 64     # 17 x 16 tiles, 38 k-stages
+    X = workloads.activations(M, K, "L1", seed=61)
+    W = workloads.weights(N, K, seed=62)
+    qw = clq.clq_quantize_weights(dev(W), block)
+    Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
+    ws = torch.zeros(clq.clq_w4a4_workspace_bytes(), dtype=torch.uint8, device="cuda")
+    split = host(clq.clq_w4a4_accum_i32(Xq, xs, qw, workspace=ws))
+    whole = host(clq.clq_w4a4_accum_i32(Xq, xs, qw, workspace=False))
+    assert np.array_equal(split, whole)
+    rows = np.r_[0:3, 2047:2051, M - 3:M]
+    _, xc, _ = oracle.quantize_act(X[rows], block)
+    _, wc, _ = oracle.quantize_weights(W, block)
+    assert np.array_equal(split[rows], oracle.gemm_i32(xc, wc))
+    groups = clq.clq_w4a4_workspace_bytes() // (128 * 256 * 4 + 4 * 4)
+    assert not host(ws[:groups * 4 * 4]).any()
 
 
 def test_accum_i32_extremes(clq):
