@@ -729,7 +729,11 @@ __global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
     using C = TileHalf;
     constexpr int NS = kHalfStages;
     constexpr int SLOT = C::STAGE_BYTES;
-    __shared__ __align__(16) uint8_t ring[2][NS][SLOT];
+    // the two rings (96 KB), reused at the end for the exchange of the
+    // halves' sums (2 x 64 KB)
+    constexpr int kExch = 65536;
+    __shared__ __align__(16) uint8_t pool[2 * NS * SLOT > 2 * kExch ? 2 * NS * SLOT : 2 * kExch];
+    auto ring = reinterpret_cast<uint8_t (*)[NS][SLOT]>(pool);
     // the tile's epilogue operands, staged at the start: channel scales,
     // biases (fp16), token scales
     __shared__ float ep_ws[C::BN], ep_xs[C::BM];
@@ -865,49 +869,53 @@ __global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
     }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
-    // the second half's sums into the first half's, through the (now idle)
-    // rings: two rounds of two channel fragments (64 KB each), 16-byte
-    // pieces with lanes consecutive
-    v4i *red = reinterpret_cast<v4i *>(&ring[0][0][0]);
-    static_for<0, 2>([&](auto rc) {
-        constexpr int r = decltype(rc)::value;
-        if (half == 1) {
-            static_for<0, 2>([&](auto fc) {
-                constexpr int f = decltype(fc)::value;
+    // the halves swap sums through the idle rings: half 0 finishes channel
+    // fragments 0-1 and half 1 fragments 2-3, each adding the other's
+    // partial (64 KB each way, 16-byte pieces with lanes consecutive)
+    auto send = [&](auto f0c) {
+        constexpr int f0 = decltype(f0c)::value;
+        v4i *out = reinterpret_cast<v4i *>(pool + half * kExch);
+        static_for<0, 2>([&](auto fc) {
+            constexpr int f = decltype(fc)::value;
 #pragma unroll
-                for (int fm = 0; fm < C::FM; ++fm)
+            for (int fm = 0; fm < C::FM; ++fm)
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) {
-                        const v16i &x = acc[2 * r + f][fm];
-                        red[(((wm * 2 + f) * C::FM + fm) * 4 + c) * 64 + lane] =
-                            v4i{x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]};
-                    }
-            });
-        }
-        __syncthreads();
-        if (half == 0) {
-            static_for<0, 2>([&](auto fc) {
-                constexpr int f = decltype(fc)::value;
+                for (int c = 0; c < 4; ++c) {
+                    const v16i &x = acc[f0 + f][fm];
+                    out[(((wm * 2 + f) * C::FM + fm) * 4 + c) * 64 + lane] =
+                        v4i{x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]};
+                }
+        });
+    };
+    auto receive = [&](auto f0c) {
+        constexpr int f0 = decltype(f0c)::value;
+        const v4i *in = reinterpret_cast<const v4i *>(pool + (1 - half) * kExch);
+        static_for<0, 2>([&](auto fc) {
+            constexpr int f = decltype(fc)::value;
 #pragma unroll
-                for (int fm = 0; fm < C::FM; ++fm)
+            for (int fm = 0; fm < C::FM; ++fm)
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) {
-                        const v4i t = red[(((wm * 2 + f) * C::FM + fm) * 4 + c) * 64 + lane];
-                        acc[2 * r + f][fm][4 * c] += t[0];
-                        acc[2 * r + f][fm][4 * c + 1] += t[1];
-                        acc[2 * r + f][fm][4 * c + 2] += t[2];
-                        acc[2 * r + f][fm][4 * c + 3] += t[3];
-                    }
-            });
-        }
-        __syncthreads();
-    });
-    if (half != 0) return;
+                for (int c = 0; c < 4; ++c) {
+                    const v4i t = in[(((wm * 2 + f) * C::FM + fm) * 4 + c) * 64 + lane];
+                    acc[f0 + f][fm][4 * c] += t[0];
+                    acc[f0 + f][fm][4 * c + 1] += t[1];
+                    acc[f0 + f][fm][4 * c + 2] += t[2];
+                    acc[f0 + f][fm][4 * c + 3] += t[3];
+                }
+        });
+    };
+    if (half == 0) send(IC<2>{});
+    else send(IC<0>{});
+    __syncthreads();
+    if (half == 0) receive(IC<0>{});
+    else receive(IC<2>{});
 
-    // epilogue (waves 0-3): lane owns token m and 16 consecutive channels
+    // epilogue: lane owns token m and 16 consecutive channels; each half
+    // its two channel fragments
     const int h16 = (lane >> 5) * 16;
-#pragma unroll
-    for (int fn = 0; fn < C::FN; ++fn) {
+    auto epilogue = [&](auto f0c) {
+    static_for<0, 2>([&](auto fc) {
+        constexpr int fn = decltype(f0c)::value + decltype(fc)::value;
         const int c0 = fn * 32 + h16, n0 = tn * C::BN + c0;
         float wsv[16];
         h2v bw[8];
@@ -962,7 +970,10 @@ __global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
                 }
             }
         }
-    }
+    });
+    };
+    if (half == 0) epilogue(IC<0>{});
+    else epilogue(IC<2>{});
 }
 
 // four waves of 128 channels x 64 tokens: 128 channels x 256 tokens per
