@@ -15,7 +15,8 @@
 //   clps_grid_kernel       alpha_lo = min of the row ratios; the G candidates
 //                          alpha_i = 1 - ((1 - alpha_lo)(G-1-i)) / (G-1).
 //   per candidate          the hot path's weight quantizer with alpha_i read
-//                          from device memory, then the W4A4 GEMM in its
+//                          from device memory (four candidates per launch,
+//                          each into its own buffer), then the W4A4 GEMM in its
 //                          squared-error mode: the epilogue forms
 //                          (Y0 - sum * x_scale * w_scale)^2 in fp64 from the
 //                          exact integer sums and keeps one partial per wave
@@ -38,6 +39,7 @@ namespace {
 
 constexpr int kRatioThreads = 256;
 constexpr int kMaxGrid = 256;   // candidates per search (checked by the caller)
+constexpr int kQuantBatch = 4;  // candidates whose weights one quantizer launch writes
 
 // one workgroup per row; LDS holds the row
 __global__ void __launch_bounds__(kRatioThreads)
@@ -153,6 +155,7 @@ __global__ void clps_argmin_kernel(const double *__restrict__ errors, int G, int
 
 struct ClpsLayout {
     size_t ratio, xq, xs, wq, ws, partial, total;
+    size_t wq_stride, ws_stride;   // between the quantized weights of a batch's candidates
 };
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
@@ -163,8 +166,10 @@ ClpsLayout clps_layout(int64_t M, int64_t N, int64_t K) {
     l.ratio = off;   off += align256((size_t)N * 4);
     l.xq = off;      off += align256((size_t)padded_act_rows(M) * (size_t)(K / 2));
     l.xs = off;      off += align256((size_t)M * 4);
-    l.wq = off;      off += align256((size_t)padded_rows(N) * (size_t)(K / 2));
-    l.ws = off;      off += align256((size_t)N * 4);
+    l.wq_stride = align256((size_t)padded_rows(N) * (size_t)(K / 2));
+    l.ws_stride = align256((size_t)N * 4);
+    l.wq = off;      off += kQuantBatch * l.wq_stride;
+    l.ws = off;      off += kQuantBatch * l.ws_stride;
     // room for every candidate's partials (the grid is at most kMaxGrid)
     l.partial = off; off += align256((size_t)kMaxGrid * (size_t)gemm_err_partials(M, N) * 8);
     l.total = off;
@@ -203,12 +208,19 @@ hipError_t launch_clps(const uint16_t *X, int64_t ldx, const uint16_t *W, const 
     hipError_t e = launch_rotate_quant(X, ldx, perm, M, padded_act_rows(M), K, block, 1.0f, false, 1.0f, xq, xs,
                                        stream);
     if (e != hipSuccess) return e;
-    for (int i = 0; i < grid; ++i) {
+    const int64_t wqs = (int64_t)l.wq_stride, wss = (int64_t)(l.ws_stride / 4);
+    for (int i0 = 0; i0 < grid; i0 += kQuantBatch) {
+        // the weights of up to kQuantBatch candidates in one launch, then
+        // one GEMM per candidate
+        const int nc = std::min(kQuantBatch, grid - i0);
         e = launch_rotate_quant(W, K, perm, N, padded_rows(N), K, block, 1.0f, true, 1.0f / (float)block, wq, wsc,
-                                stream, 4, alphas + i);
+                                stream, 4, alphas + i0, nc, wqs, wss);
         if (e != hipSuccess) return e;
-        e = launch_gemm_err(xq, xs, wq, wsc, M, N, K, Y0, ldy0, partial + (int64_t)i * P, stream);
-        if (e != hipSuccess) return e;
+        for (int c = 0; c < nc; ++c) {
+            e = launch_gemm_err(xq, xs, wq + c * wqs, wsc + c * wss, M, N, K, Y0, ldy0,
+                                partial + (int64_t)(i0 + c) * P, stream);
+            if (e != hipSuccess) return e;
+        }
     }
     hipLaunchKernelGGL(clps_sum_kernel, dim3((unsigned)grid), dim3(256), 0, stream, partial, (int)P, errors);
     hipLaunchKernelGGL(clps_argmin_kernel, dim3(1), dim3(64), 0, stream, errors, grid, best);

@@ -73,11 +73,15 @@ __host__ __device__ inline int64_t q8_piece_offset(int64_t u, int rho, int64_t c
 
 // bits: 4 (packed int4 layouts above) or 8 (int8 layout).  alpha_dev, when
 // given, holds the weights' clip ratio in device memory (alpha is then unused).
+// batch > 1 (weights with alpha_dev only): batch quantizations of the same
+// rows, quantization y with clip ratio alpha_dev[y] into out + y * out_stride
+// and scale + y * scale_stride.
 hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *perm,
                                int64_t rows, int64_t rows_alloc, int K, int block,
                                float alpha, bool weight_mode, float post_scale,
                                uint8_t *out, float *scale, hipStream_t stream, int bits = 4,
-                               const float *alpha_dev = nullptr);
+                               const float *alpha_dev = nullptr, int batch = 1, int64_t out_stride = 0,
+                               int64_t scale_stride = 0);
 
 // Single-layer clip search (CLPS): workspace bytes and the whole search.
 size_t clps_workspace_bytes(int64_t M, int64_t N, int64_t K);

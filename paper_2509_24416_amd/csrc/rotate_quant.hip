@@ -139,9 +139,15 @@ __global__ void __launch_bounds__(rq_max_threads<B>())
 rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
                     const int32_t *__restrict__ perm, int64_t rows_valid,
                     int64_t rows_alloc, int K, int R, float alpha, const float *__restrict__ alpha_dev,
-                    float post_scale, uint8_t *__restrict__ out, float *__restrict__ scale_out)
+                    float post_scale, uint8_t *__restrict__ out, float *__restrict__ scale_out,
+                    int64_t out_stride, int64_t scale_stride)
 {
     extern __shared__ __align__(16) unsigned char smem[];
+    // blockIdx.y selects one of several quantizations of the same rows
+    // (clip ratio alpha_dev[y], outputs at y * stride)
+    out += (int64_t)blockIdx.y * out_stride;
+    scale_out += (int64_t)blockIdx.y * scale_stride;
+    if (alpha_dev != nullptr) alpha_dev += blockIdx.y;
     constexpr int CPB = B / 8;            // 16-byte chunks per block
     const int cpr = K >> 3;               // chunks per row
     const int nb = K / B;                 // blocks per row
@@ -619,7 +625,8 @@ template <int B, bool WEIGHT, int QB>
 hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
                      int64_t rows_valid, int64_t rows_alloc, int K, float alpha,
                      float post_scale, uint8_t *out, float *scale, hipStream_t stream,
-                     const float *alpha_dev = nullptr) {
+                     const float *alpha_dev = nullptr, int batch = 1, int64_t out_stride = 0,
+                     int64_t scale_stride = 0) {
     const int R = pick_rows(K, B);
     const int nb = K / B;
     const int T = (R * nb + 63) / 64 * 64;
@@ -633,9 +640,9 @@ hipError_t launch_rq(const uint16_t *X, int64_t ldx, const int32_t *perm,
         attr_set = true;
     }
     const int64_t grid = (rows_alloc + R - 1) / R;
-    hipLaunchKernelGGL((rotate_quant_kernel<B, WEIGHT, QB>), dim3((unsigned)grid), dim3(T), lds,
+    hipLaunchKernelGGL((rotate_quant_kernel<B, WEIGHT, QB>), dim3((unsigned)grid, (unsigned)batch), dim3(T), lds,
                        stream, X, ldx, perm, rows_valid, rows_alloc, K, R, alpha, alpha_dev, post_scale,
-                       out, scale);
+                       out, scale, out_stride, scale_stride);
     return hipGetLastError();
 }
 
@@ -754,12 +761,13 @@ template <int QB>
 hipError_t launch_rq_bits(const uint16_t *X, int64_t ldx, const int32_t *perm,
                           int64_t rows, int64_t rows_alloc, int K, int block,
                           float alpha, bool weight_mode, float post_scale,
-                          uint8_t *out, float *scale, hipStream_t stream, const float *alpha_dev) {
+                          uint8_t *out, float *scale, hipStream_t stream, const float *alpha_dev, int batch,
+                          int64_t out_stride, int64_t scale_stride) {
     if (weight_mode) {
         switch (block) {
-            case 32: return launch_rq<32, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev);
-            case 64: return launch_rq<64, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev);
-            case 128: return launch_rq<128, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev);
+            case 32: return launch_rq<32, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev, batch, out_stride, scale_stride);
+            case 64: return launch_rq<64, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev, batch, out_stride, scale_stride);
+            case 128: return launch_rq<128, true, QB>(X, ldx, perm, rows, rows_alloc, K, alpha, post_scale, out, scale, stream, alpha_dev, batch, out_stride, scale_stride);
         }
     } else {
         switch (block) {
@@ -775,13 +783,14 @@ hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *pe
                                int64_t rows, int64_t rows_alloc, int K, int block,
                                float alpha, bool weight_mode, float post_scale,
                                uint8_t *out, float *scale, hipStream_t stream, int bits,
-                               const float *alpha_dev) {
+                               const float *alpha_dev, int batch, int64_t out_stride, int64_t scale_stride) {
+    if (batch > 1 && (!weight_mode || alpha_dev == nullptr)) return hipErrorInvalidValue;
     if (bits == 8)
         return launch_rq_bits<8>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
-                                 out, scale, stream, alpha_dev);
+                                 out, scale, stream, alpha_dev, batch, out_stride, scale_stride);
     if (bits == 4)
         return launch_rq_bits<4>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
-                                 out, scale, stream, alpha_dev);
+                                 out, scale, stream, alpha_dev, batch, out_stride, scale_stride);
     return hipErrorInvalidValue;
 }
 
