@@ -351,9 +351,9 @@ def main():
                          "byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported "
-              "(the hot path shards by token rows with no collective; see the design notes)",
-              file=sys.stderr)
+        print(f"bench.py: the benchmark runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the hot path would shard by token rows with no collective: each GPU runs the same "
+              "kernels on its share of the rows)", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -45,7 +45,7 @@ def _load():
     if _lib is not None:
         return _lib
     if not os.path.exists(_LIB_PATH):
-        from . import build as _b  # building the checker is not running it
+        from . import build as _b  # building the oracle is not running it
         _b.build()
     lib = ctypes.CDLL(_LIB_PATH)
     lib.clqo_set_threads.argtypes = [ctypes.c_int]
