@@ -148,7 +148,8 @@ def test_quantize_weights_perm(clq):
 # halves of the k loop summed in LDS), including odd stage counts (one half a
 # stage shorter) and ragged channels
 GEMM_SHAPES = [(1, 1, 64), (7, 8, 128), (129, 72, 192), (257, 200, 1152), (64, 1152, 1152),
-               (300, 130, 640), (128, 128, 128), (513, 264, 4608), (257, 200, 576), (100, 1001, 320)]
+               (300, 130, 640), (128, 128, 128), (513, 264, 4608), (257, 200, 576), (100, 1001, 320),
+               (33, 48, 256), (5, 3, 256)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
