@@ -21,8 +21,10 @@
 //                          (16 copies of the accumulators spread the
 //                          atomics of different workgroups.)
 //   obs_column_kernel<M>   one workgroup per channel over the mean matrix:
-//                          pairwise sum (peak-to-average ratio) or a bitonic
-//                          sort in LDS (top-k mean, percentile).
+//                          pairwise sum (peak-to-average ratio), or a radix
+//                          select in LDS (top-k mean: the k-th largest, then
+//                          the k largest sorted; percentile: two order
+//                          statistics).
 //   obs_rank_kernel        how many channels beat each channel, over ranges
 //                          of the scores split across workgroups.
 //   obs_partition_kernel   one workgroup: the top half (beaten by fewer than
@@ -169,6 +171,52 @@ __global__ void obs_finish_kernel(uint32_t *__restrict__ acc, int D, int metric,
 constexpr int kColThreads = 1024;
 constexpr int kMaxTopk = 512;   // k <= (32768 + 50) / 100 = 328
 
+// The rank-th smallest (0-based) of the n keys in LDS, by four passes over
+// 8-bit digits from the top: a histogram of the keys that match the digits
+// chosen so far, then a scan of the 256 bins for the one holding the rank.
+// Called by every thread of the workgroup; returns the key.
+__device__ uint32_t radix_select(const uint32_t *keys, int n, int rank, uint32_t *hist, uint32_t *wsum,
+                                 uint32_t *pick)
+{
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    uint32_t prefix = 0u, mask = 0u;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        for (int i = t; i < 256; i += kColThreads) hist[i] = 0u;
+        __syncthreads();
+        for (int i = t; i < n; i += kColThreads) {
+            const uint32_t k = keys[i];
+            if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        // inclusive scan of the 256 counts (threads 0-255: four waves)
+        uint32_t c = 0u, inc = 0u;
+        if (t < 256) {
+            c = hist[t];
+            inc = c;
+            for (int off = 1; off < 64; off <<= 1) {
+                const uint32_t o = __shfl_up(inc, off);
+                if (lane >= off) inc += o;
+            }
+            if (lane == 63) wsum[wv] = inc;
+        }
+        __syncthreads();
+        if (t < 256) {
+            for (int w = 0; w < wv; ++w) inc += wsum[w];
+            const uint32_t exc = inc - c;
+            if (exc <= (uint32_t)rank && (uint32_t)rank < inc) {   // exactly one bin
+                pick[0] = (uint32_t)t;
+                pick[1] = exc;
+            }
+        }
+        __syncthreads();
+        prefix |= pick[0] << shift;
+        mask |= 255u << shift;
+        rank -= (int)pick[1];
+        __syncthreads();   // pick and hist are rewritten by the next pass
+    }
+    return prefix;
+}
+
 // METRIC 2: peak-to-average ratio, 3: top-k mean, 4: percentile spread
 template <int METRIC>
 __global__ void __launch_bounds__(kColThreads)
@@ -176,20 +224,27 @@ obs_column_kernel(const float *__restrict__ S, int64_t N, int D, int P, float *_
 {
     extern __shared__ float w[];   // [P]
     __shared__ float top[kMaxTopk];
-    __shared__ uint32_t peak;
-    const int d = blockIdx.x, t = threadIdx.x;
-    if (t == 0) peak = 0u;
+    __shared__ uint32_t peak, hist[256], wsum[4], pick[2], cnt;
+    // Workgroups go round-robin over the eight XCDs; each XCD takes a run of
+    // D / 8 adjacent channels, so the column reads (one float per 128-byte
+    // line) share lines in that XCD's L2.  A bijection for D % 8 == 0.
+    const int d = (int)(blockIdx.x & 7u) * (D >> 3) + (int)(blockIdx.x >> 3), t = threadIdx.x;
+    if (t == 0) {
+        peak = 0u;
+        cnt = 0u;
+    }
     __syncthreads();
     uint32_t pk = 0u;
+    uint32_t *keys = reinterpret_cast<uint32_t *>(w);
     for (int i = t; i < P; i += kColThreads) {
         const float v = i < N ? S[(int64_t)i * D + d] : 0.0f;
         if constexpr (METRIC == 2) {
             w[i] = fabsf(v);
             pk = max(pk, __float_as_uint(fabsf(v)));
         } else if constexpr (METRIC == 3) {
-            w[i] = i < N ? fabsf(v) : -1.0f;              // padding sorts first
+            keys[i] = __float_as_uint(fabsf(v));   // non-negative: ordered as integers
         } else {
-            w[i] = i < N ? v : __builtin_inff();          // padding sorts last
+            keys[i] = ord_enc(v);
         }
     }
     if constexpr (METRIC == 2) atomicMax(&peak, pk);
@@ -205,40 +260,50 @@ obs_column_kernel(const float *__restrict__ S, int64_t N, int D, int P, float *_
         }
         return;
     }
-    // bitonic sort, ascending
-    for (int k = 2; k <= P; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = t; i < P; i += kColThreads) {
-                const int l = i ^ j;
-                if (l > i) {
-                    const float a = w[i], b = w[l];
-                    const bool up = (i & k) == 0;
-                    if ((a > b) == up) {
-                        w[i] = b;
-                        w[l] = a;
-                    }
-                }
-            }
-            __syncthreads();
-        }
-    }
+    const int n = (int)N;
     if constexpr (METRIC == 3) {
         const int kk = (int)std::max<int64_t>(1, (N + 50) / 100);
         int kp = 1;
         while (kp < kk) kp <<= 1;
-        // the k largest, in descending order, zero-padded; then pairwise
-        for (int i = t; i < kp; i += kColThreads) top[i] = i < kk ? w[P - 1 - i] : 0.0f;
+        // the kk-th largest; the values above it, then copies of it: the kk
+        // largest as a multiset
+        const uint32_t thr = radix_select(keys, n, n - kk, hist, wsum, pick);
+        for (int i = t; i < n; i += kColThreads) {
+            const uint32_t k = keys[i];
+            if (k > thr) top[atomicAdd(&cnt, 1u)] = __uint_as_float(k);
+        }
         __syncthreads();
+        const int above = (int)cnt;
+        for (int i = above + t; i < kp; i += kColThreads) top[i] = i < kk ? __uint_as_float(thr) : 0.0f;
+        __syncthreads();
+        // descending bitonic sort of the kp entries (the zero padding ends up
+        // last), then the pairwise sum
+        for (int k = 2; k <= kp; k <<= 1) {
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                for (int i = t; i < kp; i += kColThreads) {
+                    const int l = i ^ j;
+                    if (l > i) {
+                        const float a = top[i], b = top[l];
+                        const bool down = (i & k) == 0;
+                        if ((a < b) == down) {
+                            top[i] = b;
+                            top[l] = a;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
         for (int p = kp >> 1; p >= 1; p >>= 1) {
             for (int i = t; i < p; i += kColThreads) top[i] = top[i] + top[i + p];
             __syncthreads();
         }
         if (t == 0) scores[d] = top[0] / (float)kk;
     } else {
-        if (t == 0) {
-            const int64_t lo = (N - 1) / 100, hi = N - 1 - lo;
-            scores[d] = w[hi] - w[lo];
-        }
+        const int lo = (n - 1) / 100, hi = n - 1 - lo;
+        const uint32_t khi = radix_select(keys, n, hi, hist, wsum, pick);
+        const uint32_t klo = radix_select(keys, n, lo, hist, wsum, pick);
+        if (t == 0) scores[d] = ord_dec(khi) - ord_dec(klo);
     }
 }
 
