@@ -70,11 +70,32 @@ __device__ __forceinline__ int act_slot(int i, int j, int r, int R) {
     else return chunk_slot<B>(i, j);
 }
 
-__device__ __forceinline__ float half_lo(uint32_t w) {
-    return __half2float(__ushort_as_half((unsigned short)(w & 0xffffu)));
+// Butterfly stage h = 1 straight from fp16 inputs.  The mixed-precision fma
+// reads an f16 half of each source register and rounds u * 1 + s (or
+// u * 1 - s) once to fp32: the value of converting both halves (exact) and
+// adding, bit for bit over all 2^32 pairs of halves, in one instruction per
+// output instead of two conversions and an add per pair.
+__device__ __forceinline__ void stage1_packed(uint32_t w, float &sum, float &dif) {
+    asm("v_fma_mix_f32 %0, %1, 1.0, %1 op_sel:[0,0,1] op_sel_hi:[1,0,1]" : "=v"(sum) : "v"(w));
+    asm("v_fma_mix_f32 %0, %1, 1.0, -%1 op_sel:[0,0,1] op_sel_hi:[1,0,1]" : "=v"(dif) : "v"(w));
 }
-__device__ __forceinline__ float half_hi(uint32_t w) {
-    return __half2float(__ushort_as_half((unsigned short)(w >> 16)));
+// the same from the low halves of two registers (gathered inputs)
+__device__ __forceinline__ void stage1_pair(uint32_t u, uint32_t v, float &sum, float &dif) {
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel_hi:[1,0,1]" : "=v"(sum) : "v"(u), "v"(v));
+    asm("v_fma_mix_f32 %0, %1, 1.0, -%2 op_sel_hi:[1,0,1]" : "=v"(dif) : "v"(u), "v"(v));
+}
+
+// Largest |x| of a block: one three-operand max per pair of elements, in two
+// independent chains (a max is exact, so the order does not matter).
+template <int B>
+__device__ __forceinline__ float block_absmax(const float *x) {
+    float m0 = 0.0f, m1 = 0.0f;
+#pragma unroll
+    for (int i = 0; i < B; i += 4) {
+        m0 = fmaxf(fmaxf(m0, fabsf(x[i])), fabsf(x[i + 1]));
+        m1 = fmaxf(fmaxf(m1, fabsf(x[i + 2])), fabsf(x[i + 3]));
+    }
+    return fmaxf(m0, m1);
 }
 
 // Packs eight quantized words (code + 8 in bits 0..3, bits 4..21 clear) into
@@ -193,9 +214,7 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
                 const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float u = half_lo(w[e]), s = half_hi(w[e]);
-                    x[8 * i + 2 * e] = u + s;       // stage h = 1
-                    x[8 * i + 2 * e + 1] = u - s;
+                    stage1_packed(w[e], x[8 * i + 2 * e], x[8 * i + 2 * e + 1]);   // stage h = 1
                 }
             }
         } else {
@@ -207,10 +226,7 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
                 const int c0 = k0 >> 3, c1 = k1 >> 3;
                 const int s0 = (c0 / CPB) * CPB + chunk_slot<B>(c0 % CPB, c0 / CPB);
                 const int s1 = (c1 / CPB) * CPB + chunk_slot<B>(c1 % CPB, c1 / CPB);
-                const float u = __half2float(__ushort_as_half(rowh[s0 * 8 + (k0 & 7)]));
-                const float s = __half2float(__ushort_as_half(rowh[s1 * 8 + (k1 & 7)]));
-                x[e] = u + s;
-                x[e + 1] = u - s;
+                stage1_pair(rowh[s0 * 8 + (k0 & 7)], rowh[s1 * 8 + (k1 & 7)], x[e], x[e + 1]);
             }
         }
 #pragma unroll
@@ -224,8 +240,7 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
                 }
             }
         }
-#pragma unroll
-        for (int i = 0; i < B; ++i) bmax = fmaxf(bmax, fabsf(x[i]));
+        bmax = block_absmax<B>(x);
         atomicMax(&rowmax[r], __float_as_uint(bmax));
     }
     __syncthreads();
@@ -284,7 +299,9 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
 // barrier per batch: before it, block maxima meet in rowmax[i % 3]; after it,
 // codes are formed and stored.  The third rowmax buffer is cleared one batch
 // after its use, when no lane can still be reading it.
-template <int B, int QB>
+// GATHER: perm is set (a separate instance, so that the loads of the
+// permutation leave no pending-load state in the ungathered loop)
+template <int B, int QB, bool GATHER>
 __global__ void __launch_bounds__(256)
 rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__restrict__ perm,
               int64_t rows_valid, int64_t rows_alloc, int64_t nbatch, int K, int R,
@@ -358,7 +375,7 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
         float x[B];
         if (active) {
             float bmax = 0.0f;
-            if (perm == nullptr) {
+            if constexpr (!GATHER) {
                 const uint4 *src = tcur + r * cpr + j * CPB;
 #pragma unroll
                 for (int ii = 0; ii < CPB; ++ii) {
@@ -366,9 +383,7 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
                     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float u = half_lo(w[e]), s = half_hi(w[e]);
-                        x[8 * ii + 2 * e] = u + s;       // stage h = 1
-                        x[8 * ii + 2 * e + 1] = u - s;
+                        stage1_packed(w[e], x[8 * ii + 2 * e], x[8 * ii + 2 * e + 1]);   // stage h = 1
                     }
                 }
             } else {
@@ -380,10 +395,7 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
                     const int c0 = k0 >> 3, c1 = k1 >> 3;
                     const int s0 = (c0 / CPB) * CPB + act_slot<B>(c0 % CPB, c0 / CPB, r, R);
                     const int s1 = (c1 / CPB) * CPB + act_slot<B>(c1 % CPB, c1 / CPB, r, R);
-                    const float u = __half2float(__ushort_as_half(rowh[s0 * 8 + (k0 & 7)]));
-                    const float s = __half2float(__ushort_as_half(rowh[s1 * 8 + (k1 & 7)]));
-                    x[e] = u + s;
-                    x[e + 1] = u - s;
+                    stage1_pair(rowh[s0 * 8 + (k0 & 7)], rowh[s1 * 8 + (k1 & 7)], x[e], x[e + 1]);
                 }
             }
 #pragma unroll
@@ -397,8 +409,7 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
                     }
                 }
             }
-#pragma unroll
-            for (int ii = 0; ii < B; ii += 2) bmax = fmaxf(bmax, fmaxf(fabsf(x[ii]), fabsf(x[ii + 1])));
+            bmax = block_absmax<B>(x);
             atomicMax(&rm[r], __float_as_uint(bmax));
         }
         // 2. the next batch into the other buffer, the one after into registers
@@ -441,14 +452,17 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
 // written by several batches cost long-row launches about 40% at full HBM
 // rate.  One workgroup per CU with one LDS buffer of 8 rows; the next batch
 // waits in registers.  Two barriers per batch: after the block reads (the
-// buffer may be refilled) and after the block maxima (codes may be formed).
-// Codes of batch i are formed at the top of iteration i+1, from the
-// registers that still hold its rotated blocks.
+// buffer may be refilled, and the previous maxima have been read) and after
+// the block maxima (codes may be formed).  Codes of batch i are formed at the
+// top of iteration i+1, from the registers that still hold its rotated
+// blocks.  The buffer is refilled after the butterflies: the wait for the
+// next batch's loads then also finds the previous codes' stores complete,
+// instead of stalling on them right after they were issued.
 // at most 8 x 80 lanes (b = 64, K <= 5120)
 template <int B>
 constexpr int rows8_threads() { return 640; }
 
-template <int B, int QB>
+template <int B, int QB, bool GATHER>
 __global__ void __launch_bounds__(rows8_threads<B>())
 rq_rows8_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__restrict__ perm,
                 int64_t rows_valid, int64_t rows_alloc, int64_t nbatch, int K,
@@ -541,9 +555,8 @@ rq_rows8_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__re
         // codes of the previous batch (its maxima are complete), then this
         // batch's blocks into registers
         if (prev >= 0) codes(prev, i - 1);
-        if (t < R) rowmax[((i + 1) & 1) * R + t] = 0u;   // read last at the previous codes
         if (active) {
-            if (perm == nullptr) {
+            if constexpr (!GATHER) {
                 const uint4 *src = tile + r * cpr + j * CPB;
 #pragma unroll
                 for (int ii = 0; ii < CPB; ++ii) {
@@ -551,9 +564,7 @@ rq_rows8_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__re
                     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float u = half_lo(w[e]), s = half_hi(w[e]);
-                        x[8 * ii + 2 * e] = u + s;       // stage h = 1
-                        x[8 * ii + 2 * e + 1] = u - s;
+                        stage1_packed(w[e], x[8 * ii + 2 * e], x[8 * ii + 2 * e + 1]);   // stage h = 1
                     }
                 }
             } else {
@@ -565,16 +576,12 @@ rq_rows8_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__re
                     const int c0 = k0 >> 3, c1 = k1 >> 3;
                     const int s0 = (c0 / CPB) * CPB + ((c0 % CPB) ^ r);
                     const int s1 = (c1 / CPB) * CPB + ((c1 % CPB) ^ r);
-                    const float u = __half2float(__ushort_as_half(rowh[s0 * 8 + (k0 & 7)]));
-                    const float s = __half2float(__ushort_as_half(rowh[s1 * 8 + (k1 & 7)]));
-                    x[e] = u + s;
-                    x[e + 1] = u - s;
+                    stage1_pair(rowh[s0 * 8 + (k0 & 7)], rowh[s1 * 8 + (k1 & 7)], x[e], x[e + 1]);
                 }
             }
         }
-        __syncthreads();   // every block read: the buffer may be refilled
-        if (b + G < nbatch) stash();
-        if (b + 2 * G < nbatch) load(b + 2 * G);
+        __syncthreads();   // every block read and every read of the previous maxima done
+        if (t < R) rowmax[((i + 1) & 1) * R + t] = 0u;   // batch i+1's buffer, read last by codes(i-1)
         if (active) {
 #pragma unroll
             for (int h = 2; h < B; h <<= 1) {
@@ -587,11 +594,10 @@ rq_rows8_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__re
                     }
                 }
             }
-            float bmax = 0.0f;
-#pragma unroll
-            for (int ii = 0; ii < B; ii += 2) bmax = fmaxf(bmax, fmaxf(fabsf(x[ii]), fabsf(x[ii + 1])));
-            atomicMax(&rowmax[(i & 1) * R + r], __float_as_uint(bmax));
+            atomicMax(&rowmax[(i & 1) * R + r], __float_as_uint(block_absmax<B>(x)));
         }
+        if (b + G < nbatch) stash();
+        if (b + 2 * G < nbatch) load(b + 2 * G);
         __syncthreads();   // maxima complete, next batch staged
         prev = b;
     }
@@ -661,16 +667,16 @@ int pick_act_rows(int K, int block) {
     return best;
 }
 
-template <int B, int QB>
-hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, int64_t rows_valid,
-                         int64_t rows_alloc, int K, uint8_t *out, float *scale, hipStream_t stream) {
+template <int B, int QB, bool GATHER>
+hipError_t launch_rq_act_g(const uint16_t *X, int64_t ldx, const int32_t *perm, int64_t rows_valid,
+                           int64_t rows_alloc, int K, uint8_t *out, float *scale, hipStream_t stream) {
     const int R = pick_act_rows(K, B);
     const int nb = K / B;
     const int T = (R * nb + 63) / 64 * 64;
     const size_t lds = (size_t)2 * R * K * 2 + (size_t)3 * R * 4;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)rq_act_kernel<B, QB>,
+        hipError_t e = hipFuncSetAttribute((const void *)rq_act_kernel<B, QB, GATHER>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 65536 + 4096);
         if (e != hipSuccess) return e;
         attr_set = true;
@@ -687,7 +693,7 @@ hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, in
     if constexpr (B == 64) if (use_rows8<B>(K) && (int64_t)8 * ldx <= INT32_MAX) {
         static bool attr8 = false;
         if (!attr8) {
-            hipError_t e = hipFuncSetAttribute((const void *)rq_rows8_kernel<B, QB>,
+            hipError_t e = hipFuncSetAttribute((const void *)rq_rows8_kernel<B, QB, GATHER>,
                                                hipFuncAttributeMaxDynamicSharedMemorySize, 80 * 1024 + 64);
             if (e != hipSuccess) return e;
             attr8 = true;
@@ -696,16 +702,23 @@ hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, in
         const size_t lds8 = (size_t)8 * K * 2 + 2 * 8 * 4;
         const int64_t nb8 = (rows_alloc + 7) / 8;
         const int64_t grid8 = std::min<int64_t>(nb8, (int64_t)cus);
-        hipLaunchKernelGGL((rq_rows8_kernel<B, QB>), dim3((unsigned)grid8), dim3(T8), lds8, stream, X, ldx, perm,
+        hipLaunchKernelGGL((rq_rows8_kernel<B, QB, GATHER>), dim3((unsigned)grid8), dim3(T8), lds8, stream, X, ldx, perm,
                            rows_valid, rows_alloc, nb8, K, out, scale);
         return hipGetLastError();
     }
     const int64_t nbatch = (rows_alloc + R - 1) / R;
     const int per_cu = (int)std::min<size_t>(4, (160 * 1024) / lds);
     const int64_t grid = std::min<int64_t>(nbatch, (int64_t)cus * per_cu);
-    hipLaunchKernelGGL((rq_act_kernel<B, QB>), dim3((unsigned)grid), dim3(T), lds, stream, X, ldx, perm,
+    hipLaunchKernelGGL((rq_act_kernel<B, QB, GATHER>), dim3((unsigned)grid), dim3(T), lds, stream, X, ldx, perm,
                        rows_valid, rows_alloc, nbatch, K, R, out, scale);
     return hipGetLastError();
+}
+
+template <int B, int QB>
+hipError_t launch_rq_act(const uint16_t *X, int64_t ldx, const int32_t *perm, int64_t rows_valid,
+                         int64_t rows_alloc, int K, uint8_t *out, float *scale, hipStream_t stream) {
+    if (perm != nullptr) return launch_rq_act_g<B, QB, true>(X, ldx, perm, rows_valid, rows_alloc, K, out, scale, stream);
+    return launch_rq_act_g<B, QB, false>(X, ldx, perm, rows_valid, rows_alloc, K, out, scale, stream);
 }
 
 __global__ void unswizzle_kernel(const uint8_t *__restrict__ Wq, int64_t N, int K,
