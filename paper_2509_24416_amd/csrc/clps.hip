@@ -10,8 +10,8 @@
 //   clps_row_ratio_kernel  per weight row: gather, block FWHT in LDS (the
 //                          same fp32 butterflies as the quantizer), then the
 //                          order statistic of |.| with floor(gamma (K-1))
-//                          values above it (walked down from the max) over
-//                          the max.
+//                          values above it (a radix select on the
+//                          magnitudes' bit patterns) over the max.
 //   clps_grid_kernel       alpha_lo = min of the row ratios; the G candidates
 //                          alpha_i = 1 - ((1 - alpha_lo)(G-1-i)) / (G-1).
 //   per candidate          the hot path's weight quantizer with alpha_i read
@@ -33,6 +33,7 @@
 #include <algorithm>
 
 #include "clq_internal.h"
+#include "radix_select.h"
 
 namespace clq {
 namespace {
@@ -62,41 +63,25 @@ clps_row_ratio_kernel(const uint16_t *__restrict__ W, const int32_t *__restrict_
         }
         __syncthreads();
     }
-    // the order statistic with l = K-1-order_idx values above it, by walking
-    // down the distinct magnitudes: m = the largest magnitude below the last
-    // one, c = how many are >= m; the first m with c > l is the answer (exact
-    // with repeated values; at most l + 1 steps).  The first m is the max.
+    // |w~| as integer keys (non-negative floats order as their bit patterns)
+    // and its maximum; then the order statistic by radix selection (exact
+    // with repeated values)
     __shared__ float redf[kRatioThreads / 64];
-    __shared__ int redi[kRatioThreads / 64];
-    const int l = K - 1 - order_idx;
+    __shared__ uint32_t hist[256], wsum[4], pick[2];
+    uint32_t *keys = reinterpret_cast<uint32_t *>(w);
     const int lane = t & 63, wv = t >> 6;
-    float top = __builtin_inff(), mx = 0.0f, q = 0.0f;
-    for (int it = 0;; ++it) {
-        float m = -1.0f;
-        for (int i = t; i < K; i += kRatioThreads) {
-            const float v = fabsf(w[i]);
-            if (v < top) m = fmaxf(m, v);
-        }
-        for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-        if (lane == 0) redf[wv] = m;
-        __syncthreads();
-        m = redf[0];
-        for (int k = 1; k < kRatioThreads / 64; ++k) m = fmaxf(m, redf[k]);
-        int c = 0;
-        for (int i = t; i < K; i += kRatioThreads) c += fabsf(w[i]) >= m;
-        for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
-        if (lane == 0) redi[wv] = c;
-        __syncthreads();
-        c = 0;
-        for (int k = 0; k < kRatioThreads / 64; ++k) c += redi[k];
-        __syncthreads();   // redf / redi are rewritten in the next step
-        if (it == 0) mx = m;
-        if (c > l) {
-            q = m;
-            break;
-        }
-        top = m;
+    float m = 0.0f;
+    for (int i = t; i < K; i += kRatioThreads) {
+        const float v = fabsf(w[i]);
+        keys[i] = __float_as_uint(v);
+        m = fmaxf(m, v);
     }
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    if (lane == 0) redf[wv] = m;
+    __syncthreads();
+    float mx = redf[0];
+    for (int k = 1; k < kRatioThreads / 64; ++k) mx = fmaxf(mx, redf[k]);
+    const float q = __uint_as_float(radix_select<kRatioThreads>(keys, K, order_idx, hist, wsum, pick));
     if (t == 0) ratio[row] = mx == 0.0f ? 1.0f : q / mx;
 }
 

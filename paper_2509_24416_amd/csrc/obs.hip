@@ -36,6 +36,7 @@
 #include <algorithm>
 
 #include "clq_internal.h"
+#include "radix_select.h"
 
 namespace clq {
 namespace {
@@ -171,52 +172,6 @@ __global__ void obs_finish_kernel(uint32_t *__restrict__ acc, int D, int metric,
 constexpr int kColThreads = 1024;
 constexpr int kMaxTopk = 512;   // k <= (32768 + 50) / 100 = 328
 
-// The rank-th smallest (0-based) of the n keys in LDS, by four passes over
-// 8-bit digits from the top: a histogram of the keys that match the digits
-// chosen so far, then a scan of the 256 bins for the one holding the rank.
-// Called by every thread of the workgroup; returns the key.
-__device__ uint32_t radix_select(const uint32_t *keys, int n, int rank, uint32_t *hist, uint32_t *wsum,
-                                 uint32_t *pick)
-{
-    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-    uint32_t prefix = 0u, mask = 0u;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int i = t; i < 256; i += kColThreads) hist[i] = 0u;
-        __syncthreads();
-        for (int i = t; i < n; i += kColThreads) {
-            const uint32_t k = keys[i];
-            if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
-        }
-        __syncthreads();
-        // inclusive scan of the 256 counts (threads 0-255: four waves)
-        uint32_t c = 0u, inc = 0u;
-        if (t < 256) {
-            c = hist[t];
-            inc = c;
-            for (int off = 1; off < 64; off <<= 1) {
-                const uint32_t o = __shfl_up(inc, off);
-                if (lane >= off) inc += o;
-            }
-            if (lane == 63) wsum[wv] = inc;
-        }
-        __syncthreads();
-        if (t < 256) {
-            for (int w = 0; w < wv; ++w) inc += wsum[w];
-            const uint32_t exc = inc - c;
-            if (exc <= (uint32_t)rank && (uint32_t)rank < inc) {   // exactly one bin
-                pick[0] = (uint32_t)t;
-                pick[1] = exc;
-            }
-        }
-        __syncthreads();
-        prefix |= pick[0] << shift;
-        mask |= 255u << shift;
-        rank -= (int)pick[1];
-        __syncthreads();   // pick and hist are rewritten by the next pass
-    }
-    return prefix;
-}
-
 // METRIC 2: peak-to-average ratio, 3: top-k mean, 4: percentile spread
 template <int METRIC>
 __global__ void __launch_bounds__(kColThreads)
@@ -267,7 +222,7 @@ obs_column_kernel(const float *__restrict__ S, int64_t N, int D, int P, float *_
         while (kp < kk) kp <<= 1;
         // the kk-th largest; the values above it, then copies of it: the kk
         // largest as a multiset
-        const uint32_t thr = radix_select(keys, n, n - kk, hist, wsum, pick);
+        const uint32_t thr = radix_select<kColThreads>(keys, n, n - kk, hist, wsum, pick);
         for (int i = t; i < n; i += kColThreads) {
             const uint32_t k = keys[i];
             if (k > thr) top[atomicAdd(&cnt, 1u)] = __uint_as_float(k);
@@ -301,8 +256,8 @@ obs_column_kernel(const float *__restrict__ S, int64_t N, int D, int P, float *_
         if (t == 0) scores[d] = top[0] / (float)kk;
     } else {
         const int lo = (n - 1) / 100, hi = n - 1 - lo;
-        const uint32_t khi = radix_select(keys, n, hi, hist, wsum, pick);
-        const uint32_t klo = radix_select(keys, n, lo, hist, wsum, pick);
+        const uint32_t khi = radix_select<kColThreads>(keys, n, hi, hist, wsum, pick);
+        const uint32_t klo = radix_select<kColThreads>(keys, n, lo, hist, wsum, pick);
         if (t == 0) scores[d] = ord_dec(khi) - ord_dec(klo);
     }
 }

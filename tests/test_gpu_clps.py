@@ -84,6 +84,11 @@ def test_degenerate_windows(clq):
     Wz = W.copy()
     Wz[3] = 0
     check(clq, X, Wz, 64, G=6)
+    # weights on a coarse lattice: the rotated rows repeat their magnitudes
+    # many times, so the order statistic falls inside runs of equal values
+    Wl = (np.round(W.astype(np.float32) * 64.0) / 64.0).astype(np.float16)
+    check(clq, X, Wl, 64, gamma=0.05, G=6)
+    check(clq, X, Wl, 32, gamma=0.2, G=6)
 
 
 def test_calibration_sized_layer(clq):
