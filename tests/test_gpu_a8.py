@@ -89,8 +89,10 @@ def test_quantize_weights8_bitexact(clq, N, K, block, clip):
     assert qw.wq.numel() == clq.clq_weight8_bytes(N, K)
 
 
+# the last shape: several token-tile groups of 8 per XCD run, ragged token
+# rows and channels
 SHAPES = [(1, 1, 64), (7, 9, 128), (100, 200, 1152), (257, 129, 1152), (130, 520, 640),
-          (300, 1000, 4608), (512, 256, 64), (1000, 384, 3072)]
+          (300, 1000, 4608), (512, 256, 64), (1000, 384, 3072), (4100, 1030, 640)]
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
