@@ -708,39 +708,44 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// each half of the eight-wave workgroup: the tile geometry of TCfg
+// each half of the eight-wave workgroup: the tile geometry of TCfg (128
+// channels x 256 tokens); with few tiles, a half of two waves on 128 tokens
+// (a four-wave workgroup), so that twice as many compute units take part
 using TileHalf = Tile<1, 4, 4, 2, 2>;
+using TileHalf128 = Tile<1, 2, 4, 2, 2>;
 
 // ---- few tiles: two waves per SIMD on one tile ---------------------------------
 // With at most one tile per compute unit, a lone workgroup's k loop is bound
 // by the instruction stream of its one wave per SIMD (matrix-core work and
 // the ~180 other instructions of a stage run mostly in series).  This kernel
-// gives each tile a workgroup of eight waves: waves 0-3 run the first half of
-// the k-stages and waves 4-7 the second half, each half through its own LDS
-// ring, in lockstep on the workgroup barrier, so two waves share each SIMD.
-// The halves' integer sums meet in LDS (exact), and waves 0-3 run the
-// epilogue with the same arithmetic as the persistent kernel.
+// gives each tile two halves of C::NW waves: the first half runs the first
+// half of the k-stages and the second half the rest, each half through its
+// own LDS ring, in lockstep on the workgroup barrier (eight waves for the
+// 256-token tile, so two share each SIMD).  The halves swap integer sums in
+// LDS (exact) and each runs the epilogue of two channel fragments with the
+// same arithmetic as the persistent kernel.
 constexpr int kHalfStages = 4;   // ring depth per half
 
-template <bool I32OUT, bool RAGGED, bool BIAS>
-__global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
+template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+__global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs a)
 {
     static_assert(!(I32OUT && BIAS), "no bias on the integer output");
-    using C = TileHalf;
+    static_assert(C::WN == 1 && C::FN == 4 && C::FM == 2, "one channel panel, 4 x 2 fragments per wave");
     constexpr int NS = kHalfStages;
     constexpr int SLOT = C::STAGE_BYTES;
-    // the two rings (96 KB), reused at the end for the exchange of the
-    // halves' sums (2 x 64 KB)
-    constexpr int kExch = 65536;
+    // the two rings (96 or 64 KB), reused at the end for the exchange of the
+    // halves' sums (16 KB per wave each way)
+    constexpr int kExch = C::NW * 16384;
     __shared__ __align__(16) uint8_t pool[2 * NS * SLOT > 2 * kExch ? 2 * NS * SLOT : 2 * kExch];
     auto ring = reinterpret_cast<uint8_t (*)[NS][SLOT]>(pool);
-    // the tile's epilogue operands, staged at the start: channel scales,
-    // biases (fp16), token scales
-    __shared__ float ep_ws[C::BN], ep_xs[C::BM];
-    __shared__ _Float16 ep_b[C::BN];
+    // the tile's epilogue operands, staged at the start as floats: channel
+    // scales, biases (fp16 widened, exact), token scales
+    constexpr int EPN = 2 * C::BN + C::BM;
+    __shared__ float ep[EPN];
+    const float *ep_ws = ep, *ep_b = ep + C::BN, *ep_xs = ep + 2 * C::BN;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w8 = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int half = w8 >> 2, wm = w8 & 3;   // one channel panel per tile: wn = 0
+    const int half = w8 / C::NW, wm = w8 % C::NW;   // one channel panel per tile: wn = 0
     const int M = a.M, N = a.N, nks = a.K >> 6;
     const int L = blockIdx.x;
     int tm, tn;
@@ -828,19 +833,24 @@ __global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
         asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"((NS - 3) * C::UPW) : "memory");
     };
 
-    // epilogue operands first (one value per thread, clamped indices), then
-    // the first stages; the LDS writes land before the first barrier
-    static_assert(2 * C::BN + C::BM == 512, "one operand per thread below");
-    // (branch-free loads, so that the waits for them stay exact)
-    const int ec = tid & (C::BN - 1), er = max(tid - 2 * C::BN, 0);
-    const float *esrc = tid < 2 * C::BN ? a.ws + min(tn * C::BN + ec, N - 1) : a.xs + min(tm * C::BM + er, M - 1);
-    const float epv = *esrc;
-    _Float16 epb = (_Float16)0.0f;
-    if constexpr (BIAS) epb = reinterpret_cast<const _Float16 *>(a.bias)[min(tn * C::BN + ec, N - 1)];
+    // epilogue operands: loaded first (EPR per thread at clamped indices,
+    // branch-free, ahead of the transfers), held in registers through the k
+    // loop and written to LDS after it, when no transfer into LDS is in
+    // flight (an LDS store during the transfers would wait for all of them)
+    constexpr int EPR = (EPN + 2 * C::NT - 1) / (2 * C::NT);
+    float epv[EPR];
+    _Float16 epb[EPR];
+#pragma unroll
+    for (int r = 0; r < EPR; ++r) {
+        const int e = min(tid + r * 2 * C::NT, EPN - 1);
+        const int ec = e & (C::BN - 1), er = max(e - 2 * C::BN, 0);
+        const float *esrc = e < 2 * C::BN ? a.ws + min(tn * C::BN + ec, N - 1) : a.xs + min(tm * C::BM + er, M - 1);
+        epv[r] = *esrc;
+        epb[r] = (_Float16)0.0f;
+        if constexpr (BIAS) epb[r] = reinterpret_cast<const _Float16 *>(a.bias)[min(tn * C::BN + ec, N - 1)];
+    }
+    __builtin_amdgcn_sched_barrier(0);
     for (int q = 0; q < NS - 1; ++q) produce(q, q);
-    if (tid < C::BN) ep_ws[ec] = epv;
-    else if (tid < 2 * C::BN) ep_b[ec] = epb;
-    else ep_xs[er] = epv;
     landed_wait();
     read_packed(0);
     operands_ready();
@@ -869,9 +879,17 @@ __global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
     }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
+    // the epilogue operands into LDS (a thread past the end writes the last
+    // value again); the barrier after the sends below publishes them
+#pragma unroll
+    for (int r = 0; r < EPR; ++r) {
+        const int e = min(tid + r * 2 * C::NT, EPN - 1);
+        ep[e] = e >= C::BN && e < 2 * C::BN ? (float)epb[r] : epv[r];
+    }
+
     // the halves swap sums through the idle rings: half 0 finishes channel
     // fragments 0-1 and half 1 fragments 2-3, each adding the other's
-    // partial (64 KB each way, 16-byte pieces with lanes consecutive)
+    // partial (16 KB per wave each way, 16-byte pieces with lanes consecutive)
     auto send = [&](auto f0c) {
         constexpr int f0 = decltype(f0c)::value;
         v4i *out = reinterpret_cast<v4i *>(pool + half * kExch);
@@ -917,16 +935,11 @@ __global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
     static_for<0, 2>([&](auto fc) {
         constexpr int fn = decltype(f0c)::value + decltype(fc)::value;
         const int c0 = fn * 32 + h16, n0 = tn * C::BN + c0;
-        float wsv[16];
-        h2v bw[8];
+        float wsv[16], bw[16];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) wsv[v] = ep_ws[c0 + v];
-        if constexpr (BIAS) {
-#pragma unroll
-            for (int v = 0; v < 16; v += 2) bw[v / 2] = h2v{ep_b[c0 + v], ep_b[c0 + v + 1]};
-        } else {
-#pragma unroll
-            for (int v = 0; v < 8; ++v) bw[v] = h2v{(_Float16)0.0f, (_Float16)0.0f};
+        for (int v = 0; v < 16; ++v) {
+            wsv[v] = ep_ws[c0 + v];
+            bw[v] = BIAS ? ep_b[c0 + v] : 0.0f;
         }
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm) {
@@ -954,8 +967,8 @@ __global__ void __launch_bounds__(512, 2) w4a4_gemm_halves_kernel(GemmArgs a)
             for (int v = 0; v < 16; v += 2) {
                 const float p0 = (float)x[v] * xsc, p1 = (float)x[v + 1] * xsc;
                 h2v hh;
-                hh[0] = (_Float16)__builtin_fmaf(p0, wsv[v], (float)bw[v / 2][0]);
-                hh[1] = (_Float16)__builtin_fmaf(p1, wsv[v + 1], (float)bw[v / 2][1]);
+                hh[0] = (_Float16)__builtin_fmaf(p0, wsv[v], bw[v]);
+                hh[1] = (_Float16)__builtin_fmaf(p1, wsv[v + 1], bw[v + 1]);
                 hv[v / 2] = __builtin_bit_cast(uint32_t, hh);
             }
             uint16_t *dst = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)m * a.ldy + n0;
@@ -1004,6 +1017,24 @@ int full_grid() { return (device_cus() * TCfg::WGS + 7) / 8 * 8; }
 constexpr int kSplitMinSaved = 16;
 constexpr int kSplitMinShare = 8;
 constexpr int kHalvesMinStages = 4;   // k-stages for the eight-wave kernel
+
+template <class C>
+hipError_t launch_halves(const GemmArgs &g, bool i32out, bool bias, bool rag, hipStream_t stream) {
+    const dim3 grid((unsigned)(g.tiles_m * g.tiles_n)), block(2 * C::NT);
+    if (i32out && rag)
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, true, true, false>), grid, block, 0, stream, g);
+    else if (i32out)
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, true, false, false>), grid, block, 0, stream, g);
+    else if (bias && rag)
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, false, true, true>), grid, block, 0, stream, g);
+    else if (bias)
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, false, false, true>), grid, block, 0, stream, g);
+    else if (rag)
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, false, true, false>), grid, block, 0, stream, g);
+    else
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, false, false, false>), grid, block, 0, stream, g);
+    return hipGetLastError();
+}
 
 template <class C, bool I32OUT, bool RAGGED, bool BIAS, bool ERR = false>
 hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
@@ -1060,21 +1091,13 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
     // waves per tile
     const int ntiles = g.tiles_m * g.tiles_n;
     if (ntiles <= device_cus() && (K >> 6) >= kHalvesMinStages) {
-        const bool rag = N % 16 != 0;
-        const dim3 grid((unsigned)ntiles), block(512);
-        if (i32out && rag)
-            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<true, true, false>), grid, block, 0, stream, g);
-        else if (i32out)
-            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<true, false, false>), grid, block, 0, stream, g);
-        else if (bias && rag)
-            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, true, true>), grid, block, 0, stream, g);
-        else if (bias)
-            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, false, true>), grid, block, 0, stream, g);
-        else if (rag)
-            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, true, false>), grid, block, 0, stream, g);
-        else
-            hipLaunchKernelGGL((w4a4_gemm_halves_kernel<false, false, false>), grid, block, 0, stream, g);
-        return hipGetLastError();
+        // 128-token tiles while the 256-token ones would fill at most half
+        // the compute units
+        if (2 * ntiles <= device_cus()) {
+            g.tiles_m = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
+            return launch_halves<TileHalf128>(g, i32out, bias != nullptr, N % 16 != 0, stream);
+        }
+        return launch_halves<TileHalf>(g, i32out, bias != nullptr, N % 16 != 0, stream);
     }
     // ragged channel edges, and biases not 4-byte aligned (the fast path
     // moves them in channel pairs), use element-wise epilogue accesses
