@@ -710,9 +710,11 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
 
 // each half of the eight-wave workgroup: the tile geometry of TCfg (128
 // channels x 256 tokens); with few tiles, a half of two waves on 128 tokens
-// (a four-wave workgroup), so that twice as many compute units take part
+// (a four-wave workgroup) or of one wave on 64 tokens, so that more compute
+// units take part
 using TileHalf = Tile<1, 4, 4, 2, 2>;
 using TileHalf128 = Tile<1, 2, 4, 2, 2>;
+using TileHalf64 = Tile<1, 1, 4, 2, 2>;
 
 // ---- few tiles: two waves per SIMD on one tile ---------------------------------
 // With at most one tile per compute unit, a lone workgroup's k loop is bound
@@ -1091,10 +1093,15 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
     // waves per tile
     const int ntiles = g.tiles_m * g.tiles_n;
     if (ntiles <= device_cus() && (K >> 6) >= kHalvesMinStages) {
-        // 128-token tiles while the 256-token ones would fill at most half
-        // the compute units
+        // smaller tiles while the larger ones would fill at most half the
+        // compute units: 128 tokens, then 64
         if (2 * ntiles <= device_cus()) {
-            g.tiles_m = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
+            const int tm128 = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
+            if (2 * tm128 * g.tiles_n <= device_cus()) {
+                g.tiles_m = (int)((M + TileHalf64::BM - 1) / TileHalf64::BM);
+                return launch_halves<TileHalf64>(g, i32out, bias != nullptr, N % 16 != 0, stream);
+            }
+            g.tiles_m = tm128;
             return launch_halves<TileHalf128>(g, i32out, bias != nullptr, N % 16 != 0, stream);
         }
         return launch_halves<TileHalf>(g, i32out, bias != nullptr, N % 16 != 0, stream);
