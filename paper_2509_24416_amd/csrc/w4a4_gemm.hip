@@ -47,9 +47,10 @@
 // order); the workgroup that computes a split tile's first stages owns it
 // and adds the others' partial accumulators before its epilogue.
 //
-// With at most one tile per compute unit a second kernel runs instead
-// (w4a4_gemm_halves_kernel, below): eight waves per tile, the two halves of
-// the k loop on two waves per SIMD, summed in LDS.
+// With at most one such tile per compute unit a second kernel runs instead
+// (w4a4_gemm_halves_kernel, below): tiles of 128 or 64 tokens, each split
+// into two halves of the k loop run by two groups of waves and summed in LDS,
+// two workgroups per compute unit.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -708,24 +709,23 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// each half of the eight-wave workgroup: the tile geometry of TCfg (128
-// channels x 256 tokens); with few tiles, a half of two waves on 128 tokens
-// (a four-wave workgroup) or of one wave on 64 tokens, so that more compute
-// units take part
-using TileHalf = Tile<1, 4, 4, 2, 2>;
+// the tiles of the two-halves kernel: 128 channels x 128 tokens, a half of
+// two waves (a four-wave workgroup, two per compute unit), or x 64 tokens,
+// a half of one wave, when the 128-token tiles would fill at most half the
+// compute units
 using TileHalf128 = Tile<1, 2, 4, 2, 2>;
 using TileHalf64 = Tile<1, 1, 4, 2, 2>;
 
-// ---- few tiles: two waves per SIMD on one tile ---------------------------------
-// With at most one tile per compute unit, a lone workgroup's k loop is bound
-// by the instruction stream of its one wave per SIMD (matrix-core work and
-// the ~180 other instructions of a stage run mostly in series).  This kernel
-// gives each tile two halves of C::NW waves: the first half runs the first
-// half of the k-stages and the second half the rest, each half through its
-// own LDS ring, in lockstep on the workgroup barrier (eight waves for the
-// 256-token tile, so two share each SIMD).  The halves swap integer sums in
-// LDS (exact) and each runs the epilogue of two channel fragments with the
-// same arithmetic as the persistent kernel.
+// ---- few tiles: the k loop in two halves ---------------------------------------
+// With at most one 256-token tile per compute unit, a lone workgroup's k loop
+// is bound by the instruction stream of its one wave per SIMD (matrix-core
+// work and the ~180 other instructions of a stage run mostly in series).
+// This kernel gives each smaller tile two halves of C::NW waves: the first
+// half runs the first half of the k-stages and the second half the rest, each
+// half through its own LDS ring, in lockstep on the workgroup barrier, with
+// two workgroups per compute unit.  The halves swap integer sums in LDS
+// (exact) and each runs the epilogue of two channel fragments with the same
+// arithmetic as the persistent kernel.
 constexpr int kHalfStages = 4;   // ring depth per half
 
 template <class C, bool I32OUT, bool RAGGED, bool BIAS>
@@ -1018,7 +1018,7 @@ int full_grid() { return (device_cus() * TCfg::WGS + 7) / 8 * 8; }
 // summed from at most nks / kSplitMinShare + 1 pieces).
 constexpr int kSplitMinSaved = 16;
 constexpr int kSplitMinShare = 8;
-constexpr int kHalvesMinStages = 4;   // k-stages for the eight-wave kernel
+constexpr int kHalvesMinStages = 4;   // k-stages for the two-halves kernel
 
 template <class C>
 hipError_t launch_halves(const GemmArgs &g, bool i32out, bool bias, bool rag, hipStream_t stream) {
@@ -1089,22 +1089,19 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
     g.part = workspace ? reinterpret_cast<int32_t *>(reinterpret_cast<uint8_t *>(workspace) + G * TCfg::NW * sizeof(int))
                        : nullptr;
     const bool may_split = workspace != nullptr;
-    // at most one tile per compute unit and a k loop worth halving: eight
-    // waves per tile
+    // at most one 256-token tile per compute unit and a k loop worth
+    // halving: the two-halves kernel
     const int ntiles = g.tiles_m * g.tiles_n;
     if (ntiles <= device_cus() && (K >> 6) >= kHalvesMinStages) {
-        // smaller tiles while the larger ones would fill at most half the
-        // compute units: 128 tokens, then 64
-        if (2 * ntiles <= device_cus()) {
-            const int tm128 = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
-            if (2 * tm128 * g.tiles_n <= device_cus()) {
-                g.tiles_m = (int)((M + TileHalf64::BM - 1) / TileHalf64::BM);
-                return launch_halves<TileHalf64>(g, i32out, bias != nullptr, N % 16 != 0, stream);
-            }
-            g.tiles_m = tm128;
-            return launch_halves<TileHalf128>(g, i32out, bias != nullptr, N % 16 != 0, stream);
+        // 128-token tiles (two four-wave workgroups per compute unit), or 64
+        // while those would fill at most half the compute units
+        const int tm128 = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
+        if (2 * tm128 * g.tiles_n <= device_cus()) {
+            g.tiles_m = (int)((M + TileHalf64::BM - 1) / TileHalf64::BM);
+            return launch_halves<TileHalf64>(g, i32out, bias != nullptr, N % 16 != 0, stream);
         }
-        return launch_halves<TileHalf>(g, i32out, bias != nullptr, N % 16 != 0, stream);
+        g.tiles_m = tm128;
+        return launch_halves<TileHalf128>(g, i32out, bias != nullptr, N % 16 != 0, stream);
     }
     // ragged channel edges, and biases not 4-byte aligned (the fast path
     // moves them in channel pairs), use element-wise epilogue accesses
