@@ -47,7 +47,7 @@
 // order); the workgroup that computes a split tile's first stages owns it
 // and adds the others' partial accumulators before its epilogue.
 //
-// With at most one such tile per compute unit a second kernel runs instead
+// With at most 1.25 such tiles per compute unit a second kernel runs instead
 // (w4a4_gemm_halves_kernel, below): tiles of 128 or 64 tokens, each split
 // into two halves of the k loop run by two groups of waves and summed in LDS,
 // two workgroups per compute unit.
@@ -717,7 +717,7 @@ using TileHalf128 = Tile<1, 2, 4, 2, 2>;
 using TileHalf64 = Tile<1, 1, 4, 2, 2>;
 
 // ---- few tiles: the k loop in two halves ---------------------------------------
-// With at most one 256-token tile per compute unit, a lone workgroup's k loop
+// With about one 256-token tile per compute unit, a lone workgroup's k loop
 // is bound by the instruction stream of its one wave per SIMD (matrix-core
 // work and the ~180 other instructions of a stage run mostly in series).
 // This kernel gives each smaller tile two halves of C::NW waves: the first
@@ -1089,10 +1089,13 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
     g.part = workspace ? reinterpret_cast<int32_t *>(reinterpret_cast<uint8_t *>(workspace) + G * TCfg::NW * sizeof(int))
                        : nullptr;
     const bool may_split = workspace != nullptr;
-    // at most one 256-token tile per compute unit and a k loop worth
-    // halving: the two-halves kernel
+    // at most 1.25 256-token tiles per compute unit and a k loop worth
+    // halving: the two-halves kernel.  Just past one tile per CU the
+    // persistent kernel doubles up on a few CUs while the rest idle; the
+    // two-halves kernel fills one round of two workgroups per CU and runs a
+    // short second round on the remaining quarter at most.
     const int ntiles = g.tiles_m * g.tiles_n;
-    if (ntiles <= device_cus() && (K >> 6) >= kHalvesMinStages) {
+    if (4 * ntiles <= 5 * device_cus() && (K >> 6) >= kHalvesMinStages) {
         // 128-token tiles (two four-wave workgroups per compute unit), or 64
         // while those would fill at most half the compute units
         const int tm128 = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);

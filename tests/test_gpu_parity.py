@@ -148,11 +148,12 @@ def test_quantize_weights_perm(clq):
 # loop split in two, the halves' sums added in LDS), including odd stage
 # counts (one half a stage shorter) and ragged channels.  Its tiles have 128
 # tokens, or 64 while the 128-token tiles would fill at most half the compute
-# units: 64 for the small shapes, 128 for the last three (the last two at one
-# to two tiles per compute unit)
+# units: 64 for the small shapes, 128 for the last four (the last three at
+# one to 2.5 tiles per compute unit, 8193 x 1030 in two rounds)
 GEMM_SHAPES = [(1, 1, 64), (7, 8, 128), (129, 72, 192), (257, 200, 1152), (64, 1152, 1152),
                (300, 130, 640), (128, 128, 128), (513, 264, 4608), (257, 200, 576), (100, 1001, 320),
-               (33, 48, 256), (5, 3, 256), (2049, 1030, 640), (4097, 1030, 640), (4000, 2000, 576)]
+               (33, 48, 256), (5, 3, 256), (2049, 1030, 640), (4097, 1030, 640), (4000, 2000, 576),
+               (8193, 1030, 576)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
