@@ -504,7 +504,7 @@ def main():
                    "block": 64, "layers": {l.name.split(".")[1]: [l.K, l.N] for l in layers},
                    "parallelism": "none (one GPU)"},
         "pct_int8_peak": round(100 * value / INT8_PEAK_TOPS, 2),
-        "roofline": {"kernel": ("w4a4_gemm_kernel (128 ch x 256 tok tiles, 2 per CU)" if abits == 4 else
+        "roofline": {"kernel": ("W4A4 GEMM: w4a4_gemm_kernel (qkv, fc1) and w4a4_gemm_halves_kernel (proj, fc2), mean over the 4 linears" if abits == 4 else
                                 f"a8_gemm_kernel<{wbits}> (128 ch x 128 tok tiles)"),
                      "bound": "mfma", "achieved": round(achieved, 1),
                      "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
