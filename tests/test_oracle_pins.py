@@ -346,3 +346,96 @@ def test_extreme_fp16_rows():
     assert s[2] == 0 and np.all(q[2] == 0)
     assert s[3] > 0 and np.abs(q[3]).max() == 7
     assert np.isfinite(s).all()
+
+
+# ---- Eq. (1) Round(.): one rounding of the exact product ---------------------
+# Round(.) maps the scaled value to its nearest integer.  The scaled value is
+# the exact product x~ * r with r = fl32(qmax / a) the per-row reciprocal.
+# The cases below were chosen so that rounding that product to fp32 first
+# lands exactly on k + 1/2 while the exact product lies just off the tie: an
+# oracle that rounded twice (to fp32, then to an integer) gets the other
+# integer.  Expected codes come from exact rational arithmetic here, not from
+# the oracle's formula.
+from fractions import Fraction  # noqa: E402
+
+ROUNDING_CASES = [
+    # (qmax, abs-max a, element x) as fp32 hex; the exact product's nearest integer
+    (7.0, "0x1.448a1cp+0", "0x1.fdfd98p-1", 5),
+    (7.0, "0x1.ec480ap+0", "0x1.a5f49ap-2", 1),
+    (7.0, "0x1.228eaep+0", "0x1.9f14fap-2", 3),
+    (127.0, "0x1.4ea5a4p+0", "0x1.f749bep-1", 95),
+    (127.0, "0x1.a023dap+0", "0x1.b713aep-2", 33),
+    (127.0, "0x1.d4a706p-1", "0x1.555762p-1", 93),
+]
+
+
+def _f32_correctly_rounded_quotient(num, den):
+    """fl32(num / den) from the exact rational quotient, rounding half to
+    even, without using a floating-point division."""
+    q = Fraction(float(num)) / Fraction(float(den))
+    lo = np.float32(float(q))            # within one fp32 step of q
+    cands = [np.nextafter(lo, np.float32(-np.inf)), lo, np.nextafter(lo, np.float32(np.inf))]
+    best = min(cands, key=lambda c: (abs(Fraction(float(c)) - q),
+                                     int(np.frombuffer(np.float32(c).tobytes(), np.uint32)[0]) & 1))
+    return np.float32(best)
+
+
+@pytest.mark.parametrize("qm,a_hex,x_hex,expect", ROUNDING_CASES)
+def test_quantizer_single_rounding(qm, a_hex, x_hex, expect):
+    a = np.float32(float.fromhex(a_hex))
+    x = np.float32(float.fromhex(x_hex))
+    r = _f32_correctly_rounded_quotient(qm, a)
+    exact = Fraction(float(x)) * Fraction(float(r))
+    # the case is a discriminating one: fp32 rounding of the product is a tie
+    # that rounds (half to even) to the other integer
+    f32 = np.float32(float(exact))  # exact product (fits a double) rounded once to fp32
+    assert Fraction(float(f32)).denominator == 2
+    assert round(exact) == expect and abs(exact - expect) < Fraction(1, 2)
+    assert int(np.rint(f32)) != expect
+    row = np.array([[a, x, -x, 0.0]], np.float32)
+    bits = 4 if qm == 7.0 else 8
+    q, s, n = oracle.quantize(row, bits=bits)
+    assert q.tolist() == [[int(qm), expect, -expect, 0]]
+    assert n.tolist() == [0]
+    assert Fraction(float(s[0])) == Fraction(float(_f32_correctly_rounded_quotient(a, qm)))
+
+
+# ---- the fp16 error metric of the 2e-3 bound (hand-computed cases) -----------
+
+def test_err_metric_identity_and_empty():
+    y64 = np.array([[1.5, -2.0], [0.25, 8.0]])
+    assert oracle.err_metric(y64.astype(np.float16), y64, y64) == 0.0
+    assert oracle.err_metric(np.zeros((0, 3)), np.zeros((0, 3)), np.zeros((0, 3))) == 0.0
+
+
+def test_err_metric_one_element_off():
+    p64 = np.array([[2.0, -4.0, 0.5]])
+    y = p64.copy()
+    y[0, 1] += 2.0 ** -7          # error d = 2^-7 on |p| = 4
+    assert oracle.err_metric(y, p64, p64) == 2.0 ** -9
+
+
+def test_err_metric_cancelling_bias():
+    # p = 3, bias = -3: y64 = 0; the denominator is |p| + |bias| = 6, not |y64|
+    p64 = np.array([[3.0, 1.0]])
+    bias = np.array([-3.0, 1.0])
+    y64 = p64 + bias[None, :]
+    y = y64.copy()
+    y[0, 0] = 0.5
+    assert oracle.err_metric(y, y64, p64, bias) == 0.5 / 6.0
+    # without the bias term the same deviation is measured against |p| only
+    assert oracle.err_metric(y, y64, p64) == 0.5 / 3.0
+
+
+def test_err_metric_floor():
+    # p = bias = 0: the denominator is the 2^-24 floor
+    z = np.zeros((1, 2))
+    y = np.array([[2.0 ** -30, 0.0]])
+    assert oracle.err_metric(y, z, z, np.zeros(2)) == 2.0 ** -6
+
+
+def test_err_metric_worst_element_wins():
+    p64 = np.array([[10.0, 10.0, 10.0]])
+    y = np.array([[11.0, 10.0, 7.0]])   # relative errors 0.1, 0, 0.3
+    assert oracle.err_metric(y, p64, p64) == pytest.approx(0.3, abs=0, rel=1e-15)
+    assert oracle.err_metric(y, p64, p64) > 0.3 - 1e-15
