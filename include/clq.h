@@ -104,6 +104,13 @@ clq_status clq_quantize_weights(const void *W, const int32_t *perm, int64_t N,
  *            two per byte (the lower-k code of a pair in the low nibble), in
  *            an opaque tiled order that clq_w4a4_linear reads with whole-line
  *            transfers; clq_unswizzle_act gives the row-major form.
+ *            Note: this is deliberately NOT the plain row-major uint8
+ *            [M][K/2] array a caller might expect.  Rows are padded to a
+ *            multiple of 32 and cut into 32-token x 64-code units of 1 KB,
+ *            so that the GEMM moves one whole unit per wave instruction
+ *            straight into LDS; a row-major buffer would need a 32-row
+ *            gather of 32-byte pieces per transfer.  Callers that need the
+ *            row-major codes convert with clq_unswizzle_act.
  *   x_scale  out, fp32 [M]: max|x~| / 7 for the row (0 for an all-zero row).
  * x~ = FWHT_b(gather(X[m], perm)) in fp32 with the stage order h = 1, 2, 4,
  * ..., b/2; q = rne(x~ * fl32(7 / max|x~|)), the product taken exactly. */
@@ -211,7 +218,7 @@ clq_status clq_unswizzle_weights8(const void *Wq8, int64_t N, int64_t K, void *c
                                   hipStream_t stream);
 
 /* ---- OBS calibration (Sec. 3.3 "Orthogonal-Based Smoothing", outlier
- * detection; Sec. 4.3 ablation of the outlier metric) ----------------------
+ * detection; Sec. 4.2 ablation of the outlier metric) ----------------------
  * Produces the gather vector s (perm) that the entry points above take:
  * calibration activations are averaged over the batch, each channel gets an
  * outlier score, and the top-scoring half of the channels moves to the left
@@ -263,7 +270,7 @@ clq_status clq_obs_permutation(const float *scores, int64_t D, int32_t *perm,
                                hipStream_t stream);
 
 /* ---- CLPS single-layer clip search (Sec. 3.4 "Cross-Layer Parameter
- * Searching", Eq. (2); Sec. 4.1: beta = 0, gamma = 0.01, one percentile for
+ * Searching", Eq. (3); Sec. 4.1: beta = 0, gamma = 0.01, one percentile for
  * all channels of a matrix) -------------------------------------------------
  * Grid search of the weight clip ratio alpha (row bound alpha * max|w~|)
  * that minimises ||Y0 - Yhat_alpha||_F^2 on calibration activations, with

@@ -8,7 +8,7 @@ Paper: "CLQ" (arXiv 2509.24416), Sec. 3.4 (Cross-Layer Parameter Searching):
 a grid search over the quantizer bounds of the layer being optimised, between
 quantiles of its weights (beta = 0, gamma = 0.01 in Sec. 4.1, one percentile
 for all channels of a matrix), minimising the squared Frobenius norm of the
-output error, Eq. (2).  The single-layer form here takes the layer's own
+output error, Eq. (3).  The single-layer form here takes the layer's own
 output as the target (the cross-layer target needs a whole model).
 
 Readings (where the paper is silent):

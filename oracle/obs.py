@@ -8,7 +8,7 @@ Paper: "CLQ" (arXiv 2509.24416), Sec. 3.3 (Orthogonal-Based Smoothing):
   * Data preparing: calibration activations X [B, N, D] are averaged over the
     batch, giving a mean matrix of N tokens x D channels.
   * Outlier detection: one outlier score per channel (the paper keeps the
-    absolute maximum; its ablation, Sec. 4.3 "Choice of Outlier Metric",
+    absolute maximum; its ablation, Sec. 4.2 "Choice of Outlier Metric",
     also tries percentile (1%, 99%), top-k mean with k = 1%, range and peak
     average ratio); channels are ranked by score, the top half moves to the
     left half of the columns and the rest to the right.  No full descending

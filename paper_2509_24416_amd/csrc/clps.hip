@@ -1,7 +1,7 @@
 // Single-layer CLPS clip search on the GPU (CLQ, arXiv 2509.24416, Sec. 3.4:
 // a grid search of the quantizer bounds between quantiles of the layer's
 // weights that minimises the squared Frobenius norm of the output error,
-// Eq. (2); Sec. 4.1: beta = 0, gamma = 0.01, one percentile for every
+// Eq. (3); Sec. 4.1: beta = 0, gamma = 0.01, one percentile for every
 // channel of a matrix).  The target is the layer's own unquantised output;
 // the searched quantity is the weight clip ratio alpha of the hot path
 // (row bound alpha * max|w~_row|).

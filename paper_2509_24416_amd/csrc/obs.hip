@@ -1,5 +1,5 @@
 // OBS calibration on the GPU (CLQ, arXiv 2509.24416, Sec. 3.3
-// "Orthogonal-Based Smoothing"; the five outlier metrics of the Sec. 4.3
+// "Orthogonal-Based Smoothing"; the five outlier metrics of the Sec. 4.2
 // ablation): the batch mean of the calibration activations, one outlier
 // score per channel, and the column swap s that moves the top-scoring half
 // of the channels to the left half, each half in its original order.

@@ -1,6 +1,6 @@
 """GPU parity of the single-layer CLPS clip search against the CPU oracle.
 
-Paper: "CLQ" (arXiv 2509.24416), Sec. 3.4, Eq. (2) and Sec. 4.1 (beta = 0,
+Paper: "CLQ" (arXiv 2509.24416), Sec. 3.4, Eq. (3) and Sec. 4.1 (beta = 0,
 gamma = 0.01).  The candidate clip ratios must match bit for bit (integer
 order statistics and fp32 arithmetic in the same order); the fp64 errors
 agree to 1e-12 relative (sums in different orders); the chosen candidate

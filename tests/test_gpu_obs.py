@@ -4,7 +4,7 @@ against the CPU oracle: scores and the gather vector must match bit for bit
 result -- the swap -- is decided identically).
 
 Paper: "CLQ" (arXiv 2509.24416), Sec. 3.3 (Orthogonal-Based Smoothing) and
-the outlier-metric ablation of Sec. 4.3.
+the outlier-metric ablation of Sec. 4.2.
 """
 import numpy as np
 import pytest

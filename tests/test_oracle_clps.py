@@ -1,7 +1,7 @@
 """Pins of the single-layer CLPS clip search oracle.
 
 Paper: "CLQ" (arXiv 2509.24416), Sec. 3.4 (grid search of the quantizer
-bounds between weight quantiles, squared Frobenius objective, Eq. (2)) and
+bounds between weight quantiles, squared Frobenius objective, Eq. (3)) and
 Sec. 4.1 (beta = 0, gamma = 0.01, one percentile for all channels).  Each
 test checks the oracle against hand-worked values, an independent way of
 computing the objective, or invariants of the definition.

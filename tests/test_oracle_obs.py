@@ -2,7 +2,7 @@
 
 Paper: "CLQ" (arXiv 2509.24416), Sec. 3.3 (Orthogonal-Based Smoothing: batch
 mean, per-channel outlier metric, top half of the channels to the left) and
-Sec. 4.3 (the five outlier metrics of the ablation).  Each test checks the
+Sec. 4.2 (the five outlier metrics of the ablation).  Each test checks the
 oracle against a hand-worked value, an independent library routine, a
 closed form, or an invariant of the definition.
 """

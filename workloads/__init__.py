@@ -5,10 +5,12 @@ lives here.  It is the one module that both the GPU-side tests/bench and the
 CPU oracle use, so that both see the very same fp16 tensors.
 
 The trained PixArt-alpha / Open-Sora weights and their calibration data are
-not available, so seeded draws stand in for them.  Shapes follow the
-transformer blocks of the models the paper evaluates (Sec. 4.1: PixArt-alpha,
-hidden 1152; Open-Sora 1.2 video, hidden 1152) plus a FLUX-style width 3072
-block; activation laws plant the per-channel outliers that motivate OBS
+not available, so seeded draws stand in for them.  The paper evaluates
+PixArt-alpha and Open-Sora 1.2 (Sec. 4.1) but states neither their depth nor
+their width; the shapes here are the workload definitions this library is
+measured on (hidden 1152 with 28 blocks for the PixArt-style and video
+blocks, a FLUX-style width 3072 block), not figures from the paper.
+Activation laws plant the per-channel outliers that motivate OBS
 (Sec. 1 and Sec. 3.3: a few channels with much larger magnitude, stable
 across tokens).
 
