@@ -1,31 +1,44 @@
 """Benchmark of the W4A4 DiT-linear hot path on one MI355X.
 
-One step = the whole hot path over the four linears of a PixArt-style DiT
-block (hidden 1152, MLP 4608; 4096 image tokens x CFG batch 2 -> M = 8192;
-Hadamard block 64): for each linear, clq_rotate_quant_act on its fp16 input,
+One step = the whole hot path over the four linears of a DiT block (qkv,
+proj, fc1, fc2): for each linear, clq_rotate_quant_act on its fp16 input,
 then clq_w4a4_linear against its offline-quantized weights.  Inputs and
 weights are resident in HBM before timing starts; weights are quantized
 once, outside the timed region (as the method does offline).
 
+Default workload: the video DiT block, hidden 1152, MLP 4608, 16 latent
+frames x 30 x 45 patches x batch 2 -> M = 43200 tokens, Hadamard block 64
+(the largest per-layer shapes; rotate+quant's bandwidth-bound regime).
+`--workload pixart_block` (M = 8192) and `flux_block` (width 3072, M = 4608,
+block 128) time the other block configurations the same way.
+
 Prints ONE JSON line:
   value      effective TOPS of the step = sum(2 M N K) / step time, the step
-             time from K back-to-back steps (no events between launches)
+             time from K back-to-back steps (no events between launches);
+             step_ms_percentiles: median / p10 / p90 of single steps (HIP
+             events at step boundaries, a separate pass)
   roofline   the GEMM kernel (dominant): algorithmic int8-MFMA ops per launch
              / average launch time (HIP events on the launch stream, in a
-             second pass of K steps right after the timed one), against
-             the dense int8 peak (5.0 POP/s); traffic = HBM bytes per launch
-             from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary when
-             it was taken on the current kernel sources, else null
+             pass of K steps after the timed one), against the dense int8
+             peak (5.0 POP/s); traffic = HBM bytes per launch from the
+             committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary when it was
+             taken on the current kernel source, else null
   rotate_quant  algorithmic bytes per launch / average launch time, against
-             HBM (8 TB/s), measured in the same timed loop, and separately
-             with the 256 MB Infinity Cache flushed before every launch
+             HBM (8 TB/s), from the same pass; and per layer with the 256 MB
+             Infinity Cache flushed before every launch (cold)
+  clocks     graphics (SCLK) and memory (MCLK) clock and socket power
+             sampled through amd-smi while the timed loop runs
   cpu_baseline  the CPU oracle timed on the host cores on a bounded sample
-             of the same workload (token rows of every layer)
+             of the same workload (token rows of every layer), plus one
+             thread on a smaller sample
+  extra      the PixArt block (M = 8192) and the 28-block stack at 16384
+             tokens, timed the same way (context, not the headline)
 """
 import argparse
 import json
 import os
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -38,7 +51,12 @@ import workloads  # noqa: E402
 
 INT8_PEAK_TOPS = 5000.0      # dense int8 MFMA, MI355X (5.0 POP/s)
 HBM_PEAK_GBPS = 8000.0       # HBM3E, MI355X
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic_pixart_block_m8192.txt")
+TRAFFIC_FILES = {
+    "video_block_m43200_h1152_b64": os.path.join(ROOT, "profiles", "gemm_traffic_video_block_m43200.txt"),
+    "pixart_block_m8192_h1152_b64": os.path.join(ROOT, "profiles", "gemm_traffic_pixart_block_m8192.txt"),
+    "flux_block_m4608_h3072_b128": os.path.join(ROOT, "profiles", "gemm_traffic_flux_block_m4608.txt"),
+}
+BLOCKS = {"video_block": workloads.C4, "pixart_block": workloads.C2, "flux_block": workloads.C3}
 
 
 def rq_bytes(l, abits=4):
@@ -52,13 +70,21 @@ def gemm_ops(l):
     return 2 * l.M * l.N * l.K
 
 
-def load_traffic(kernel_src_sha):
-    """Per-launch HBM traffic from the committed rocprofv3 PMC summary, only
-    if it was taken on the current kernel source."""
-    if not os.path.exists(TRAFFIC_FILE):
+def rq_kernel_name(l, abits=4):
+    """The activation kernel the library runs for this layer: the 8-row
+    kernel for rows of 2048..5120 codes at block 64, else the batched one."""
+    if l.block == 64 and 2048 <= l.K <= 5120:
+        return f"rq_rows8_kernel<64, {abits}, false>"
+    return f"rq_act_kernel<{l.block}, {abits}, false>"
+
+
+def load_traffic(path, kernel_src_sha):
+    """Per-launch HBM traffic from a committed rocprofv3 PMC summary, only if
+    it was taken on the current kernel source."""
+    if path is None or not os.path.exists(path):
         return None
     vals = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if line.startswith("traffic:"):
             for kv in line.split()[1:]:
                 k, v = kv.split("=")
@@ -77,10 +103,122 @@ def kernel_sha():
     return h.hexdigest()[:16]
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def blas_threads():
+    """Threads of numpy's BLAS (the numpy oracles' matrix products), as the
+    thread-pool library reports them; 1 if it cannot tell."""
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        return int(max(n)) if n else 1
+    except Exception:
+        return 1
+
+
+class ClockSampler:
+    """Samples the GPU's graphics and memory clocks and socket power through
+    amd-smi in a background thread (every ~20 ms) while a timed region runs.
+    Reports None where amd-smi is unavailable."""
+
+    def __init__(self, torch, dev):
+        self.samples = []
+        self.handle = None
+        self.err = None
+        try:
+            import amdsmi
+            self.amdsmi = amdsmi
+            amdsmi.amdsmi_init()
+            handles = amdsmi.amdsmi_get_processor_handles()
+            want = None
+            try:
+                p = torch.cuda.get_device_properties(dev)
+                want = (int(getattr(p, "pci_domain_id", 0)), int(p.pci_bus_id), int(p.pci_device_id))
+            except Exception:
+                pass
+            for h in handles:
+                if want is None:
+                    break
+                bdf = amdsmi.amdsmi_get_gpu_device_bdf(h)   # "dddd:bb:dd.f"
+                dom, bus, rest = bdf.split(":")
+                if (int(dom, 16), int(bus, 16), int(rest.split(".")[0], 16)) == want:
+                    self.handle = h
+                    break
+            if self.handle is None and len(handles) == 1:
+                self.handle = handles[0]
+        except Exception as e:   # no amd-smi: clocks are reported as null
+            self.err = repr(e)
+        self._stop = threading.Event()
+        self._t = None
+
+    def _read(self):
+        a = self.amdsmi
+        g = a.amdsmi_get_clock_info(self.handle, a.AmdSmiClkType.GFX)["clk"]
+        m = a.amdsmi_get_clock_info(self.handle, a.AmdSmiClkType.MEM)["clk"]
+        pw = None
+        try:
+            pi = a.amdsmi_get_power_info(self.handle)
+            pw = pi.get("socket_power") or pi.get("current_socket_power") or pi.get("average_socket_power")
+        except Exception:
+            pass
+        return g, m, pw
+
+    def _loop(self):
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self._read())
+            except Exception as e:
+                self.err = repr(e)
+                return
+            time.sleep(0.02)
+
+    def __enter__(self):
+        if self.handle is not None:
+            self._t = threading.Thread(target=self._loop, daemon=True)
+            self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._t is not None:
+            self._t.join()
+
+    def summary(self):
+        if not self.samples:
+            return {"sclk_mhz": None, "mclk_mhz": None, "power_w": None, "samples": 0,
+                    "note": self.err or "amd-smi handle not found"}
+        a = np.array([[x if isinstance(x, (int, float)) else np.nan for x in s] for s in self.samples],
+                     dtype=np.float64)
+
+        def stats(col):
+            v = a[:, col]
+            v = v[np.isfinite(v)]
+            if v.size == 0:
+                return None
+            return {"median": float(np.median(v)), "min": float(v.min()), "max": float(v.max())}
+        return {"sclk_mhz": stats(0), "mclk_mhz": stats(1), "power_w": stats(2), "samples": int(a.shape[0])}
+
+
+def pct(v):
+    v = np.asarray(v, np.float64)
+    return {"median": round(float(np.median(v)), 5), "p10": round(float(np.percentile(v, 10)), 5),
+            "p90": round(float(np.percentile(v, 90)), 5)}
+
+
 def cpu_baseline(layers, inputs, budget_s=15.0, wbits=4, abits=4):
     """Times the CPU oracle's online path (rotate + quantize the activations,
     integer GEMM, fp64 epilogue) on a sample of token rows of every layer,
-    sized to roughly budget_s seconds; returns TOPS on that sample."""
+    sized to roughly budget_s seconds, on all the threads the oracle uses,
+    then on one thread for a fifth of the budget; returns TOPS on those
+    samples."""
     import oracle
     threads = oracle.get_threads()
     wq = {}
@@ -100,13 +238,161 @@ def cpu_baseline(layers, inputs, budget_s=15.0, wbits=4, abits=4):
             ops += 2 * rows * l.N * l.K
         return time.perf_counter() - t0, ops
 
-    t_cal, _ = run(64)
-    rows = int(min(layers[0].M, max(64, 64 * budget_s / max(t_cal, 1e-3))))
-    rows = max(16, rows // 16 * 16)
+    def sized(budget):
+        t_cal, _ = run(32)
+        rows = int(min(layers[0].M, max(32, 32 * budget / max(t_cal, 1e-3))))
+        return max(16, rows // 16 * 16)
+
+    rows = sized(budget_s)
     t, ops = run(rows)
-    return {"value": ops / t / 1e12, "unit": "TOPS", "cores": threads, "kind": "oracle",
-            "sample": f"first {rows} token rows of each of the {len(layers)} linears "
-                      f"({ops / 2e9:.1f} G MAC, {t:.1f} s; weights quantized beforehand, untimed)"}
+    out = {"value": ops / t / 1e12, "unit": "TOPS", "cores": threads, "kind": "oracle",
+           "cpu_model": cpu_model(),
+           "sample": f"first {rows} token rows of each of the {len(layers)} linears "
+                     f"({ops / 2e9:.1f} G MAC, {t:.1f} s; weights quantized beforehand, untimed)"}
+    try:
+        oracle.set_threads(1)
+        rows1 = sized(budget_s / 5)
+        t1, ops1 = run(rows1)
+        out["single_thread"] = {"value": ops1 / t1 / 1e12, "unit": "TOPS", "cores": 1,
+                                "sample": f"first {rows1} token rows of each linear ({t1:.1f} s)"}
+    finally:
+        oracle.set_threads(threads)
+    return out
+
+
+def bench_block(wl, args, clq, torch, dev, wbits=4, abits=4, steps=None, warmup=None, cold_reps=None,
+                sample_clocks=True):
+    """Times the hot path over the four linears of a DiT block workload.
+    Returns a dict of measurements (see the module docstring)."""
+    steps = args.steps if steps is None else steps
+    warmup = args.warmup if warmup is None else warmup
+    cold_reps = args.cold_reps if cold_reps is None else cold_reps
+    layers = list(wl.layers)
+    inputs = {l.name: workloads.layer_inputs(l) for l in layers}
+    quant_w = clq.clq_quantize_weights if wbits == 4 else clq.clq_quantize_weights8
+    if abits == 4:
+        act_bytes, rq_fn, lin_fn = clq.clq_act_bytes, clq.clq_rotate_quant_act, clq.clq_w4a4_linear
+    else:
+        act_bytes, rq_fn, lin_fn = clq.clq_act8_bytes, clq.clq_rotate_quant_act8, clq.clq_a8_linear
+
+    # resident device data; weights quantized once (offline step)
+    state = []
+    for l in layers:
+        X, W, b = inputs[l.name]
+        Xd = torch.from_numpy(X).to(dev)
+        qw = quant_w(torch.from_numpy(W).to(dev), l.block)
+        bd = torch.from_numpy(b).to(dev)
+        Xq = torch.empty(act_bytes(l.M, l.K), dtype=torch.uint8, device=dev)
+        xs = torch.empty(l.M, dtype=torch.float32, device=dev)
+        Y = torch.empty((l.M, l.N), dtype=torch.float16, device=dev)
+        state.append((l, Xd, qw, bd, Xq, xs, Y))
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(events=None):
+        for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
+            if events is not None:
+                events[i][0].record(stream)
+            rq_fn(Xd, l.block, out=Xq, scale_out=xs)
+            if events is not None:
+                events[i][1].record(stream)
+            lin_fn(Xq, xs, qw, bd, out=Y)
+            if events is not None:
+                events[i][2].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` steps, launched back to back
+    sampler = ClockSampler(torch, dev) if sample_clocks else None
+    if sampler is not None:
+        sampler.__enter__()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if sampler is not None:
+        sampler.__exit__()
+    ms_per_step = wall * 1e3 / steps
+
+    # single-step times: one event pair per step, nothing between launches
+    se = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for s in range(steps):
+        se[s][0].record(stream)
+        step()
+        se[s][1].record(stream)
+    torch.cuda.synchronize()
+    step_ms = [a.elapsed_time(b) for a, b in se]
+
+    # per-launch pass: the same `steps` steps again with HIP events recorded
+    # around every launch on the launch stream (the records themselves add
+    # gaps between launches, so the step time above is taken without them)
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for s in range(steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    rq_t = np.array([[ev[s][i][0].elapsed_time(ev[s][i][1]) for i in range(len(layers))] for s in range(steps)])
+    gm_t = np.array([[ev[s][i][1].elapsed_time(ev[s][i][2]) for i in range(len(layers))] for s in range(steps)])
+    rq_ms = rq_t.mean(axis=0)
+    gemm_ms = gm_t.mean(axis=0)
+
+    # rotate+quant and GEMM with the Infinity Cache flushed before each launch
+    # (by reading 512 MB: a flush that writes would leave dirty lines to be
+    # written back during the timed launch)
+    cold_rq = np.full(len(layers), np.nan)
+    cold_gemm = np.full(len(layers), np.nan)
+    if cold_reps > 0:
+        flush = torch.ones(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
+            t_rq, t_g = [], []
+            for _ in range(cold_reps):
+                flush.sum()
+                e0.record(stream)
+                rq_fn(Xd, l.block, out=Xq, scale_out=xs)
+                e1.record(stream)
+                e1.synchronize()
+                t_rq.append(e0.elapsed_time(e1))
+                flush.sum()
+                e0.record(stream)
+                lin_fn(Xq, xs, qw, bd, out=Y)
+                e1.record(stream)
+                e1.synchronize()
+                t_g.append(e0.elapsed_time(e1))
+            cold_rq[i] = np.median(t_rq)
+            cold_gemm[i] = np.median(t_g)
+        del flush
+    res = dict(layers=layers, inputs=inputs, ms_per_step=ms_per_step, step_ms=step_ms, rq_t=rq_t, gm_t=gm_t,
+               rq_ms=rq_ms, gemm_ms=gemm_ms, cold_rq=cold_rq, cold_gemm=cold_gemm,
+               clocks=sampler.summary() if sampler is not None else None,
+               total_ops=sum(gemm_ops(l) for l in layers))
+    del state
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def block_summary(wl, r, abits=4):
+    """Compact per-layer and per-kernel figures of a bench_block result."""
+    layers = r["layers"]
+    value = r["total_ops"] / (r["ms_per_step"] * 1e-3) / 1e12
+    gemm_avg_ms = float(r["gemm_ms"].mean())
+    ops_launch = r["total_ops"] / len(layers)
+    per = {}
+    for i, l in enumerate(layers):
+        per[l.name] = {
+            "M": l.M, "K": l.K, "N": l.N,
+            "gemm_us": pct(r["gm_t"][:, i] * 1e3), "gemm_TOPS": round(gemm_ops(l) / (r["gemm_ms"][i] * 1e-3) / 1e12, 1),
+            "gemm_cold_us": round(float(r["cold_gemm"][i]) * 1e3, 2) if np.isfinite(r["cold_gemm"][i]) else None,
+            "rq_kernel": rq_kernel_name(l, abits),
+            "rq_us": pct(r["rq_t"][:, i] * 1e3), "rq_GBps": round(rq_bytes(l, abits) / (r["rq_ms"][i] * 1e-3) / 1e9, 1),
+            "rq_cold_us": round(float(r["cold_rq"][i]) * 1e3, 2) if np.isfinite(r["cold_rq"][i]) else None,
+            "rq_cold_GBps": (round(rq_bytes(l, abits) / (r["cold_rq"][i] * 1e-3) / 1e9, 1)
+                             if np.isfinite(r["cold_rq"][i]) else None)}
+    return dict(value=value, gemm_avg_ms=gemm_avg_ms, ops_launch=ops_launch, per=per)
 
 
 def obs_bytes(B, N, D, metric):
@@ -251,82 +537,102 @@ def bench_clps(args, clq, torch, dev):
         oclps.search(X[:256], W, Y0h, b, G=4)
         t = time.perf_counter() - t0
         out["cpu_baseline"] = {"value": round(4 * 2.0 * 256 * N * K / t / 1e12, 4), "unit": "TOPS",
-                               "cores": 16, "kind": "oracle",
+                               "cores": blas_threads(), "kind": "oracle", "cpu_model": cpu_model(),
                                "sample": f"256 of the 4096 tokens, 4 of the 20 candidates ({t:.1f} s)"}
     print(json.dumps(out), flush=True)
 
 
-def bench_stack(args, clq, torch, dev):
-    """The multi-layer path: 28 PixArt-width DiT blocks (112 linears, 223 MB
-    of resident int4 weights), rotate+quant + W4A4 GEMM per linear, replayed
-    as one HIP graph.  value = effective TOPS at M = 4096 tokens; the eager
-    (launch-by-launch) step and M = 1024 / 16384 are reported beside it."""
+_STACK_W = {}
+
+
+def stack_weights(torch, dev, nb=28):
+    """Device weights and biases of the 28-block stack (drawn once; they do
+    not depend on M or the block size)."""
+    if nb not in _STACK_W:
+        wl = workloads.dit_stack(nb, 4096, 64)
+        weights = []
+        for j in range(nb):
+            blk = {}
+            for l in wl.layers[4 * j:4 * j + 4]:
+                blk[l.name.split(".")[1]] = (torch.from_numpy(workloads.weights(l.N, l.K, l.seed + 1)).to(dev),
+                                             torch.from_numpy(workloads.bias(l.N, l.seed + 2)).to(dev))
+            weights.append(blk)
+        _STACK_W[nb] = weights
+    return _STACK_W[nb]
+
+
+def stack_point(clq, torch, dev, M, b, steps, perms=None, fold=False, eager=False):
+    """One stack configuration: graph replays timed back to back, plus
+    single-replay percentiles (events at replay boundaries)."""
     from paper_2509_24416_amd.stack import DiTStack
-    nb, b = 28, 64
-    # weights are generated once (at the largest M; shapes do not depend on M)
-    wl = workloads.dit_stack(nb, 4096, b)
-    weights = []
-    for j in range(nb):
-        blk = {}
-        for l in wl.layers[4 * j:4 * j + 4]:
-            blk[l.name.split(".")[1]] = (torch.from_numpy(workloads.weights(l.N, l.K, l.seed + 1)).to(dev),
-                                         torch.from_numpy(workloads.bias(l.N, l.seed + 2)).to(dev))
-        weights.append(blk)
-    res = {}
-    for M in (4096, 1024, 16384):
-        st = DiTStack(weights, M, b)
-        x = torch.from_numpy(workloads.activations(M, 1152, "L1", 500)).to(dev)
-        st.forward(x)
-        st.capture()
-        steps = args.steps if M == 4096 else max(5, args.steps // 4)
-        for _ in range(3):
-            st.replay()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(steps):
-            st.replay()
-        torch.cuda.synchronize()
-        g_ms = (time.perf_counter() - t0) * 1e3 / steps
+    st = DiTStack(stack_weights(torch, dev), M, b, perms=perms, fold=fold)
+    x = torch.from_numpy(workloads.activations(M, 1152, "L1", 500)).to(dev)
+    st.forward(x)
+    st.capture()
+    for _ in range(3):
+        st.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        st.replay()
+    torch.cuda.synchronize()
+    g_ms = (time.perf_counter() - t0) * 1e3 / steps
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, e in ev:
+        a.record(stream)
+        st.replay()
+        e.record(stream)
+    torch.cuda.synchronize()
+    out = {"graph_ms": round(g_ms, 4), "graph_TOPS": round(st.ops / (g_ms * 1e-3) / 1e12, 1),
+           "replay_ms_percentiles": pct([a.elapsed_time(e) for a, e in ev]), "launches_per_step": 224}
+    if eager:
         t0 = time.perf_counter()
         for _ in range(steps):
             st.forward()
         torch.cuda.synchronize()
         e_ms = (time.perf_counter() - t0) * 1e3 / steps
-        res[M] = (g_ms, e_ms, st.ops)
-        del st
-        torch.cuda.synchronize()
+        out["eager_ms"] = round(e_ms, 4)
+        out["eager_TOPS"] = round(st.ops / (e_ms * 1e-3) / 1e12, 1)
+    out["ops"] = st.ops
+    del st
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_stack(args, clq, torch, dev):
+    """The multi-layer path: 28 PixArt-width DiT blocks (112 linears, 223 MB
+    of resident int4 weights), rotate+quant + W4A4 GEMM per linear, replayed
+    as one HIP graph.  value = effective TOPS at M = 4096 tokens, block 64;
+    M = 1024 / 16384, the eager step and the Hadamard block sweep 32 / 64 /
+    128 at every M are reported beside it."""
+    nb = 28
+    res = {}
+    for M in (4096, 1024, 16384):
+        for b in (64, 32, 128):
+            steps = args.steps if M == 4096 else max(5, args.steps // 4)
+            print(f"bench: dit_stack M={M} block={b}", file=sys.stderr, flush=True)
+            res[(M, b)] = stack_point(clq, torch, dev, M, b, steps, eager=(b == 64))
     # one swap vector per layer input (random stand-ins for OBS outputs):
     # gathered by every rotate+quant, or folded into the producing layers
     from paper_2509_24416_amd.stack import LAYERS
+    weights = stack_weights(torch, dev)
     perms = [{name: torch.from_numpy(workloads.random_perm(weights[j][name][0].shape[1], 1000 + 4 * j + i)).to(dev)
               for i, name in enumerate(LAYERS)} for j in range(nb)]
     swap = {}
     for fold in (False, True):
-        st = DiTStack(weights, 4096, b, perms=perms, fold=fold)
-        x = torch.from_numpy(workloads.activations(4096, 1152, "L1", 500)).to(dev)
-        st.forward(x)
-        st.capture()
-        for _ in range(3):
-            st.replay()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            st.replay()
-        torch.cuda.synchronize()
-        swap["folded_ms" if fold else "gather_ms"] = round((time.perf_counter() - t0) * 1e3 / args.steps, 4)
-        del st
-        torch.cuda.synchronize()
-    g_ms, e_ms, ops = res[4096]
+        swap["folded_ms" if fold else "gather_ms"] = stack_point(clq, torch, dev, 4096, 64, args.steps,
+                                                                 perms=perms, fold=fold)["graph_ms"]
+    head = res[(4096, 64)]
     out = {
         "metric": "DiT stack (28 blocks x 4 W4A4 linears) effective TOPS, one HIP graph per step",
-        "value": round(ops / (g_ms * 1e-3) / 1e12, 2), "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
-        "warmup": 3, "ms_per_step": round(g_ms, 4), "higher_is_better": True, "scaling": "weak",
+        "value": head["graph_TOPS"], "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": 3, "ms_per_step": head["graph_ms"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "int4", "data": "synthetic",
-        "config": {"workload": "dit_stack_28x4_m4096_h1152_b64", "blocks": nb, "M": 4096, "block": b,
+        "config": {"workload": "dit_stack_28x4_m4096_h1152_b64", "blocks": nb, "M": 4096, "block": 64,
                    "launches_per_step": 2 * 4 * nb, "parallelism": "none (one GPU)"},
-        "per_M": {str(M): {"graph_ms": round(v[0], 4), "eager_ms": round(v[1], 4),
-                           "graph_TOPS": round(v[2] / (v[0] * 1e-3) / 1e12, 1),
-                           "eager_TOPS": round(v[2] / (v[1] * 1e-3) / 1e12, 1)} for M, v in res.items()},
+        "per_M_block": {f"M{M}_b{b}": v for (M, b), v in res.items()},
         "swap_vectors_m4096": swap,
         "gpu": torch.cuda.get_device_name(dev),
     }
@@ -336,16 +642,21 @@ def bench_stack(args, clq, torch, dev):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=1000)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--cold-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", default="pixart_block",
-                    choices=["pixart_block", "pixart_block_w4a8", "pixart_block_w8a8", "obs_calibration",
-                             "clps_search", "dit_stack"],
-                    help="pixart_block: the W4A4 linear hot path (default); pixart_block_w4a8 / _w8a8: the "
-                         "same block at 8-bit activations (and weights); obs_calibration: the OBS "
-                         "channel-score pass over a calibration batch")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the PixArt block and 28-block stack figures beside the headline")
+    ap.add_argument("--workload", default="video_block",
+                    choices=["video_block", "pixart_block", "flux_block", "video_block_w4a8", "video_block_w8a8",
+                             "pixart_block_w4a8", "pixart_block_w8a8", "obs_calibration", "clps_search",
+                             "dit_stack"],
+                    help="video_block: the W4A4 hot path on the video DiT block, M = 43200 (default); "
+                         "pixart_block (M = 8192) and flux_block (width 3072, M = 4608, block 128): the same "
+                         "on the other block configurations; *_w4a8 / *_w8a8: 8-bit activations (and "
+                         "weights); obs_calibration: the OBS channel-score pass; clps_search: the CLPS "
+                         "clip search; dit_stack: the 28-block stack, one HIP graph per step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (reference for the HBM "
                          "byte counters) and exit")
@@ -380,153 +691,94 @@ def main():
         bench_stack(args, clq, torch, dev)
         return
 
-    wl = workloads.C2
-    layers = list(wl.layers)
-    inputs = {l.name: workloads.layer_inputs(l) for l in layers}
-    # bit setting (Sec. 4.1: W4A4, W4A8, W8A8)
-    wbits, abits = {"pixart_block": (4, 4), "pixart_block_w4a8": (4, 8),
-                    "pixart_block_w8a8": (8, 8)}[args.workload]
-    quant_w = clq.clq_quantize_weights if wbits == 4 else clq.clq_quantize_weights8
-    if abits == 4:
-        act_bytes, rq_fn, lin_fn = clq.clq_act_bytes, clq.clq_rotate_quant_act, clq.clq_w4a4_linear
-    else:
-        act_bytes, rq_fn, lin_fn = clq.clq_act8_bytes, clq.clq_rotate_quant_act8, clq.clq_a8_linear
-
-    # resident device data; weights quantized once (offline step)
-    state = []
-    for l in layers:
-        X, W, b = inputs[l.name]
-        Xd = torch.from_numpy(X).to(dev)
-        qw = quant_w(torch.from_numpy(W).to(dev), l.block)
-        bd = torch.from_numpy(b).to(dev)
-        Xq = torch.empty(act_bytes(l.M, l.K), dtype=torch.uint8, device=dev)
-        xs = torch.empty(l.M, dtype=torch.float32, device=dev)
-        Y = torch.empty((l.M, l.N), dtype=torch.float16, device=dev)
-        state.append((l, Xd, qw, bd, Xq, xs, Y))
-    stream = torch.cuda.current_stream()
-    torch.cuda.synchronize()
-
-    def step(events=None):
-        for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
-            if events is not None:
-                events[i][0].record(stream)
-            rq_fn(Xd, l.block, out=Xq, scale_out=xs)
-            if events is not None:
-                events[i][1].record(stream)
-            lin_fn(Xq, xs, qw, bd, out=Y)
-            if events is not None:
-                events[i][2].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # timed region: exactly `steps` steps, launched back to back
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
-
-    # per-launch pass: the same `steps` steps again with HIP events recorded
-    # around every launch on the launch stream (the records themselves add
-    # gaps between launches, so the step time above is taken without them)
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
-          for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for s in range(args.steps):
-        step(ev[s])
-    torch.cuda.synchronize()
-
-    rq_ms = np.zeros(len(layers))
-    gemm_ms = np.zeros(len(layers))
-    for s in range(args.steps):
-        for i in range(len(layers)):
-            rq_ms[i] += ev[s][i][0].elapsed_time(ev[s][i][1])
-            gemm_ms[i] += ev[s][i][1].elapsed_time(ev[s][i][2])
-    rq_ms /= args.steps
-    gemm_ms /= args.steps
-
-    total_ops = sum(gemm_ops(l) for l in layers)
-    value = total_ops / (ms_per_step * 1e-3) / 1e12
-    gemm_tops = [gemm_ops(l) / (gemm_ms[i] * 1e-3) / 1e12 for i, l in enumerate(layers)]
-    gemm_avg_ms = float(gemm_ms.mean())
-    gemm_ops_per_launch = total_ops / len(layers)
-    achieved = gemm_ops_per_launch / (gemm_avg_ms * 1e-3) / 1e12
-    rq_gbps = [rq_bytes(l, abits) / (rq_ms[i] * 1e-3) / 1e9 for i, l in enumerate(layers)]
+    base = args.workload.split("_w")[0]
+    wbits, abits = 4, 4
+    if args.workload.endswith("_w4a8"):
+        wbits, abits = 4, 8
+    elif args.workload.endswith("_w8a8"):
+        wbits, abits = 8, 8
+    wl = BLOCKS[base]
+    print(f"bench: {wl.name} W{wbits}A{abits}: {args.warmup} warmup + {args.steps} timed steps",
+          file=sys.stderr, flush=True)
+    r = bench_block(wl, args, clq, torch, dev, wbits, abits)
+    sm = block_summary(wl, r, abits)
+    layers = r["layers"]
+    achieved = sm["ops_launch"] / (sm["gemm_avg_ms"] * 1e-3) / 1e12
     rq_avg_bytes = sum(rq_bytes(l, abits) for l in layers) / len(layers)
-    rq_achieved = rq_avg_bytes / (float(rq_ms.mean()) * 1e-3) / 1e9
-
-    # rotate+quant and GEMM with the Infinity Cache flushed before each launch
-    # (by reading 512 MB: a flush that writes would leave dirty lines to be
-    # written back during the timed launch)
-    flush = torch.ones(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
-    cold_rq = np.zeros(len(layers))
-    cold_gemm = np.zeros(len(layers))
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for i, (l, Xd, qw, bd, Xq, xs, Y) in enumerate(state):
-        t_rq, t_g = [], []
-        for _ in range(args.cold_reps):
-            flush.sum()
-            e0.record(stream)
-            rq_fn(Xd, l.block, out=Xq, scale_out=xs)
-            e1.record(stream)
-            e1.synchronize()
-            t_rq.append(e0.elapsed_time(e1))
-            flush.sum()
-            e0.record(stream)
-            lin_fn(Xq, xs, qw, bd, out=Y)
-            e1.record(stream)
-            e1.synchronize()
-            t_g.append(e0.elapsed_time(e1))
-        cold_rq[i] = np.median(t_rq)
-        cold_gemm[i] = np.median(t_g)
-    del flush
-
-    traffic = load_traffic(kernel_sha()) if (wbits, abits) == (4, 4) else None
+    rq_achieved = rq_avg_bytes / (float(r["rq_ms"].mean()) * 1e-3) / 1e9
+    cold_bytes = sum(rq_bytes(l, abits) for l in layers)
+    cold_rq_total = float(np.nansum(r["cold_rq"]))
+    traffic = load_traffic(TRAFFIC_FILES.get(wl.name), kernel_sha()) if (wbits, abits) == (4, 4) else None
+    plans = [clq.clq_w4a4_schedule(l.M, l.N, l.K) for l in layers] if abits == 4 else None
+    if abits == 4:
+        kinds = sorted({("w4a4_gemm_kernel" if p["kernel"] == 0 else "w4a4_gemm_halves_kernel") for p in plans})
+        gemm_name = " / ".join(kinds) + " (mean over the 4 linears)"
+    else:
+        gemm_name = f"a8_gemm_kernel<{wbits}> (mean over the 4 linears)"
     setting = f"W{wbits}A{abits}"
     out = {
         "metric": f"{setting} linear effective TOPS + % int8-MFMA peak; rotate+quant HBM GB/s",
-        "value": round(value, 2),
+        "value": round(sm["value"], 2),
         "unit": "TOPS",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": round(r["ms_per_step"], 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int4" if (wbits, abits) == (4, 4) else ("int4 x int8" if wbits == 4 else "int8"),
         "data": "synthetic",
-        "config": {"workload": wl.name + ("" if abits == 4 else f"_{setting.lower()}"), "M": layers[0].M,
-                   "hidden": 1152, "mlp": 4608,
-                   "block": 64, "layers": {l.name.split(".")[1]: [l.K, l.N] for l in layers},
+        "config": {"workload": wl.name + ("" if (wbits, abits) == (4, 4) else f"_{setting.lower()}"),
+                   "M": layers[0].M, "hidden": layers[0].K, "mlp": layers[2].N,
+                   "block": layers[0].block, "layers": {l.name.split(".")[1]: [l.K, l.N] for l in layers},
                    "parallelism": "none (one GPU)"},
-        "pct_int8_peak": round(100 * value / INT8_PEAK_TOPS, 2),
-        "roofline": {"kernel": ("W4A4 GEMM: w4a4_gemm_kernel (qkv, fc1) and w4a4_gemm_halves_kernel (proj, fc2), mean over the 4 linears" if abits == 4 else
-                                f"a8_gemm_kernel<{wbits}> (128 ch x 128 tok tiles)"),
-                     "bound": "mfma", "achieved": round(achieved, 1),
+        "pct_int8_peak": round(100 * sm["value"] / INT8_PEAK_TOPS, 2),
+        "step_ms_percentiles": pct(r["step_ms"]),
+        "roofline": {"kernel": gemm_name, "bound": "mfma", "achieved": round(achieved, 1),
                      "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / INT8_PEAK_TOPS, 4),
-                     "traffic": traffic, "avg_launch_us": round(gemm_avg_ms * 1e3, 2),
-                     "ops_per_launch": gemm_ops_per_launch},
-        "rotate_quant": {"kernel": f"rq_act_kernel<64, {abits}>", "bound": "hbm",
+                     "traffic": traffic, "avg_launch_us": round(sm["gemm_avg_ms"] * 1e3, 2),
+                     "ops_per_launch": sm["ops_launch"],
+                     "launch_us_percentiles": pct(r["gm_t"].mean(axis=1) * 1e3)},
+        "rotate_quant": {"kernels": {l.name: rq_kernel_name(l, abits) for l in layers}, "bound": "hbm",
                          "achieved": round(rq_achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": round(rq_achieved / HBM_PEAK_GBPS, 4),
-                         "avg_launch_us": round(float(rq_ms.mean()) * 1e3, 2),
+                         "avg_launch_us": round(float(r["rq_ms"].mean()) * 1e3, 2),
                          "bytes_per_launch": rq_avg_bytes,
-                         "cold_cache_GBps": {l.name: round(rq_bytes(l, abits) / (cold_rq[i] * 1e-3) / 1e9, 1)
-                                             for i, l in enumerate(layers)}},
-        "per_layer": {l.name: {"gemm_us": round(gemm_ms[i] * 1e3, 2), "gemm_TOPS": round(gemm_tops[i], 1),
-                               "gemm_cold_us": round(cold_gemm[i] * 1e3, 2),
-                               "rq_us": round(rq_ms[i] * 1e3, 2), "rq_GBps": round(rq_gbps[i], 1),
-                               "rq_cold_us": round(cold_rq[i] * 1e3, 2)}
-                      for i, l in enumerate(layers)},
+                         "cold_GBps_all_layers": (round(cold_bytes / (cold_rq_total * 1e-3) / 1e9, 1)
+                                                  if cold_rq_total > 0 else None),
+                         "cold_frac_all_layers": (round(cold_bytes / (cold_rq_total * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)
+                                                  if cold_rq_total > 0 else None)},
+        "per_layer": sm["per"],
+        "gemm_schedule": ({l.name: plans[i] for i, l in enumerate(layers)} if plans else None),
+        "clocks": r["clocks"],
         "gpu": torch.cuda.get_device_name(dev),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers, inputs, wbits=wbits, abits=abits)
+        out["cpu_baseline"] = cpu_baseline(layers, r["inputs"], wbits=wbits, abits=abits)
+    r = None
+    if not args.no_extra and (wbits, abits) == (4, 4):
+        extra = {}
+        for name in ("video_block", "pixart_block"):
+            if name == base:
+                continue
+            wl2 = BLOCKS[name]
+            print(f"bench: extra {wl2.name}", file=sys.stderr, flush=True)
+            r2 = bench_block(wl2, args, clq, torch, dev, steps=max(20, args.steps // 2),
+                             warmup=max(20, args.warmup // 2), cold_reps=0, sample_clocks=False)
+            s2 = block_summary(wl2, r2)
+            extra[wl2.name] = {"value_TOPS": round(s2["value"], 2), "ms_per_step": round(r2["ms_per_step"], 5),
+                               "step_ms_percentiles": pct(r2["step_ms"]),
+                               "gemm_avg_us": round(s2["gemm_avg_ms"] * 1e3, 2),
+                               "gemm_frac": round(s2["ops_launch"] / (s2["gemm_avg_ms"] * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+                               "per_layer": {k: {"gemm_us": v["gemm_us"]["median"], "gemm_TOPS": v["gemm_TOPS"],
+                                                 "rq_us": v["rq_us"]["median"], "rq_GBps": v["rq_GBps"]}
+                                             for k, v in s2["per"].items()}}
+            del r2
+        print("bench: extra dit_stack m16384", file=sys.stderr, flush=True)
+        extra["dit_stack_28x4_m16384_h1152_b64"] = stack_point(clq, torch, dev, 16384, 64, steps=20)
+        out["extra"] = extra
     print(json.dumps(out), flush=True)
 
 

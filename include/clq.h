@@ -121,8 +121,34 @@ clq_status clq_rotate_quant_act(const void *X, int64_t ldx, const int32_t *perm,
 /* Size in bytes of the optional GEMM workspace (depends only on the current
  * device's compute-unit count; a few tens of MB).  With a workspace the GEMM
  * may split the k loop of its last tile rounds over every workgroup, which
- * balances shapes whose tile count fills the chip badly. */
+ * balances shapes whose tile count fills the chip badly.
+ *
+ * The split schedule assumes that all of the GEMM's workgroups (two per
+ * compute unit) are resident at once: the workgroup that owns a split tile
+ * waits for the others' partial sums.  The wait is bounded (about a second).
+ * Kernels of other streams holding compute units can delay a contributor
+ * past that bound; the owner then leaves that partial out and the call's
+ * output is wrong.  Every such event is counted in the workspace's status
+ * words (clq_w4a4_workspace_status).  Callers that cannot rule this out pass
+ * workspace = NULL (whole tiles only, no waiting) or check the status. */
 size_t clq_w4a4_workspace_bytes(void);
+
+/* Diagnostic (host only, nothing enqueued): the schedule clq_w4a4_linear
+ * picks for an M x N x K product on the current device, with or without a
+ * workspace, as info[0..4] = {kernel (0: persistent grid of 256-token
+ * tiles, 1 / 2: two halves of the k loop per 128- / 64-token tile), output
+ * tiles, tiles computed whole, k-stages (of 64 codes) split across the
+ * grid, workgroups launched}. */
+clq_status clq_w4a4_schedule(int64_t M, int64_t N, int64_t K, int32_t with_workspace, int64_t *info);
+
+/* Enqueues a copy of the workspace's split-k status words to `status`
+ * (device int32 [3]): [0] the number of waits that gave up since the
+ * workspace was last zero-filled (0 = every result was complete), [1] the
+ * first such output tile, [2] the rank of its missing contributor.  After a
+ * nonzero count, synchronise and zero-fill the workspace before reusing it:
+ * the late contributor's flag may still be raised. */
+clq_status clq_w4a4_workspace_status(const void *workspace, size_t workspace_bytes,
+                                     int32_t *status, hipStream_t stream);
 
 /* W4A4 linear: Y = dequant(Xq . Wq^T) + bias, written as fp16 (Eq. (1): the
  * integer product of the codes times the two scales).
@@ -307,6 +333,29 @@ clq_status clq_clps_search(const void *X, int64_t ldx, const void *W, const floa
                            int64_t K, int32_t block, float gamma, int32_t grid,
                            void *workspace, size_t workspace_bytes, float *alphas,
                            double *errors, int32_t *best, hipStream_t stream);
+
+/* ---- Debugging and test knobs ------------------------------------------------
+ * Process-wide host settings, read by every later call (any thread).
+ *   CLQ_DEBUG_SYNC              1: each entry point waits for the kernels it
+ *                               enqueued and returns CLQ_ERR_HIP if they
+ *                               failed (not for use under stream capture).
+ *                               Initial value from the CLQ_SYNC environment
+ *                               variable (unset or "0" = off).
+ *   CLQ_DEBUG_SPLIT_SPIN_LIMIT  bound on a split-k wait, in sleeps of about
+ *                               0.2 us (default 2^22); 0 .. 2^30.
+ *   CLQ_DEBUG_SPLIT_DROP_SIGNAL 1: split-k contributors never signal, so every
+ *                               owner's wait runs out (tests of the failure
+ *                               report only: outputs are then wrong).
+ * clq_debug_set returns CLQ_ERR_ARG for an unknown knob or a value out of
+ * range; clq_debug_get returns the current value, or -1 for an unknown knob. */
+typedef enum {
+    CLQ_DEBUG_SYNC = 0,
+    CLQ_DEBUG_SPLIT_SPIN_LIMIT = 1,
+    CLQ_DEBUG_SPLIT_DROP_SIGNAL = 2
+} clq_debug_knob;
+
+clq_status clq_debug_set(int32_t knob, int64_t value);
+int64_t clq_debug_get(int32_t knob);
 
 #ifdef __cplusplus
 }

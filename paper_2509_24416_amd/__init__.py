@@ -77,11 +77,17 @@ _lib.clq_clps_workspace_bytes.restype = ctypes.c_size_t
 _lib.clq_clps_workspace_bytes.argtypes = [_i64, _i64, _i64]
 _lib.clq_clps_search.argtypes = [_p, _i64, _p, _p, _i64, _p, _i64, _i64, _i64, _i32, _f32, _i32, _p,
                                  ctypes.c_size_t, _p, _p, _p, _p]
+_lib.clq_w4a4_workspace_status.argtypes = [_p, ctypes.c_size_t, _p, _p]
+_lib.clq_debug_set.argtypes = [_i32, _i64]
+_lib.clq_w4a4_schedule.argtypes = [_i64, _i64, _i64, _i32, _p]
+_lib.clq_debug_get.argtypes = [_i32]
+_lib.clq_debug_get.restype = _i64
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
            "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
            "clq_quantize_weights8", "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8",
-           "clq_unswizzle_weights8", "clq_clps_search"):
+           "clq_unswizzle_weights8", "clq_clps_search", "clq_w4a4_workspace_status", "clq_debug_set",
+           "clq_w4a4_schedule"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -90,7 +96,10 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_obs_workspace_bytes", "clq_obs_channel_scores", "clq_obs_permutation",
            "clq_act8_bytes", "clq_weight8_bytes", "clq_rotate_quant_act8", "clq_quantize_weights8",
            "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8", "clq_unswizzle_weights8",
-           "clq_clps_workspace_bytes", "clq_clps_search")
+           "clq_clps_workspace_bytes", "clq_clps_search", "clq_w4a4_workspace_status",
+           "clq_debug_set", "clq_debug_get", "clq_w4a4_schedule")
+
+CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
 
 OBS_METRICS = ("absmax", "range", "par", "topk_mean", "percentile")
 
@@ -117,6 +126,25 @@ def _check(status, where):
 def _stream(stream):
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def clq_debug_set(knob, value):
+    """Sets a process-wide debug knob (CLQ_DEBUG_*)."""
+    _check(_lib.clq_debug_set(int(knob), int(value)), "clq_debug_set")
+
+
+def clq_debug_get(knob):
+    return int(_lib.clq_debug_get(int(knob)))
+
+
+def clq_w4a4_schedule(M, N, K, with_workspace=True):
+    """The GEMM schedule for an M x N x K product on the current device:
+    dict(kernel=0 persistent / 1 halves-128 / 2 halves-64, tiles, whole,
+    split_stages, grid)."""
+    info = (ctypes.c_int64 * 5)()
+    _check(_lib.clq_w4a4_schedule(M, N, K, 1 if with_workspace else 0, ctypes.cast(info, ctypes.c_void_p)),
+           "clq_w4a4_schedule")
+    return dict(kernel=info[0], tiles=info[1], whole=info[2], split_stages=info[3], grid=info[4])
 
 
 def _dev(t, name, dtype):
@@ -214,21 +242,50 @@ def clq_w4a4_workspace_bytes():
 _workspaces = {}
 
 
-def _workspace(device, workspace):
+def _workspace(device, workspace, stream=None):
     """The GEMM workspace: the caller's tensor, False for none, or (default)
-    one zero-filled buffer per device, allocated on first use.  Calls that
-    share it run in stream order; pass a tensor of your own per stream to
-    run GEMMs concurrently on several streams."""
+    one zero-filled buffer per (device, stream), allocated on first use and
+    zero-filled on that stream, so calls sharing it run in stream order and
+    calls on different streams never share one."""
     if workspace is False:
         return None, 0
     if workspace is None:
-        key = device.index if device.index is not None else torch.cuda.current_device()
-        workspace = _workspaces.get(key)
-        if workspace is None:
-            workspace = torch.zeros(clq_w4a4_workspace_bytes(), dtype=torch.uint8, device=device)
-            _workspaces[key] = workspace
+        workspace = default_workspace(device, stream)
     _dev(workspace, "workspace", torch.uint8)
     return workspace, workspace.numel()
+
+
+def default_workspace(device=None, stream=None):
+    """The default GEMM workspace of (device, stream) (the current stream if
+    None): created on first use, zero-filled on that stream."""
+    device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    idx = device.index if device.index is not None else torch.cuda.current_device()
+    s = torch.cuda.current_stream(idx) if stream is None else stream
+    key = (idx, s.cuda_stream)
+    ws = _workspaces.get(key)
+    if ws is None:
+        with torch.cuda.device(idx), torch.cuda.stream(s):
+            ws = torch.empty(clq_w4a4_workspace_bytes(), dtype=torch.uint8, device=device)
+            ws.zero_()   # a fill kernel on the stream that will use it
+        _workspaces[key] = ws
+    return ws
+
+
+def clq_w4a4_workspace_status(workspace=None, device=None, stream=None):
+    """The split-k status words of a GEMM workspace (the default one of
+    (device, stream) if None), as host ints [gave_up, first_tile, rank]:
+    gave_up == 0 means every split tile was summed completely.  Synchronises
+    with the stream."""
+    if workspace is None:
+        workspace = default_workspace(device, stream)
+    _dev(workspace, "workspace", torch.uint8)
+    s = torch.cuda.current_stream(workspace.device) if stream is None else stream
+    with torch.cuda.stream(s):
+        out = torch.empty(3, dtype=torch.int32, device=workspace.device)
+        _check(_lib.clq_w4a4_workspace_status(_ptr(workspace), workspace.numel(), _ptr(out),
+                                              ctypes.c_void_p(s.cuda_stream)), "clq_w4a4_workspace_status")
+        s.synchronize()
+        return [int(v) for v in out.cpu()]
 
 
 def _check_xq(Xq, x_scale, K):
@@ -256,7 +313,7 @@ def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None, workspace
     _dev(Y, "Y", torch.float16)
     if Y.dim() != 2 or Y.stride(1) != 1 or Y.shape != (M, qw.N):
         raise ValueError("Y must be 2-D [M, N] with unit column stride")
-    wsp, wsb = _workspace(Xq.device, workspace)
+    wsp, wsb = _workspace(Xq.device, workspace, stream)
     _check(_lib.clq_w4a4_linear(_ptr(Xq), _ptr(x_scale), _ptr(qw.wq), _ptr(qw.w_scale), _ptr(bias),
                                 M, qw.N, qw.K, _ptr(Y), Y.stride(0), _ptr(wsp), wsb, _stream(stream)),
            "clq_w4a4_linear")
@@ -271,7 +328,7 @@ def clq_w4a4_accum_i32(Xq, x_scale, qw, out=None, stream=None, workspace=None):
         out = torch.empty((M, (qw.N + 3) // 4 * 4), dtype=torch.int32, device=Xq.device)[:, :qw.N]
     acc = out
     _dev(acc, "acc", torch.int32)
-    wsp, wsb = _workspace(Xq.device, workspace)
+    wsp, wsb = _workspace(Xq.device, workspace, stream)
     _check(_lib.clq_w4a4_accum_i32(_ptr(Xq), _ptr(qw.wq), M, qw.N, qw.K, _ptr(acc), acc.stride(0),
                                    _ptr(wsp), wsb, _stream(stream)), "clq_w4a4_accum_i32")
     return acc

@@ -29,10 +29,7 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
-def build(extra_flags=(), out=LIB):
-    """Compile libclq.so; returns its path."""
-    tmp = out + ".tmp"
-    cmd = [HIPCC, *FLAGS, *extra_flags, *sources(), "-o", tmp]
+def _run(cmd):
     proc = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass does not know the packed-fp32 feature and says so: harmless
     noise = "'-packed-fp32-ops' is not a recognized feature for this target"
@@ -41,6 +38,23 @@ def build(extra_flags=(), out=LIB):
         raise RuntimeError(f"hipcc failed ({proc.returncode}):\n{err}")
     if err.strip():
         sys.stderr.write(err + "\n")
+
+
+def build(extra_flags=(), out=LIB):
+    """Compile libclq.so (one object per source, compiled in parallel, then
+    linked); returns its path."""
+    from concurrent.futures import ThreadPoolExecutor
+    objdir = os.path.join(HERE, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    srcs = sources()
+    objs = [os.path.join(objdir, os.path.basename(f) + ".o") for f in srcs]
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    jobs = min(len(srcs), max(1, min(os.cpu_count() or 1, 8)))
+    with ThreadPoolExecutor(jobs) as ex:
+        list(ex.map(lambda so: _run([HIPCC, *compile_flags, *extra_flags, "-c", so[0], "-o", so[1]]),
+                    zip(srcs, objs)))
+    tmp = out + ".tmp"
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, out)
     return out
 

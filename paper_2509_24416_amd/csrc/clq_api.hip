@@ -4,13 +4,16 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
+
+#include <atomic>
 
 #include "../../include/clq.h"
 #include "clq_internal.h"
 
 namespace {
 
-constexpr int kVersion = 6;
+constexpr int kVersion = 7;
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxRows = 2147483647;
 
@@ -32,7 +35,32 @@ clq_status check_rows(int64_t R) {
     return CLQ_OK;
 }
 
-clq_status from_hip(hipError_t e) { return e == hipSuccess ? CLQ_OK : CLQ_ERR_HIP; }
+// Debug knobs (process-wide host state).  CLQ_DEBUG_SYNC starts from the
+// CLQ_SYNC environment variable.
+std::atomic<int> debug_sync{-1};
+
+bool sync_mode() {
+    int v = debug_sync.load(std::memory_order_relaxed);
+    if (v < 0) {
+        const char *e = getenv("CLQ_SYNC");
+        v = (e != nullptr && e[0] != '\0' && e[0] != '0') ? 1 : 0;
+        int expect = -1;
+        debug_sync.compare_exchange_strong(expect, v);
+        v = debug_sync.load(std::memory_order_relaxed);
+    }
+    return v != 0;
+}
+
+// The status of an enqueued launch; in sync mode the stream is drained first,
+// so that a kernel's own failure is reported by the call that launched it.
+clq_status done(hipStream_t stream, hipError_t e) {
+    if (e != hipSuccess) return CLQ_ERR_HIP;
+    if (sync_mode()) {
+        if (hipStreamSynchronize(stream) != hipSuccess) return CLQ_ERR_HIP;
+        if (hipGetLastError() != hipSuccess) return CLQ_ERR_HIP;
+    }
+    return CLQ_OK;
+}
 
 }  // namespace
 
@@ -74,7 +102,7 @@ clq_status clq_quantize_weights(const void *W, const int32_t *perm, int64_t N, i
     if (!(clip_ratio >= 0x1p-24f && clip_ratio <= 1.0f)) return CLQ_ERR_ARG;
     if (!aligned(W, 16) || !aligned(Wq, 16) || !aligned(w_scale, 4) || (perm && !aligned(perm, 4)))
         return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_rotate_quant(
+    return done(stream, clq::launch_rotate_quant(
         static_cast<const uint16_t *>(W), K, perm, N, clq::padded_rows(N), (int)K, block,
         clip_ratio, true, 1.0f / (float)block, static_cast<uint8_t *>(Wq), w_scale, stream));
 }
@@ -89,7 +117,7 @@ clq_status clq_rotate_quant_act(const void *X, int64_t ldx, const int32_t *perm,
     if (ldx < K || ldx % 8 != 0) return CLQ_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(Xq, 16) || !aligned(x_scale, 4) || (perm && !aligned(perm, 4)))
         return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_rotate_quant(static_cast<const uint16_t *>(X), ldx, perm, M,
+    return done(stream, clq::launch_rotate_quant(static_cast<const uint16_t *>(X), ldx, perm, M,
                                              clq::padded_act_rows(M), (int)K, block, 1.0f, false,
                                              1.0f, static_cast<uint8_t *>(Xq), x_scale, stream));
 }
@@ -114,6 +142,54 @@ static clq_status check_workspace(const void *workspace, size_t workspace_bytes)
 
 size_t clq_w4a4_workspace_bytes(void) { return clq::gemm_workspace_bytes(); }
 
+clq_status clq_w4a4_workspace_status(const void *workspace, size_t workspace_bytes, int32_t *status,
+                                     hipStream_t stream) {
+    if (!workspace || !status) return CLQ_ERR_NULL;
+    if (workspace_bytes < clq::gemm_workspace_bytes()) return CLQ_ERR_WORKSPACE;
+    if (!aligned(workspace, 16) || !aligned(status, 4)) return CLQ_ERR_ALIGN;
+    return done(stream, hipMemcpyAsync(status, workspace, 3 * sizeof(int32_t), hipMemcpyDeviceToDevice, stream));
+}
+
+clq_status clq_w4a4_schedule(int64_t M, int64_t N, int64_t K, int32_t with_workspace, int64_t *info) {
+    if (!info) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    const clq::GemmPlan p = clq::plan_gemm(M, N, (int)K, with_workspace != 0);
+    info[0] = p.kernel;
+    info[1] = p.tiles;
+    info[2] = p.dp;
+    info[3] = p.sk;
+    info[4] = p.grid;
+    return CLQ_OK;
+}
+
+clq_status clq_debug_set(int32_t knob, int64_t value) {
+    switch (knob) {
+        case CLQ_DEBUG_SYNC:
+            if (value != 0 && value != 1) return CLQ_ERR_ARG;
+            debug_sync.store((int)value, std::memory_order_relaxed);
+            return CLQ_OK;
+        case CLQ_DEBUG_SPLIT_SPIN_LIMIT:
+            if (value < 0 || value > (1 << 30)) return CLQ_ERR_ARG;
+            __atomic_store_n(&clq::gemm_spin_limit, (int)value, __ATOMIC_RELAXED);
+            return CLQ_OK;
+        case CLQ_DEBUG_SPLIT_DROP_SIGNAL:
+            if (value != 0 && value != 1) return CLQ_ERR_ARG;
+            __atomic_store_n(&clq::gemm_drop_signal, (int)value, __ATOMIC_RELAXED);
+            return CLQ_OK;
+    }
+    return CLQ_ERR_ARG;
+}
+
+int64_t clq_debug_get(int32_t knob) {
+    switch (knob) {
+        case CLQ_DEBUG_SYNC: return sync_mode() ? 1 : 0;
+        case CLQ_DEBUG_SPLIT_SPIN_LIMIT: return __atomic_load_n(&clq::gemm_spin_limit, __ATOMIC_RELAXED);
+        case CLQ_DEBUG_SPLIT_DROP_SIGNAL: return __atomic_load_n(&clq::gemm_drop_signal, __ATOMIC_RELAXED);
+    }
+    return -1;
+}
+
 clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
                            const float *w_scale, const void *bias, int64_t M, int64_t N,
                            int64_t K, void *Y, int64_t ldy, void *workspace,
@@ -124,7 +200,7 @@ clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
     if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2)))
         return CLQ_ERR_ALIGN;
     if ((s = check_workspace(workspace, workspace_bytes)) != CLQ_OK) return s;
-    return from_hip(clq::launch_gemm(static_cast<const uint8_t *>(Xq), x_scale,
+    return done(stream, clq::launch_gemm(static_cast<const uint8_t *>(Xq), x_scale,
                                      static_cast<const uint8_t *>(Wq), w_scale,
                                      static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy,
                                      false, workspace, stream));
@@ -136,7 +212,7 @@ clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M, int64_t
     clq_status s = check_gemm(Xq, Wq, M, N, K, acc, ldacc, 4);
     if (s != CLQ_OK) return s;
     if ((s = check_workspace(workspace, workspace_bytes)) != CLQ_OK) return s;
-    return from_hip(clq::launch_gemm(static_cast<const uint8_t *>(Xq), nullptr,
+    return done(stream, clq::launch_gemm(static_cast<const uint8_t *>(Xq), nullptr,
                                      static_cast<const uint8_t *>(Wq), nullptr, nullptr, M, N,
                                      (int)K, acc, ldacc, true, workspace, stream));
 }
@@ -147,7 +223,7 @@ clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K, void *Wq_
     clq_status s;
     if ((s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
     if (!aligned(Wq, 16) || !aligned(Wq_canonical, 8)) return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_unswizzle(static_cast<const uint8_t *>(Wq), N, (int)K,
+    return done(stream, clq::launch_unswizzle(static_cast<const uint8_t *>(Wq), N, (int)K,
                                           static_cast<uint8_t *>(Wq_canonical), stream));
 }
 
@@ -157,7 +233,7 @@ clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K, void *Xq_cano
     clq_status s;
     if ((s = check_rows(M)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
     if (!aligned(Xq, 16) || !aligned(Xq_canonical, 16)) return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_unswizzle_act(static_cast<const uint8_t *>(Xq), M, (int)K,
+    return done(stream, clq::launch_unswizzle_act(static_cast<const uint8_t *>(Xq), M, (int)K,
                                               static_cast<uint8_t *>(Xq_canonical), stream));
 }
 
@@ -177,7 +253,7 @@ clq_status clq_obs_channel_scores(const void *X, int64_t ldx, int64_t B, int64_t
     if (ldx < D || ldx % 8 != 0) return CLQ_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(workspace, 16) || !aligned(scores, 4)) return CLQ_ERR_ALIGN;
     if (workspace_bytes < clq::obs_workspace_bytes(N, D, metric)) return CLQ_ERR_WORKSPACE;
-    return from_hip(clq::launch_obs_scores(static_cast<const uint16_t *>(X), ldx, B, N, (int)D, metric,
+    return done(stream, clq::launch_obs_scores(static_cast<const uint16_t *>(X), ldx, B, N, (int)D, metric,
                                            workspace, scores, stream));
 }
 
@@ -185,7 +261,7 @@ clq_status clq_obs_permutation(const float *scores, int64_t D, int32_t *perm, hi
     if (!scores || !perm) return CLQ_ERR_NULL;
     if (D < 2 || D > 65536 || D % 2 != 0) return CLQ_ERR_SHAPE;
     if (!aligned(scores, 4) || !aligned(perm, 4)) return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_obs_permutation(scores, (int)D, perm, stream));
+    return done(stream, clq::launch_obs_permutation(scores, (int)D, perm, stream));
 }
 
 /* ---- 8-bit activations (W4A8, W8A8) -------------------------------------- */
@@ -210,7 +286,7 @@ clq_status clq_rotate_quant_act8(const void *X, int64_t ldx, const int32_t *perm
     if (ldx < K || ldx % 8 != 0) return CLQ_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(Xq8, 16) || !aligned(x_scale, 4) || (perm && !aligned(perm, 4)))
         return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_rotate_quant(
+    return done(stream, clq::launch_rotate_quant(
         static_cast<const uint16_t *>(X), ldx, perm, M, clq::padded_act_rows(M), (int)K, block, 1.0f,
         false, 1.0f, static_cast<uint8_t *>(Xq8), x_scale, stream, 8));
 }
@@ -225,7 +301,7 @@ clq_status clq_quantize_weights8(const void *W, const int32_t *perm, int64_t N, 
     if (!(clip_ratio >= 0x1p-24f && clip_ratio <= 1.0f)) return CLQ_ERR_ARG;
     if (!aligned(W, 16) || !aligned(Wq8, 16) || !aligned(w_scale, 4) || (perm && !aligned(perm, 4)))
         return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_rotate_quant(
+    return done(stream, clq::launch_rotate_quant(
         static_cast<const uint16_t *>(W), K, perm, N, clq::padded_rows(N), (int)K, block, clip_ratio,
         true, 1.0f / (float)block, static_cast<uint8_t *>(Wq8), w_scale, stream, 8));
 }
@@ -248,7 +324,7 @@ clq_status clq_a8_linear(const void *Xq8, const float *x_scale, const void *Wq, 
     clq_status s = check_a8(Xq8, Wq, wbits, M, N, K, Y, ldy, 8);
     if (s != CLQ_OK) return s;
     if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2))) return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_a8_gemm(static_cast<const uint8_t *>(Xq8), x_scale,
+    return done(stream, clq::launch_a8_gemm(static_cast<const uint8_t *>(Xq8), x_scale,
                                         static_cast<const uint8_t *>(Wq), wbits, w_scale,
                                         static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy, false,
                                         stream));
@@ -258,7 +334,7 @@ clq_status clq_a8_accum_i32(const void *Xq8, const void *Wq, int32_t wbits, int6
                             int64_t K, int32_t *acc, int64_t ldacc, hipStream_t stream) {
     clq_status s = check_a8(Xq8, Wq, wbits, M, N, K, acc, ldacc, 4);
     if (s != CLQ_OK) return s;
-    return from_hip(clq::launch_a8_gemm(static_cast<const uint8_t *>(Xq8), nullptr,
+    return done(stream, clq::launch_a8_gemm(static_cast<const uint8_t *>(Xq8), nullptr,
                                         static_cast<const uint8_t *>(Wq), wbits, nullptr, nullptr, M, N,
                                         (int)K, acc, ldacc, true, stream));
 }
@@ -268,7 +344,7 @@ clq_status clq_unswizzle_act8(const void *Xq8, int64_t M, int64_t K, void *codes
     clq_status s;
     if ((s = check_rows(M)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
     if (!aligned(Xq8, 16)) return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_unswizzle8(static_cast<const uint8_t *>(Xq8), M, (int)K, false,
+    return done(stream, clq::launch_unswizzle8(static_cast<const uint8_t *>(Xq8), M, (int)K, false,
                                            static_cast<int8_t *>(codes), stream));
 }
 
@@ -277,7 +353,7 @@ clq_status clq_unswizzle_weights8(const void *Wq8, int64_t N, int64_t K, void *c
     clq_status s;
     if ((s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
     if (!aligned(Wq8, 16)) return CLQ_ERR_ALIGN;
-    return from_hip(clq::launch_unswizzle8(static_cast<const uint8_t *>(Wq8), N, (int)K, true,
+    return done(stream, clq::launch_unswizzle8(static_cast<const uint8_t *>(Wq8), N, (int)K, true,
                                            static_cast<int8_t *>(codes), stream));
 }
 
@@ -305,7 +381,7 @@ clq_status clq_clps_search(const void *X, int64_t ldx, const void *W, const floa
     if (workspace_bytes < clq::clps_workspace_bytes(M, N, K)) return CLQ_ERR_WORKSPACE;
     // l = floor(gamma (K - 1)) weights above the order statistic
     const int l = (int)floor((double)gamma * (double)(K - 1));
-    return from_hip(clq::launch_clps(static_cast<const uint16_t *>(X), ldx, static_cast<const uint16_t *>(W), Y0,
+    return done(stream, clq::launch_clps(static_cast<const uint16_t *>(X), ldx, static_cast<const uint16_t *>(W), Y0,
                                      ldy0, perm, M, N, (int)K, block, (int)(K - 1 - l), grid, workspace, alphas,
                                      errors, best, stream));
 }

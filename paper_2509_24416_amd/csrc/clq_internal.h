@@ -109,8 +109,24 @@ hipError_t launch_unswizzle_act(const uint8_t *Xq, int64_t M, int K, uint8_t *ou
                                 hipStream_t stream);
 
 // Workspace for the split-k schedule of launch_gemm (bytes; depends on the
-// device's compute-unit count only).
+// device's compute-unit count only).  Its first 256 bytes hold the split-k
+// status words: [0] waits that gave up, [1] the first such tile, [2] its
+// contributor's rank.
 size_t gemm_workspace_bytes();
+
+// Split-k wait bound (sleeps) and the test-only switch that stops
+// contributors from signalling; read at each launch.
+extern int gemm_spin_limit;
+extern int gemm_drop_signal;
+
+// The W4A4 GEMM's schedule for a shape.  kernel: 0 the persistent kernel
+// (256-token tiles), 1 / 2 the two-halves kernel with 128- / 64-token tiles;
+// tiles: output tiles; dp: tiles computed whole (the persistent kernel's
+// first rounds); sk: k-stages split over the grid; grid: workgroups.
+struct GemmPlan {
+    int kernel, tiles_m, tiles, dp, sk, grid;
+};
+GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split);
 
 // workspace: gemm_workspace_bytes() zero-filled bytes, or nullptr (whole
 // tiles only).  Calls that share a workspace must not overlap in time.

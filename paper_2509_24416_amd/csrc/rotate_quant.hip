@@ -688,7 +688,11 @@ hipError_t launch_rq_act_g(const uint16_t *X, int64_t ldx, const int32_t *perm, 
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
     }
-    if ((int64_t)R * ldx > INT32_MAX)   // 32-bit in-batch offsets: very wide strides take the one-shot kernel
+    // The one-shot kernel (up to 1024 lanes and 64 KB of staged row) takes
+    // what this kernel's launch cannot: very wide strides (32-bit in-batch
+    // offsets), rows of more than 256 blocks (b = 32, K > 8192) and rows
+    // whose two staged copies exceed the LDS limit (K > 16384).
+    if ((int64_t)R * ldx > INT32_MAX || R * nb > 256 || lds > 65536 + 4096)
         return launch_rq<B, false, QB>(X, ldx, perm, rows_valid, rows_alloc, K, 1.0f, 1.0f, out, scale, stream);
     if constexpr (B == 64) if (use_rows8<B>(K) && (int64_t)8 * ldx <= INT32_MAX) {
         static bool attr8 = false;

@@ -98,6 +98,10 @@ __device__ __forceinline__ v4i widen16(uint32_t d0, uint32_t d1) {
 constexpr int kStages = 5;   // ring depth
 constexpr int kGroupM = 4;          // token panels per tile group (L2 reuse of channel panels)
 constexpr int kSpinLimit = 1 << 22;  // bound on a split-tile wait (about a second)
+// Split-k status words at the head of the workspace: [0] the number of waves
+// whose wait for a contributor's partial gave up, [1] the first such tile,
+// [2] its contributor's rank (see launch_gemm)
+constexpr int kStatusBytes = 256;
 
 template <int WN_, int WM_, int FN_, int FM_, int WGS_>
 struct Tile {
@@ -135,6 +139,9 @@ struct GemmArgs {
     int sk;        // k-stages of the remaining tiles, split evenly over the grid
     int32_t *part; // partial accumulators, one tile per workgroup
     int *flags;    // one per wave of every workgroup
+    int *status;   // split-k status words (kStatusBytes at the workspace head)
+    int spin_limit;   // bound on a wait for a contributor's flag (sleeps)
+    int drop_signal;  // test only: contributors never raise their flags
     // squared-error mode: target Y0 fp32 [M][ldy0]; one fp64 partial per
     // wave of every tile, at errp[tile * waves + wave]
     const float *y0;
@@ -381,16 +388,32 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
                     : "memory");
             }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __hip_atomic_store(a.flags + rank * C::NW + wave, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (!a.drop_signal)
+            __hip_atomic_store(a.flags + rank * C::NW + wave, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     };
     // Partials are read two contributors at a time (16 loads in flight per
     // wave), so a tile split many ways pays half as many memory round trips.
-    auto wait_flag = [&](int r2) {
+    // The wait is bounded: all workgroups of the grid are meant to be
+    // resident at once, but nothing stops other kernels from holding compute
+    // units.  A wait that gives up leaves that contributor's partial out of
+    // the sum (its flag may still rise later and is not cleared), and records
+    // the failure in the status words for the host: the call's output is then
+    // invalid and the workspace must be zero-filled again before reuse.
+    auto wait_flag = [&](int L, int r2) -> bool {
         int *fl = a.flags + r2 * C::NW + wave;
-        for (int spin = 0; spin < kSpinLimit; ++spin) {
-            if (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
+        for (int spin = 0; spin < a.spin_limit; ++spin) {
+            if (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return true;
             __builtin_amdgcn_s_sleep(8);
         }
+        if (__hip_atomic_load(fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return true;
+        if (lane == 0) {
+            const int old = __hip_atomic_fetch_add(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (old == 0) {
+                __hip_atomic_store(a.status + 1, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(a.status + 2, r2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        return false;
     };
     auto part_base = [&](int r2) -> const uint8_t * {
         uint32_t lo = (uint32_t)lane * 16;
@@ -470,7 +493,7 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
             if (st >= end) break;
             const int en = (r2 + 1) * S / G;
             if (en <= st || st <= beg) continue;
-            wait_flag(r2);
+            if (!wait_flag(L, r2)) continue;   // not added; its flag is left as it is
             if (pending < 0) {
                 pending = r2;
                 continue;
@@ -1038,35 +1061,75 @@ hipError_t launch_halves(const GemmArgs &g, bool i32out, bool bias, bool rag, hi
     return hipGetLastError();
 }
 
-template <class C, bool I32OUT, bool RAGGED, bool BIAS, bool ERR = false>
-hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
-    const int ntiles = g.tiles_m * g.tiles_n, nks = g.K >> 6;
-    int grid = full_grid();
-    g.dp = ntiles;
-    g.sk = 0;
+// The persistent kernel's schedule: whole tiles for all but the last one or
+// two rounds; when that fills the chip badly (and a workspace is given) the
+// rest is spread over every workgroup in k-stage units (1 to 2 tiles each).
+void plan_persistent(int ntiles, int nks, bool may_split, int &dp, int &sk, int &grid) {
+    grid = full_grid();
+    dp = ntiles;
+    sk = 0;
     if (may_split && ntiles % grid != 0) {
-        // whole tiles for all but the last one or two rounds; the rest is
-        // spread over every workgroup in k-stage units (1 to 2 tiles each)
-        const int dp = max(0, ntiles / grid - 1) * grid;
+        const int d = max(0, ntiles / grid - 1) * grid;
         const int64_t whole = (int64_t)((ntiles + grid - 1) / grid) * nks;
-        const int64_t split = (int64_t)(dp / grid) * nks + ((int64_t)(ntiles - dp) * nks + grid - 1) / grid;
-        const bool share_ok = (int64_t)(ntiles - dp) * nks >= (int64_t)kSplitMinShare * grid;
+        const int64_t split = (int64_t)(d / grid) * nks + ((int64_t)(ntiles - d) * nks + grid - 1) / grid;
+        const bool share_ok = (int64_t)(ntiles - d) * nks >= (int64_t)kSplitMinShare * grid;
         if (share_ok && whole - split > kSplitMinSaved && 6 * (whole - split) > whole) {
-            g.dp = dp;
-            g.sk = (ntiles - dp) * nks;
+            dp = d;
+            sk = (ntiles - d) * nks;
         }
     }
-    if (g.sk == 0) grid = max(8, (min(ntiles, grid) + 7) / 8 * 8);
+    if (sk == 0) grid = max(8, (min(ntiles, grid) + 7) / 8 * 8);
+}
+
+template <class C, bool I32OUT, bool RAGGED, bool BIAS, bool ERR = false>
+hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
+    int grid;
+    plan_persistent(g.tiles_m * g.tiles_n, g.K >> 6, may_split, g.dp, g.sk, grid);
     hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS, ERR>), dim3((unsigned)grid), dim3(C::NT), 0, stream, g);
     return hipGetLastError();
 }
 
 }  // namespace
 
+GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split) {
+    GemmPlan p{};
+    const int tiles_n = (int)((N + TCfg::BN - 1) / TCfg::BN);
+    const int ntiles = (int)((M + TCfg::BM - 1) / TCfg::BM) * tiles_n;
+    // at most 1.25 256-token tiles per compute unit and a k loop worth
+    // halving: the two-halves kernel.  Just past one tile per CU the
+    // persistent kernel doubles up on a few CUs while the rest idle; the
+    // two-halves kernel fills one round of two workgroups per CU and runs a
+    // short second round on the remaining quarter at most.
+    if (4 * ntiles <= 5 * device_cus() && (K >> 6) >= kHalvesMinStages) {
+        // 128-token tiles (two four-wave workgroups per compute unit), or 64
+        // while those would fill at most half the compute units
+        const int tm128 = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
+        if (2 * tm128 * tiles_n <= device_cus()) {
+            p.kernel = 2;
+            p.tiles_m = (int)((M + TileHalf64::BM - 1) / TileHalf64::BM);
+        } else {
+            p.kernel = 1;
+            p.tiles_m = tm128;
+        }
+        p.tiles = p.tiles_m * tiles_n;
+        p.dp = p.tiles;
+        p.grid = p.tiles;
+        return p;
+    }
+    p.kernel = 0;
+    p.tiles_m = (int)((M + TCfg::BM - 1) / TCfg::BM);
+    p.tiles = ntiles;
+    plan_persistent(ntiles, K >> 6, may_split, p.dp, p.sk, p.grid);
+    return p;
+}
+
 size_t gemm_workspace_bytes() {
     const size_t G = (size_t)full_grid();
-    return G * TCfg::NW * sizeof(int) + G * TCfg::PART_INTS * sizeof(int32_t);
+    return kStatusBytes + G * TCfg::NW * sizeof(int) + G * TCfg::PART_INTS * sizeof(int32_t);
 }
+
+int gemm_spin_limit = kSpinLimit;
+int gemm_drop_signal = 0;
 
 hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
                        const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
@@ -1085,25 +1148,22 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
     g.tiles_m = (int)((M + TCfg::BM - 1) / TCfg::BM);
     g.tiles_n = (int)((N + TCfg::BN - 1) / TCfg::BN);
     const size_t G = (size_t)full_grid();
-    g.flags = reinterpret_cast<int *>(workspace);
-    g.part = workspace ? reinterpret_cast<int32_t *>(reinterpret_cast<uint8_t *>(workspace) + G * TCfg::NW * sizeof(int))
-                       : nullptr;
+    // workspace: status words | one flag per wave of every workgroup | one
+    // partial tile per workgroup
+    uint8_t *wsb = reinterpret_cast<uint8_t *>(workspace);
+    g.status = workspace ? reinterpret_cast<int *>(wsb) : nullptr;
+    g.flags = workspace ? reinterpret_cast<int *>(wsb + kStatusBytes) : nullptr;
+    g.part = workspace ? reinterpret_cast<int32_t *>(wsb + kStatusBytes + G * TCfg::NW * sizeof(int)) : nullptr;
+    g.spin_limit = __atomic_load_n(&gemm_spin_limit, __ATOMIC_RELAXED);
+    g.drop_signal = __atomic_load_n(&gemm_drop_signal, __ATOMIC_RELAXED);
     const bool may_split = workspace != nullptr;
-    // at most 1.25 256-token tiles per compute unit and a k loop worth
-    // halving: the two-halves kernel.  Just past one tile per CU the
-    // persistent kernel doubles up on a few CUs while the rest idle; the
-    // two-halves kernel fills one round of two workgroups per CU and runs a
-    // short second round on the remaining quarter at most.
-    const int ntiles = g.tiles_m * g.tiles_n;
-    if (4 * ntiles <= 5 * device_cus() && (K >> 6) >= kHalvesMinStages) {
-        // 128-token tiles (two four-wave workgroups per compute unit), or 64
-        // while those would fill at most half the compute units
-        const int tm128 = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
-        if (2 * tm128 * g.tiles_n <= device_cus()) {
-            g.tiles_m = (int)((M + TileHalf64::BM - 1) / TileHalf64::BM);
-            return launch_halves<TileHalf64>(g, i32out, bias != nullptr, N % 16 != 0, stream);
-        }
-        g.tiles_m = tm128;
+    const GemmPlan pl = plan_gemm(M, N, K, may_split);
+    if (pl.kernel == 2) {
+        g.tiles_m = pl.tiles_m;
+        return launch_halves<TileHalf64>(g, i32out, bias != nullptr, N % 16 != 0, stream);
+    }
+    if (pl.kernel == 1) {
+        g.tiles_m = pl.tiles_m;
         return launch_halves<TileHalf128>(g, i32out, bias != nullptr, N % 16 != 0, stream);
     }
     // ragged channel edges, and biases not 4-byte aligned (the fast path

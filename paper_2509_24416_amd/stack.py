@@ -24,7 +24,8 @@ each.
 """
 import torch
 
-from . import (clq_act_bytes, clq_quantize_weights, clq_rotate_quant_act, clq_w4a4_linear)
+from . import (clq_act_bytes, clq_quantize_weights, clq_rotate_quant_act, clq_w4a4_linear,
+               clq_w4a4_workspace_bytes)
 
 LAYERS = ("qkv", "proj", "fc1", "fc2")
 
@@ -84,6 +85,9 @@ class DiTStack:
         self.xq = {h: torch.empty(clq_act_bytes(M, h), dtype=torch.uint8, device=dev),
                    f: torch.empty(clq_act_bytes(M, f), dtype=torch.uint8, device=dev)}
         self.xs = torch.empty(M, dtype=torch.float32, device=dev)
+        # the GEMM workspace of this stack: every launch (eager or replayed)
+        # runs in the order of one stream, so one is enough
+        self.ws = torch.zeros(clq_w4a4_workspace_bytes(), dtype=torch.uint8, device=dev)
         self.graph = None
 
     @staticmethod
@@ -109,7 +113,7 @@ class DiTStack:
                 x = self._input(j, name)
                 xq = self.xq[qw.K]
                 clq_rotate_quant_act(x, self.block, perm=self.gather[j][name], out=xq, scale_out=self.xs)
-                clq_w4a4_linear(xq, self.xs, qw, b, out=self.out[name])
+                clq_w4a4_linear(xq, self.xs, qw, b, out=self.out[name], workspace=self.ws)
                 if taps is not None and (j, name) in taps:
                     taps[(j, name)] = (x.clone(), self.out[name].clone())
 

@@ -63,12 +63,17 @@ def lib():
     L.clq_clps_workspace_bytes.argtypes = [i64, i64, i64]
     L.clq_clps_search.argtypes = [p, i64, p, p, i64, p, i64, i64, i64, i32, f32, i32, p, ctypes.c_size_t,
                                   p, p, p, p]
+    L.clq_w4a4_workspace_status.argtypes = [p, ctypes.c_size_t, p, p]
+    L.clq_debug_set.argtypes = [i32, i64]
+    L.clq_debug_get.argtypes = [i32]
+    L.clq_debug_get.restype = i64
+    L.clq_w4a4_schedule.argtypes = [i64, i64, i64, i32, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 24, names
+    assert len(names) == 28, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -80,7 +85,7 @@ def test_binding_names_match_header():
 
 
 def test_version_and_strings(lib):
-    assert lib.clq_version() == 6
+    assert lib.clq_version() == 7
     for code in range(8):
         s = lib.clq_status_string(code).decode()
         assert s.startswith("CLQ")
@@ -174,9 +179,71 @@ def test_linear_validation(lib):
 def test_workspace_bytes(lib):
     # one partial tile (128 x 256 int32) and four flags per workgroup, two
     # workgroups per compute unit, the grid a multiple of 8
-    n = lib.clq_w4a4_workspace_bytes()
+    # 256 bytes of status words, then one partial tile (128 x 256 int32) and
+    # four flags per workgroup, two workgroups per compute unit, the grid a
+    # multiple of 8
+    n = lib.clq_w4a4_workspace_bytes() - 256
     per_wg = 128 * 256 * 4 + 4 * 4
     assert n % per_wg == 0 and (n // per_wg) % 8 == 0
+
+
+def test_workspace_status_validation(lib):
+    need = lib.clq_w4a4_workspace_bytes()
+    assert lib.clq_w4a4_workspace_status(None, need, A, None) == NULL
+    assert lib.clq_w4a4_workspace_status(A, need, None, None) == NULL
+    assert lib.clq_w4a4_workspace_status(A, need - 1, A, None) == WORKSPACE
+    assert lib.clq_w4a4_workspace_status(A + 8, need, A, None) == ALIGN
+    assert lib.clq_w4a4_workspace_status(A, need, A + 2, None) == ALIGN
+
+
+def schedule(lib, M, N, K, ws=1):
+    info = (ctypes.c_int64 * 5)()
+    assert lib.clq_w4a4_schedule(M, N, K, ws, ctypes.cast(info, ctypes.c_void_p)) == OK
+    return list(info)
+
+
+def test_schedule(lib):
+    # host planning only (no device here: 256 compute units assumed, 512
+    # persistent workgroups)
+    info = (ctypes.c_int64 * 5)()
+    assert lib.clq_w4a4_schedule(0, 8, 64, 1, ctypes.cast(info, ctypes.c_void_p)) == SHAPE
+    assert lib.clq_w4a4_schedule(8, 8, 96, 1, ctypes.cast(info, ctypes.c_void_p)) == SHAPE
+    assert lib.clq_w4a4_schedule(8, 8, 64, 1, None) == NULL
+    # 17 x 16 tiles of 256 tokens (<= 1.25 per CU): two halves, 128-token tiles
+    assert schedule(lib, 4352, 2048, 2432)[:2] == [1, 34 * 16]
+    # few tiles: 64-token tiles
+    assert schedule(lib, 1024, 1152, 1152)[:2] == [2, 16 * 9]
+    # the 28-block stack's fc2 at 16384 tokens: 576 tiles, every k-stage split
+    k, tiles, dp, sk, grid = schedule(lib, 16384, 1152, 4608)
+    assert (k, tiles, dp, sk, grid) == (0, 576, 0, 576 * 72, 512)
+    assert schedule(lib, 16384, 1152, 4608, ws=0) == [0, 576, 576, 0, 512]
+    # 600 tiles of 24 stages: both rounds split, 28.1 stages per workgroup
+    assert schedule(lib, 6400, 3072, 1536) == [0, 600, 0, 600 * 24, 512]
+    # 1100 tiles: one whole round first, the last 588 tiles split
+    assert schedule(lib, 11264, 3200, 1536) == [0, 1100, 512, 588 * 24, 512]
+    # the PixArt block linears (M = 8192) and the video ones (M = 43200)
+    # take whole tiles on the persistent grid
+    for M, N, K in ((8192, 3456, 1152), (8192, 4608, 1152), (43200, 3456, 1152), (43200, 1152, 4608)):
+        k, tiles, dp, sk, grid = schedule(lib, M, N, K)
+        assert k == 0 and sk == 0 and dp == tiles
+
+
+def test_debug_knobs(lib):
+    SYNC, SPIN, DROP = 0, 1, 2
+    assert lib.clq_debug_get(SPIN) == 1 << 22 and lib.clq_debug_get(DROP) == 0
+    assert lib.clq_debug_get(7) == -1
+    assert lib.clq_debug_set(7, 0) == ARG
+    assert lib.clq_debug_set(SYNC, 2) == ARG and lib.clq_debug_set(DROP, -1) == ARG
+    assert lib.clq_debug_set(SPIN, -1) == ARG and lib.clq_debug_set(SPIN, (1 << 30) + 1) == ARG
+    try:
+        assert lib.clq_debug_set(SPIN, 5) == OK and lib.clq_debug_get(SPIN) == 5
+        assert lib.clq_debug_set(DROP, 1) == OK and lib.clq_debug_get(DROP) == 1
+        assert lib.clq_debug_set(SYNC, 1) == OK and lib.clq_debug_get(SYNC) == 1
+    finally:
+        assert lib.clq_debug_set(SPIN, 1 << 22) == OK
+        assert lib.clq_debug_set(DROP, 0) == OK
+        assert lib.clq_debug_set(SYNC, 0) == OK
+    assert lib.clq_debug_get(SYNC) == 0
 
 
 def test_accum_and_unswizzle_validation(lib):

@@ -43,15 +43,29 @@ def host(t):
     return t.cpu().numpy()
 
 
+_HOST_W = {}
+
+
+def stack_weights(nblocks, M, block):
+    """Host weights and biases of the stack's linears (they do not depend on
+    M or the block size; drawn once per process)."""
+    wl = workloads.dit_stack(nblocks, M, block)
+    host_w = {}
+    for l in wl.layers:
+        if l.name not in _HOST_W:
+            _HOST_W[l.name] = (workloads.weights(l.N, l.K, l.seed + 1), workloads.bias(l.N, l.seed + 2))
+        host_w[l.name] = _HOST_W[l.name]
+    return wl, host_w
+
+
 def build(nblocks, M, block):
     from paper_2509_24416_amd.stack import DiTStack
-    wl = workloads.dit_stack(nblocks, M, block)
-    weights, host_w = [], {}
+    wl, host_w = stack_weights(nblocks, M, block)
+    weights = []
     for j in range(nblocks):
         blk = {}
         for l in wl.layers[4 * j:4 * j + 4]:
-            W, b = workloads.weights(l.N, l.K, l.seed + 1), workloads.bias(l.N, l.seed + 2)
-            host_w[l.name] = (W, b)
+            W, b = host_w[l.name]
             blk[l.name.split(".")[1]] = (dev(W), dev(b))
         weights.append(blk)
     x = workloads.activations(M, wl.layers[0].K, "L1", wl.layers[0].seed)
@@ -71,6 +85,33 @@ def test_layers_match_oracle_on_their_inputs(clq, M, block):
         assert np.isfinite(xin_h.astype(np.float32)).all()
         r = oracle.linear(xin_h, W, b, block)
         assert oracle.err_metric(host(y)[rows].astype(np.float64), r["y64"], r["p64"], b) <= TOL, (j, name)
+
+
+@pytest.mark.parametrize("block", [32, 64, 128])
+def test_full_depth_stack_layers_match_oracle(clq, block):
+    # the 28-block stack (112 linears) at M = 4096: every linear of blocks 0,
+    # 13 and 27 against the oracle on that linear's actual fp16 input, on
+    # sampled token rows -- activation codes and scales bit for bit, the fp16
+    # output within the tolerance
+    M, nb = 4096, 28
+    st, host_w, x = build(nb, M, block)
+    taps = {(j, n): None for j in (0, 13, 27) for n in ("qkv", "proj", "fc1", "fc2")}
+    st.forward(dev(x), taps=taps)
+    rng = np.random.default_rng(block)
+    rows = np.unique(np.concatenate([[0, 1, M - 1], rng.choice(M, 13, replace=False)]))
+    rows_t = torch.from_numpy(rows).cuda()
+    for (j, name), (xin, y) in taps.items():
+        W, b = host_w[f"blk{j}.{name}"]
+        xin_h = host(xin)[rows]
+        assert np.isfinite(xin_h.astype(np.float32)).all(), (j, name)
+        r = oracle.linear(xin_h, W, b, block)
+        Xq, xs = clq.clq_rotate_quant_act(xin, block)
+        K = xin.shape[1]
+        assert np.array_equal(host(xs)[rows], r["x_scale"]), (j, name)
+        assert np.array_equal(host(clq.clq_unswizzle_act(Xq, M, K)[rows_t]), r["xq"]), (j, name)
+        assert oracle.err_metric(host(y)[rows].astype(np.float64), r["y64"], r["p64"], b) <= TOL, (j, name)
+    del st
+    torch.cuda.empty_cache()
 
 
 def test_graph_replays_match_eager(clq):
