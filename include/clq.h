@@ -170,6 +170,27 @@ clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
                            void *workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/* clq_w4a4_linear for callers that cannot allocate device memory (code
+ * under stream capture, tight serving loops, hosts that forbid allocation):
+ * the same kernels and results, with the split schedule's workspace taken
+ * from a scratch array the library holds on each device instead of an
+ * argument.  The call allocates nothing and frees nothing.
+ *   Arguments as clq_w4a4_linear, without the workspace, plus
+ *   status   NULL, or device int32 [3] that receives this call's split-k
+ *            status words (as clq_w4a4_workspace_status; all zero when the
+ *            call did not split or every wait completed).
+ * The scratch is 64 MiB + 8448 bytes per device (a grid of up to 512
+ * workgroups, i.e. 256 compute units); on a device whose workspace would be
+ * larger the call returns CLQ_ERR_WORKSPACE.  It stays allocated until the
+ * process ends.  All calls on one device share it: calls that overlap in
+ * time on one device (several streams, several threads) race and must be
+ * ordered by the caller.  A call that splits clears the scratch's status
+ * words and flags first (a small fill kernel on `stream`). */
+clq_status clq_w4a4_linear_noalloc(const void *Xq, const float *x_scale, const void *Wq,
+                                   const float *w_scale, const void *bias, int64_t M,
+                                   int64_t N, int64_t K, void *Y, int64_t ldy,
+                                   int32_t *status, hipStream_t stream);
+
 /* Diagnostic: the exact integer accumulators acc[m][n] = sum_k qx*qw as
  * int32 [M][N] with row stride ldacc (elements).  Same kernels and workspace
  * rules as clq_w4a4_linear with the epilogue replaced by an int32 store. */

@@ -80,6 +80,7 @@ _lib.clq_clps_search.argtypes = [_p, _i64, _p, _p, _i64, _p, _i64, _i64, _i64, _
 _lib.clq_w4a4_workspace_status.argtypes = [_p, ctypes.c_size_t, _p, _p]
 _lib.clq_debug_set.argtypes = [_i32, _i64]
 _lib.clq_w4a4_schedule.argtypes = [_i64, _i64, _i64, _i32, _p]
+_lib.clq_w4a4_linear_noalloc.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p, _p]
 _lib.clq_debug_get.argtypes = [_i32]
 _lib.clq_debug_get.restype = _i64
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
@@ -87,7 +88,7 @@ for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
            "clq_quantize_weights8", "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8",
            "clq_unswizzle_weights8", "clq_clps_search", "clq_w4a4_workspace_status", "clq_debug_set",
-           "clq_w4a4_schedule"):
+           "clq_w4a4_schedule", "clq_w4a4_linear_noalloc"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -97,7 +98,7 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_act8_bytes", "clq_weight8_bytes", "clq_rotate_quant_act8", "clq_quantize_weights8",
            "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8", "clq_unswizzle_weights8",
            "clq_clps_workspace_bytes", "clq_clps_search", "clq_w4a4_workspace_status",
-           "clq_debug_set", "clq_debug_get", "clq_w4a4_schedule")
+           "clq_debug_set", "clq_debug_get", "clq_w4a4_schedule", "clq_w4a4_linear_noalloc")
 
 CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
 
@@ -317,6 +318,33 @@ def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None, workspace
     _check(_lib.clq_w4a4_linear(_ptr(Xq), _ptr(x_scale), _ptr(qw.wq), _ptr(qw.w_scale), _ptr(bias),
                                 M, qw.N, qw.K, _ptr(Y), Y.stride(0), _ptr(wsp), wsb, _stream(stream)),
            "clq_w4a4_linear")
+    return Y
+
+
+def clq_w4a4_linear_noalloc(Xq, x_scale, qw, bias=None, out=None, status=None, stream=None):
+    """clq_w4a4_linear without a workspace argument: the split schedule uses
+    the library's own per-device scratch (nothing is allocated by the call
+    when `out` is given).  status: None or a device int32 [3] tensor that
+    receives the call's split-k status words.  Calls on one device must not
+    overlap."""
+    M = _check_xq(Xq, x_scale, qw.K)
+    if bias is not None:
+        _dev(bias, "bias", torch.float16)
+        if bias.shape != (qw.N,) or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous fp16 [N] tensor")
+    if out is None:
+        out = torch.empty((M, (qw.N + 7) // 8 * 8), dtype=torch.float16, device=Xq.device)[:, :qw.N]
+    Y = out
+    _dev(Y, "Y", torch.float16)
+    if Y.dim() != 2 or Y.stride(1) != 1 or Y.shape != (M, qw.N):
+        raise ValueError("Y must be 2-D [M, N] with unit column stride")
+    if status is not None:
+        _dev(status, "status", torch.int32)
+        if status.numel() < 3 or not status.is_contiguous():
+            raise ValueError("status must be a contiguous int32 tensor of at least 3 elements")
+    _check(_lib.clq_w4a4_linear_noalloc(_ptr(Xq), _ptr(x_scale), _ptr(qw.wq), _ptr(qw.w_scale), _ptr(bias),
+                                        M, qw.N, qw.K, _ptr(Y), Y.stride(0), _ptr(status), _stream(stream)),
+           "clq_w4a4_linear_noalloc")
     return Y
 
 

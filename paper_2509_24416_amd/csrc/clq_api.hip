@@ -206,6 +206,22 @@ clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
                                      false, workspace, stream));
 }
 
+clq_status clq_w4a4_linear_noalloc(const void *Xq, const float *x_scale, const void *Wq,
+                                   const float *w_scale, const void *bias, int64_t M, int64_t N,
+                                   int64_t K, void *Y, int64_t ldy, int32_t *status,
+                                   hipStream_t stream) {
+    if (!x_scale || !w_scale) return CLQ_ERR_NULL;
+    clq_status s = check_gemm(Xq, Wq, M, N, K, Y, ldy, 8);
+    if (s != CLQ_OK) return s;
+    if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2)) || (status && !aligned(status, 4)))
+        return CLQ_ERR_ALIGN;
+    if (clq::gemm_workspace_bytes() > clq::gemm_scratch_bytes()) return CLQ_ERR_WORKSPACE;
+    return done(stream, clq::launch_gemm_noalloc(static_cast<const uint8_t *>(Xq), x_scale,
+                                                 static_cast<const uint8_t *>(Wq), w_scale,
+                                                 static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy,
+                                                 status, stream));
+}
+
 clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M, int64_t N, int64_t K,
                               int32_t *acc, int64_t ldacc, void *workspace,
                               size_t workspace_bytes, hipStream_t stream) {

@@ -114,6 +114,15 @@ hipError_t launch_unswizzle_act(const uint8_t *Xq, int64_t M, int K, uint8_t *ou
 // contributor's rank.
 size_t gemm_workspace_bytes();
 
+// The allocation-free linear: launch_gemm with the library's own scratch
+// (one per device) as the split workspace.  status: NULL, or device int32[3]
+// receiving the call's split-k status words.  Calls on one device share the
+// scratch and must not overlap.
+size_t gemm_scratch_bytes();
+hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                               const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
+                               int32_t *status, hipStream_t stream);
+
 // Split-k wait bound (sleeps) and the test-only switch that stops
 // contributors from signalling; read at each launch.
 extern int gemm_spin_limit;

@@ -56,6 +56,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "clq_internal.h"
@@ -1130,6 +1131,78 @@ size_t gemm_workspace_bytes() {
 
 int gemm_spin_limit = kSpinLimit;
 int gemm_drop_signal = 0;
+
+// ---- the allocation-free GEMM entry point's scratch ---------------------------
+// The workspace of the split schedule (status words, flags, one partial tile
+// per workgroup) for grids of up to kScratchGrid workgroups (256 compute
+// units), held by the library: each device the library runs on keeps its own
+// copy for the life of the process.  Host code reaches it only through the
+// address hipGetSymbolAddress returns for the current device.
+constexpr int kScratchGrid = 512;
+constexpr size_t kScratchBytes =
+    kStatusBytes + (size_t)kScratchGrid * TCfg::NW * sizeof(int) + (size_t)kScratchGrid * TCfg::PART_INTS * sizeof(int32_t);
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+void *scratch_ptr[kMaxDevices];   // per device, set once
+std::mutex scratch_mu;
+
+// clears the status words and flags before a split launch (a fill kernel,
+// not a memset: callers may capture the call in a graph)
+__global__ void clear_words_kernel(int *p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+}
+
+// the call's status words (zeros when the call did not split)
+__global__ void status_copy_kernel(const int *hdr, int *out, int split) {
+    const int i = threadIdx.x;
+    if (i < 3) out[i] = split ? hdr[i] : 0;
+}
+
+hipError_t device_scratch(void **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        scratch_ptr[dev] = p;
+    }
+    *out = scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+size_t gemm_scratch_bytes() { return kScratchBytes; }
+
+hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                               const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
+                               int32_t *status, hipStream_t stream) {
+    if (gemm_workspace_bytes() > kScratchBytes) return hipErrorInvalidValue;   // more CUs than the scratch serves
+    void *sp = nullptr;
+    hipError_t e = device_scratch(&sp);
+    if (e != hipSuccess) return e;
+    const GemmPlan pl = plan_gemm(M, N, K, true);
+    const int split = pl.sk > 0;
+    if (split) {
+        // status words and flags start at zero on every split call
+        const int nwords = (int)((kStatusBytes + (size_t)full_grid() * TCfg::NW * sizeof(int)) / sizeof(int));
+        hipLaunchKernelGGL(clear_words_kernel, dim3((nwords + 255) / 256), dim3(256), 0, stream,
+                           reinterpret_cast<int *>(sp), nwords);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    e = launch_gemm(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, false, sp, stream);
+    if (e != hipSuccess || status == nullptr) return e;
+    hipLaunchKernelGGL(status_copy_kernel, dim3(1), dim3(64), 0, stream, reinterpret_cast<const int *>(sp), status,
+                       split);
+    return hipGetLastError();
+}
 
 hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
                        const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
