@@ -27,7 +27,14 @@ Prints ONE JSON line:
              HBM (8 TB/s), from the same pass; and per layer with the 256 MB
              Infinity Cache flushed before every launch (cold)
   clocks     graphics (SCLK) and memory (MCLK) clock and socket power
-             sampled through amd-smi while the timed loop runs
+             sampled through amd-smi over 2.5 s of the same back-to-back
+             steps right after the timed loop (its first second dropped:
+             the readings trail the load)
+  ceilings   measured ceilings beside the nominal peaks: a 1 GiB device copy
+             (HBM) and the library's matrix-core probe loop (int8 MFMA on
+             int4-shaped operands, two workgroups per compute unit), with the
+             clock and power during the probe; roofline.frac_of_measured_ceiling
+             and rotate_quant.*_frac_of_copy_ceiling divide by them
   cpu_baseline  the CPU oracle timed on the host cores on a bounded sample
              of the same workload (token rows of every layer), plus one
              thread on a smaller sample
@@ -158,6 +165,7 @@ class ClockSampler:
             self.err = repr(e)
         self._stop = threading.Event()
         self._t = None
+        self.t0 = time.perf_counter()
 
     def _read(self):
         a = self.amdsmi
@@ -174,13 +182,14 @@ class ClockSampler:
     def _loop(self):
         while not self._stop.is_set():
             try:
-                self.samples.append(self._read())
+                self.samples.append((time.perf_counter(),) + tuple(self._read()))
             except Exception as e:
                 self.err = repr(e)
                 return
             time.sleep(0.02)
 
     def __enter__(self):
+        self.t0 = time.perf_counter()
         if self.handle is not None:
             self._t = threading.Thread(target=self._loop, daemon=True)
             self._t.start()
@@ -191,12 +200,18 @@ class ClockSampler:
         if self._t is not None:
             self._t.join()
 
-    def summary(self):
+    def summary(self, settle_s=0.3):
+        """Median / min / max over the samples taken after the first settle_s
+        seconds of the sampled region (the readings trail the load)."""
         if not self.samples:
             return {"sclk_mhz": None, "mclk_mhz": None, "power_w": None, "samples": 0,
                     "note": self.err or "amd-smi handle not found"}
         a = np.array([[x if isinstance(x, (int, float)) else np.nan for x in s] for s in self.samples],
                      dtype=np.float64)
+        keep = a[:, 0] >= self.t0 + settle_s
+        if keep.sum() >= 3:
+            a = a[keep]
+        a = a[:, 1:]
 
         def stats(col):
             v = a[:, col]
@@ -261,7 +276,7 @@ def cpu_baseline(layers, inputs, budget_s=15.0, wbits=4, abits=4):
 
 
 def bench_block(wl, args, clq, torch, dev, wbits=4, abits=4, steps=None, warmup=None, cold_reps=None,
-                sample_clocks=True):
+                sample_clocks=True, clock_s=2.5):
     """Times the hot path over the four linears of a DiT block workload.
     Returns a dict of measurements (see the module docstring)."""
     steps = args.steps if steps is None else steps
@@ -305,17 +320,24 @@ def bench_block(wl, args, clq, torch, dev, wbits=4, abits=4, steps=None, warmup=
     torch.cuda.synchronize()
 
     # timed region: exactly `steps` steps, launched back to back
-    sampler = ClockSampler(torch, dev) if sample_clocks else None
-    if sampler is not None:
-        sampler.__enter__()
     t0 = time.perf_counter()
     for _ in range(steps):
         step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    if sampler is not None:
-        sampler.__exit__()
     ms_per_step = wall * 1e3 / steps
+
+    # clocks and power: amd-smi's readings trail the load by up to a second,
+    # so they are sampled over a separate run of back-to-back steps (same
+    # work) lasting clock_s seconds, the first second dropped
+    sampler = None
+    if sample_clocks:
+        sampler = ClockSampler(torch, dev)
+        n_clk = max(1, int(clock_s * 1e3 / ms_per_step))
+        with sampler:
+            for _ in range(n_clk):
+                step()
+            torch.cuda.synchronize()
 
     # single-step times: one event pair per step, nothing between launches
     se = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
@@ -367,12 +389,63 @@ def bench_block(wl, args, clq, torch, dev, wbits=4, abits=4, steps=None, warmup=
         del flush
     res = dict(layers=layers, inputs=inputs, ms_per_step=ms_per_step, step_ms=step_ms, rq_t=rq_t, gm_t=gm_t,
                rq_ms=rq_ms, gemm_ms=gemm_ms, cold_rq=cold_rq, cold_gemm=cold_gemm,
-               clocks=sampler.summary() if sampler is not None else None,
+               clocks=sampler.summary(settle_s=1.0) if sampler is not None else None,
                total_ops=sum(gemm_ops(l) for l in layers))
     del state
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     return res
+
+
+def measure_ceilings(clq, torch, dev, seconds=1.0):
+    """Measured ceilings beside the nominal peaks: a 1 GiB device-to-device
+    copy (torch copy_, 2 GiB moved per launch) for HBM, and the library's
+    matrix-core probe loop (int4-shaped random operands, no memory traffic,
+    two workgroups per compute unit) for int8 MFMA, with the clocks and power
+    sampled while the probe runs."""
+    out = {}
+    src = torch.ones(1 << 29, dtype=torch.float16, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record()
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / 10
+    out["hbm_copy_GBps"] = round(2 * src.numel() * 2 / (ms * 1e-3) / 1e9, 1)
+    out["hbm_copy_note"] = "torch copy_ of 1 GiB (read 1 GiB + write 1 GiB per launch), 10 launches"
+    del src, dst
+    ops = torch.randint(0, 256, (clq.clq_diag_mfma_probe_bytes(),), dtype=torch.uint8, device=dev)
+    grid = 2 * torch.cuda.get_device_properties(dev).multi_processor_count
+    sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
+    n = clq.clq_diag_mfma_probe(ops, 200, grid, sink)   # warm up, and size the timed launches
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    clq.clq_diag_mfma_probe(ops, 200, grid, sink)
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t
+    iters = max(200, int(200 * (seconds / 4) / max(t, 1e-6)))
+    sampler = ClockSampler(torch, dev)
+    with sampler:
+        for _ in range(4):   # brings the clock to its loaded state (and the readings up to date)
+            clq.clq_diag_mfma_probe(ops, iters, grid, sink)
+        e0.record()
+        for _ in range(4):
+            n = clq.clq_diag_mfma_probe(ops, iters, grid, sink)
+        e1.record()
+        e1.synchronize()
+    ms = e0.elapsed_time(e1) / 4
+    out["mfma_probe_TOPS"] = round(n / (ms * 1e-3) / 1e12, 1)
+    out["mfma_probe_frac_of_nominal"] = round(n / (ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)
+    out["mfma_probe_ms"] = round(ms, 3)
+    out["mfma_probe_clocks"] = sampler.summary(settle_s=1.0)
+    out["mfma_probe_note"] = ("v_mfma_i32_32x32x32_i8 loop on random int4 codes widened to 16 q, "
+                              f"{grid} workgroups x 4 waves, 8 accumulators per wave, no memory traffic")
+    return out
 
 
 def block_summary(wl, r, abits=4):
@@ -643,9 +716,13 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=500)
-    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--cold-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-clocks", action="store_true",
+                    help="skip the 2.5 s clock and power sampling pass")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the measured HBM-copy and matrix-core ceilings")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the PixArt block and 28-block stack figures beside the headline")
     ap.add_argument("--workload", default="video_block",
@@ -700,7 +777,7 @@ def main():
     wl = BLOCKS[base]
     print(f"bench: {wl.name} W{wbits}A{abits}: {args.warmup} warmup + {args.steps} timed steps",
           file=sys.stderr, flush=True)
-    r = bench_block(wl, args, clq, torch, dev, wbits, abits)
+    r = bench_block(wl, args, clq, torch, dev, wbits, abits, sample_clocks=not args.no_clocks)
     sm = block_summary(wl, r, abits)
     layers = r["layers"]
     achieved = sm["ops_launch"] / (sm["gemm_avg_ms"] * 1e-3) / 1e12
@@ -755,6 +832,15 @@ def main():
         "clocks": r["clocks"],
         "gpu": torch.cuda.get_device_name(dev),
     }
+    if not args.no_ceilings:
+        print("bench: measured ceilings", file=sys.stderr, flush=True)
+        ceil = measure_ceilings(clq, torch, dev)
+        out["ceilings"] = ceil
+        out["roofline"]["frac_of_measured_ceiling"] = round(achieved / ceil["mfma_probe_TOPS"], 4)
+        out["rotate_quant"]["frac_of_copy_ceiling"] = round(rq_achieved / ceil["hbm_copy_GBps"], 4)
+        if cold_rq_total > 0:
+            out["rotate_quant"]["cold_frac_of_copy_ceiling"] = round(
+                cold_bytes / (cold_rq_total * 1e-3) / 1e9 / ceil["hbm_copy_GBps"], 4)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, r["inputs"], wbits=wbits, abits=abits)
     r = None

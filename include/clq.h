@@ -378,6 +378,19 @@ typedef enum {
 clq_status clq_debug_set(int32_t knob, int64_t value);
 int64_t clq_debug_get(int32_t knob);
 
+/* ---- Measured ceiling (diagnostic) -------------------------------------------
+ * An int8 matrix-core loop with no memory traffic, on operands shaped like
+ * the W4A4 GEMM's (random int4 codes widened to 16 q), at the GEMM's
+ * occupancy: the rate the chip sustains for this arithmetic at the clock its
+ * power limit allows.  Each 256-lane workgroup runs iters x 16 x 4
+ * v_mfma_i32_32x32x32_i8 (2 x 32^3 ops each).
+ *   ops   device buffer of clq_diag_mfma_probe_bytes() random bytes.
+ *   sink  device int32 [grid * 256], overwritten (keeps the work live).
+ *   grid  workgroups (2 per compute unit fills the chip as the GEMM does). */
+size_t clq_diag_mfma_probe_bytes(void);
+clq_status clq_diag_mfma_probe(const void *ops, size_t ops_bytes, int32_t iters, int32_t grid,
+                               int32_t *sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

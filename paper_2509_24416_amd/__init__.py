@@ -81,6 +81,9 @@ _lib.clq_w4a4_workspace_status.argtypes = [_p, ctypes.c_size_t, _p, _p]
 _lib.clq_debug_set.argtypes = [_i32, _i64]
 _lib.clq_w4a4_schedule.argtypes = [_i64, _i64, _i64, _i32, _p]
 _lib.clq_w4a4_linear_noalloc.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p, _p]
+_lib.clq_diag_mfma_probe_bytes.restype = ctypes.c_size_t
+_lib.clq_diag_mfma_probe_bytes.argtypes = []
+_lib.clq_diag_mfma_probe.argtypes = [_p, ctypes.c_size_t, _i32, _i32, _p, _p]
 _lib.clq_debug_get.argtypes = [_i32]
 _lib.clq_debug_get.restype = _i64
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
@@ -88,7 +91,7 @@ for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
            "clq_quantize_weights8", "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8",
            "clq_unswizzle_weights8", "clq_clps_search", "clq_w4a4_workspace_status", "clq_debug_set",
-           "clq_w4a4_schedule", "clq_w4a4_linear_noalloc"):
+           "clq_w4a4_schedule", "clq_w4a4_linear_noalloc", "clq_diag_mfma_probe"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -98,7 +101,8 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_act8_bytes", "clq_weight8_bytes", "clq_rotate_quant_act8", "clq_quantize_weights8",
            "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8", "clq_unswizzle_weights8",
            "clq_clps_workspace_bytes", "clq_clps_search", "clq_w4a4_workspace_status",
-           "clq_debug_set", "clq_debug_get", "clq_w4a4_schedule", "clq_w4a4_linear_noalloc")
+           "clq_debug_set", "clq_debug_get", "clq_w4a4_schedule", "clq_w4a4_linear_noalloc",
+           "clq_diag_mfma_probe_bytes", "clq_diag_mfma_probe")
 
 CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
 
@@ -136,6 +140,23 @@ def clq_debug_set(knob, value):
 
 def clq_debug_get(knob):
     return int(_lib.clq_debug_get(int(knob)))
+
+
+def clq_diag_mfma_probe_bytes():
+    return int(_lib.clq_diag_mfma_probe_bytes())
+
+
+def clq_diag_mfma_probe(ops, iters, grid, sink, stream=None):
+    """Enqueues the matrix-core ceiling loop (diagnostic): ops a uint8
+    device tensor of clq_diag_mfma_probe_bytes() random bytes, sink an int32
+    device tensor of grid * 256 elements.  Returns the int8 ops it performs."""
+    _dev(ops, "ops", torch.uint8)
+    _dev(sink, "sink", torch.int32)
+    if sink.numel() < grid * 256:
+        raise ValueError("sink needs grid * 256 elements")
+    _check(_lib.clq_diag_mfma_probe(_ptr(ops), ops.numel(), iters, grid, _ptr(sink), _stream(stream)),
+           "clq_diag_mfma_probe")
+    return grid * iters * 64 * 2 * 32 ** 3
 
 
 def clq_w4a4_schedule(M, N, K, with_workspace=True):

@@ -123,6 +123,12 @@ hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t
                                const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
                                int32_t *status, hipStream_t stream);
 
+// Diagnostic: an int8 matrix-core loop on GEMM-shaped operands (16 MFMAs
+// of 32x32x32 per iteration per wave) reading mfma_probe_bytes() of random
+// bytes; sink receives one int per lane (grid * 256).
+size_t mfma_probe_bytes();
+hipError_t launch_mfma_probe(const void *ops, int iters, int *sink, int grid, hipStream_t stream);
+
 // Split-k wait bound (sleeps) and the test-only switch that stops
 // contributors from signalling; read at each launch.
 extern int gemm_spin_limit;

@@ -68,12 +68,14 @@ def lib():
     L.clq_debug_get.argtypes = [i32]
     L.clq_debug_get.restype = i64
     L.clq_w4a4_schedule.argtypes = [i64, i64, i64, i32, p]
+    L.clq_diag_mfma_probe_bytes.restype = ctypes.c_size_t
+    L.clq_diag_mfma_probe.argtypes = [p, ctypes.c_size_t, i32, i32, p, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 29, names
+    assert len(names) == 31, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -226,6 +228,16 @@ def test_schedule(lib):
     for M, N, K in ((8192, 3456, 1152), (8192, 4608, 1152), (43200, 3456, 1152), (43200, 1152, 4608)):
         k, tiles, dp, sk, grid = schedule(lib, M, N, K)
         assert k == 0 and sk == 0 and dp == tiles
+
+
+def test_mfma_probe_validation(lib):
+    need = lib.clq_diag_mfma_probe_bytes()
+    assert need == 1024 * 16 * 64 * 16
+    assert lib.clq_diag_mfma_probe(None, need, 1, 1, A, None) == NULL
+    assert lib.clq_diag_mfma_probe(A, need - 1, 1, 1, A, None) == WORKSPACE
+    assert lib.clq_diag_mfma_probe(A, need, 0, 1, A, None) == ARG
+    assert lib.clq_diag_mfma_probe(A, need, 1, 0, A, None) == ARG
+    assert lib.clq_diag_mfma_probe(A + 8, need, 1, 1, A, None) == ALIGN
 
 
 def test_debug_knobs(lib):
