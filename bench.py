@@ -60,7 +60,6 @@ INT8_PEAK_TOPS = 5000.0      # dense int8 MFMA, MI355X (5.0 POP/s)
 HBM_PEAK_GBPS = 8000.0       # HBM3E, MI355X
 TRAFFIC_FILES = {
     "video_block_m43200_h1152_b64": os.path.join(ROOT, "profiles", "gemm_traffic_video_block_m43200.txt"),
-    "pixart_block_m8192_h1152_b64": os.path.join(ROOT, "profiles", "gemm_traffic_pixart_block_m8192.txt"),
     "flux_block_m4608_h3072_b128": os.path.join(ROOT, "profiles", "gemm_traffic_flux_block_m4608.txt"),
 }
 BLOCKS = {"video_block": workloads.C4, "pixart_block": workloads.C2, "flux_block": workloads.C3}
