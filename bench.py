@@ -633,11 +633,11 @@ def stack_weights(torch, dev, nb=28):
     return _STACK_W[nb]
 
 
-def stack_point(clq, torch, dev, M, b, steps, perms=None, fold=False, eager=False):
+def stack_point(clq, torch, dev, M, b, steps, perms=None, fold=False, eager=False, fuse=False):
     """One stack configuration: graph replays timed back to back, plus
     single-replay percentiles (events at replay boundaries)."""
     from paper_2509_24416_amd.stack import DiTStack
-    st = DiTStack(stack_weights(torch, dev), M, b, perms=perms, fold=fold)
+    st = DiTStack(stack_weights(torch, dev), M, b, perms=perms, fold=fold, fuse=fuse)
     x = torch.from_numpy(workloads.activations(M, 1152, "L1", 500)).to(dev)
     st.forward(x)
     st.capture()
@@ -656,8 +656,11 @@ def stack_point(clq, torch, dev, M, b, steps, perms=None, fold=False, eager=Fals
         st.replay()
         e.record(stream)
     torch.cuda.synchronize()
+    plans = [clq.clq_w4a4_rq_schedule(M, N, K, b)["fused"] if fuse else 0
+             for (K, N) in ((1152, 3456), (1152, 1152), (1152, 4608), (4608, 1152))]
     out = {"graph_ms": round(g_ms, 4), "graph_TOPS": round(st.ops / (g_ms * 1e-3) / 1e12, 1),
-           "replay_ms_percentiles": pct([a.elapsed_time(e) for a, e in ev]), "launches_per_step": 224}
+           "replay_ms_percentiles": pct([a.elapsed_time(e) for a, e in ev]),
+           "launches_per_step": len(st.blocks) * (8 - sum(plans)), "fused_layers": plans}
     if eager:
         t0 = time.perf_counter()
         for _ in range(steps):
@@ -677,15 +680,20 @@ def bench_stack(args, clq, torch, dev):
     """The multi-layer path: 28 PixArt-width DiT blocks (112 linears, 223 MB
     of resident int4 weights), rotate+quant + W4A4 GEMM per linear, replayed
     as one HIP graph.  value = effective TOPS at M = 4096 tokens, block 64;
-    M = 1024 / 16384, the eager step and the Hadamard block sweep 32 / 64 /
-    128 at every M are reported beside it."""
+    M = 1024 / 16384, the eager step, the Hadamard block sweep 32 / 64 / 128
+    at every M, and the stack with each input's rotate+quantize folded into
+    its GEMM launch where the schedule allows (clq_w4a4_rq_linear) are
+    reported beside it."""
     nb = 28
-    res = {}
+    res, fused = {}, {}
     for M in (4096, 1024, 16384):
         for b in (64, 32, 128):
             steps = args.steps if M == 4096 else max(5, args.steps // 4)
             print(f"bench: dit_stack M={M} block={b}", file=sys.stderr, flush=True)
             res[(M, b)] = stack_point(clq, torch, dev, M, b, steps, eager=(b == 64))
+        # the same stack with each rotate+quantize folded into its GEMM launch
+        # where the schedule allows (clq_w4a4_rq_linear)
+        fused[M] = stack_point(clq, torch, dev, M, 64, max(5, args.steps // 4), fuse=True)
     # one swap vector per layer input (random stand-ins for OBS outputs):
     # gathered by every rotate+quant, or folded into the producing layers
     from paper_2509_24416_amd.stack import LAYERS
@@ -705,6 +713,7 @@ def bench_stack(args, clq, torch, dev):
         "config": {"workload": "dit_stack_28x4_m4096_h1152_b64", "blocks": nb, "M": 4096, "block": 64,
                    "launches_per_step": 2 * 4 * nb, "parallelism": "none (one GPU)"},
         "per_M_block": {f"M{M}_b{b}": v for (M, b), v in res.items()},
+        "fused_block64": {f"M{M}": v for M, v in fused.items()},
         "swap_vectors_m4096": swap,
         "gpu": torch.cuda.get_device_name(dev),
     }

@@ -170,6 +170,37 @@ clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
                            void *workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/* The consumer's rotate+quantize and the W4A4 linear in one call (the fused
+ * inter-layer path of a layer stack: Sec. 3.3's online rotation and Sec. 3.1's
+ * quantizer folded into the GEMM launch).
+ *   X, ldx, block   the layer's fp16 input as for clq_rotate_quant_act (no
+ *                   gather vector: a stack folds each swap into its producing
+ *                   layer instead).
+ *   Xq, x_scale     out, exactly what clq_rotate_quant_act writes.
+ *   the rest        as clq_w4a4_linear (Y exactly what it writes).
+ * When the GEMM's schedule is the two-halves kernel (few tiles), N % 16 == 0
+ * and a workspace is given, this is ONE launch: its first work items rotate
+ * and quantize batches of rows, its GEMM tiles wait for the batches holding
+ * their tokens (work items are taken in order from a counter in the
+ * workspace, so a tile only waits for items already taken by running
+ * workgroups: no co-residency is assumed).  Otherwise it is the two launches
+ * clq_rotate_quant_act + clq_w4a4_linear.  clq_w4a4_rq_schedule tells which.
+ * The workspace rules of clq_w4a4_linear apply; the fused launch counts in
+ * its status words too (a wait that gives up, never expected).
+ * Performance note: on MI355X the fused launch is slower than the two
+ * launches at every size measured (the rotate+quantize items run latency-
+ * bound in workgroups sized for the GEMM); it is kept for callers that need
+ * a single launch per layer. */
+clq_status clq_w4a4_rq_linear(const void *X, int64_t ldx, int32_t block, void *Xq, float *x_scale,
+                              const void *Wq, const float *w_scale, const void *bias, int64_t M,
+                              int64_t N, int64_t K, void *Y, int64_t ldy, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/* Diagnostic (host only): info[0..3] = {1 if clq_w4a4_rq_linear fuses this
+ * shape into one launch, rows per rotate+quantize item, items, GEMM tiles}. */
+clq_status clq_w4a4_rq_schedule(int64_t M, int64_t N, int64_t K, int32_t block, int32_t with_workspace,
+                                int64_t *info);
+
 /* clq_w4a4_linear for callers that cannot allocate device memory (code
  * under stream capture, tight serving loops, hosts that forbid allocation):
  * the same kernels and results, with the split schedule's workspace taken
@@ -179,7 +210,8 @@ clq_status clq_w4a4_linear(const void *Xq, const float *x_scale, const void *Wq,
  *   status   NULL, or device int32 [3] that receives this call's split-k
  *            status words (as clq_w4a4_workspace_status; all zero when the
  *            call did not split or every wait completed).
- * The scratch is 64 MiB + 8448 bytes per device (a grid of up to 512
+ * The scratch is 64 MiB + 8448 bytes per device (the split schedule's part
+ * of a workspace: status words, flags and partials, for a grid of up to 512
  * workgroups, i.e. 256 compute units); on a device whose workspace would be
  * larger the call returns CLQ_ERR_WORKSPACE.  It stays allocated until the
  * process ends.  All calls on one device share it: calls that overlap in

@@ -81,6 +81,9 @@ _lib.clq_w4a4_workspace_status.argtypes = [_p, ctypes.c_size_t, _p, _p]
 _lib.clq_debug_set.argtypes = [_i32, _i64]
 _lib.clq_w4a4_schedule.argtypes = [_i64, _i64, _i64, _i32, _p]
 _lib.clq_w4a4_linear_noalloc.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p, _p]
+_lib.clq_w4a4_rq_linear.argtypes = [_p, _i64, _i32, _p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p,
+                                    ctypes.c_size_t, _p]
+_lib.clq_w4a4_rq_schedule.argtypes = [_i64, _i64, _i64, _i32, _i32, _p]
 _lib.clq_diag_mfma_probe_bytes.restype = ctypes.c_size_t
 _lib.clq_diag_mfma_probe_bytes.argtypes = []
 _lib.clq_diag_mfma_probe.argtypes = [_p, ctypes.c_size_t, _i32, _i32, _p, _p]
@@ -91,7 +94,8 @@ for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
            "clq_quantize_weights8", "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8",
            "clq_unswizzle_weights8", "clq_clps_search", "clq_w4a4_workspace_status", "clq_debug_set",
-           "clq_w4a4_schedule", "clq_w4a4_linear_noalloc", "clq_diag_mfma_probe"):
+           "clq_w4a4_schedule", "clq_w4a4_linear_noalloc", "clq_diag_mfma_probe",
+           "clq_w4a4_rq_linear", "clq_w4a4_rq_schedule"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -102,7 +106,8 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8", "clq_unswizzle_weights8",
            "clq_clps_workspace_bytes", "clq_clps_search", "clq_w4a4_workspace_status",
            "clq_debug_set", "clq_debug_get", "clq_w4a4_schedule", "clq_w4a4_linear_noalloc",
-           "clq_diag_mfma_probe_bytes", "clq_diag_mfma_probe")
+           "clq_diag_mfma_probe_bytes", "clq_diag_mfma_probe", "clq_w4a4_rq_linear",
+           "clq_w4a4_rq_schedule")
 
 CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
 
@@ -367,6 +372,54 @@ def clq_w4a4_linear_noalloc(Xq, x_scale, qw, bias=None, out=None, status=None, s
                                         M, qw.N, qw.K, _ptr(Y), Y.stride(0), _ptr(status), _stream(stream)),
            "clq_w4a4_linear_noalloc")
     return Y
+
+
+def clq_w4a4_rq_schedule(M, N, K, block, with_workspace=True):
+    """Whether clq_w4a4_rq_linear runs this shape as one launch: dict(fused,
+    rows_per_item, items, tiles)."""
+    info = (ctypes.c_int64 * 4)()
+    _check(_lib.clq_w4a4_rq_schedule(M, N, K, block, 1 if with_workspace else 0, ctypes.cast(info, ctypes.c_void_p)),
+           "clq_w4a4_rq_schedule")
+    return dict(fused=info[0], rows_per_item=info[1], items=info[2], tiles=info[3])
+
+
+def clq_w4a4_rq_linear(X, block, qw, bias=None, Xq_out=None, scale_out=None, out=None, stream=None,
+                       workspace=None):
+    """Rotate+quantize X (fp16 [M, K], row stride allowed) and run the W4A4
+    linear against qw, in one launch when clq_w4a4_rq_schedule says so (else
+    the two launches).  X is not gathered: if qw was quantized with a swap
+    vector, X must already be in that column order (gathered upstream).  Returns (Y, Xq, x_scale), each exactly what
+    clq_rotate_quant_act and clq_w4a4_linear would write.  workspace: None
+    (the default of (device, stream)), False (none: two launches), or a
+    zero-filled uint8 tensor of clq_w4a4_workspace_bytes() bytes."""
+    _dev(X, "X", torch.float16)
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D [M, K] with unit column stride")
+    M, K = X.shape
+    if K != qw.K or qw.bits != 4 or qw.block != block:
+        raise ValueError("qw must be a 4-bit weight of the same K and block")
+    nbytes = clq_act_bytes(M, K)
+    Xq = Xq_out if Xq_out is not None else torch.empty(nbytes, dtype=torch.uint8, device=X.device)
+    xs = scale_out if scale_out is not None else torch.empty(M, dtype=torch.float32, device=X.device)
+    _dev(Xq, "Xq", torch.uint8)
+    _dev(xs, "x_scale", torch.float32)
+    if Xq.numel() < nbytes or not Xq.is_contiguous() or xs.numel() < M:
+        raise ValueError("Xq / x_scale buffers are too small")
+    if bias is not None:
+        _dev(bias, "bias", torch.float16)
+        if bias.shape != (qw.N,) or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous fp16 [N] tensor")
+    if out is None:
+        out = torch.empty((M, (qw.N + 7) // 8 * 8), dtype=torch.float16, device=X.device)[:, :qw.N]
+    Y = out
+    _dev(Y, "Y", torch.float16)
+    if Y.dim() != 2 or Y.stride(1) != 1 or Y.shape != (M, qw.N):
+        raise ValueError("Y must be 2-D [M, N] with unit column stride")
+    wsp, wsb = _workspace(X.device, workspace, stream)
+    _check(_lib.clq_w4a4_rq_linear(_ptr(X), X.stride(0), block, _ptr(Xq), _ptr(xs), _ptr(qw.wq), _ptr(qw.w_scale),
+                                   _ptr(bias), M, qw.N, K, _ptr(Y), Y.stride(0), _ptr(wsp), wsb, _stream(stream)),
+           "clq_w4a4_rq_linear")
+    return Y, Xq, xs
 
 
 def clq_w4a4_accum_i32(Xq, x_scale, qw, out=None, stream=None, workspace=None):

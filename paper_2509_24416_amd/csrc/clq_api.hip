@@ -226,11 +226,43 @@ clq_status clq_w4a4_linear_noalloc(const void *Xq, const float *x_scale, const v
     if (s != CLQ_OK) return s;
     if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2)) || (status && !aligned(status, 4)))
         return CLQ_ERR_ALIGN;
-    if (clq::gemm_workspace_bytes() > clq::gemm_scratch_bytes()) return CLQ_ERR_WORKSPACE;
+    if (clq::gemm_split_bytes() > clq::gemm_scratch_bytes()) return CLQ_ERR_WORKSPACE;
     return done(stream, clq::launch_gemm_noalloc(static_cast<const uint8_t *>(Xq), x_scale,
                                                  static_cast<const uint8_t *>(Wq), w_scale,
                                                  static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy,
                                                  status, stream));
+}
+
+clq_status clq_w4a4_rq_linear(const void *X, int64_t ldx, int32_t block, void *Xq, float *x_scale,
+                              const void *Wq, const float *w_scale, const void *bias, int64_t M, int64_t N,
+                              int64_t K, void *Y, int64_t ldy, void *workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+    if (!X || !x_scale || !w_scale) return CLQ_ERR_NULL;
+    clq_status s = check_gemm(Xq, Wq, M, N, K, Y, ldy, 8);
+    if (s != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (ldx < K || ldx % 8 != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(X, 16) || !aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2)))
+        return CLQ_ERR_ALIGN;
+    if ((s = check_workspace(workspace, workspace_bytes)) != CLQ_OK) return s;
+    return done(stream, clq::launch_rq_gemm(static_cast<const uint16_t *>(X), ldx, block, static_cast<uint8_t *>(Xq),
+                                            x_scale, static_cast<const uint8_t *>(Wq), w_scale,
+                                            static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy, workspace,
+                                            stream));
+}
+
+clq_status clq_w4a4_rq_schedule(int64_t M, int64_t N, int64_t K, int32_t block, int32_t with_workspace,
+                                int64_t *info) {
+    if (!info) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    const clq::RqGemmPlan p = clq::plan_rq_gemm(M, N, (int)K, block, with_workspace != 0);
+    info[0] = p.fused;
+    info[1] = p.rq_rows;
+    info[2] = p.n_rq;
+    info[3] = p.tiles;
+    return CLQ_OK;
 }
 
 clq_status clq_w4a4_accum_i32(const void *Xq, const void *Wq, int64_t M, int64_t N, int64_t K,

@@ -108,10 +108,11 @@ hipError_t launch_unswizzle(const uint8_t *Wq, int64_t N, int K, uint8_t *out,
 hipError_t launch_unswizzle_act(const uint8_t *Xq, int64_t M, int K, uint8_t *out,
                                 hipStream_t stream);
 
-// Workspace for the split-k schedule of launch_gemm (bytes; depends on the
-// device's compute-unit count only).  Its first 256 bytes hold the split-k
-// status words: [0] waits that gave up, [1] the first such tile, [2] its
-// contributor's rank.
+// Workspace of launch_gemm and launch_rq_gemm (bytes; depends on the
+// device's compute-unit count only).  Its first 256 bytes hold the status
+// words: [0] waits that gave up, [1] the first such tile, [2] the missing
+// contributor's rank (or rotate+quantize item); words 4..6 are the fused
+// variant's queue state.
 size_t gemm_workspace_bytes();
 
 // The allocation-free linear: launch_gemm with the library's own scratch
@@ -142,6 +143,23 @@ struct GemmPlan {
     int kernel, tiles_m, tiles, dp, sk, grid;
 };
 GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split);
+
+// Rotate+quantize folded into the GEMM (the two-halves kernel's fused
+// variant): fused = 0 when the shape or arguments take two launches instead.
+struct RqGemmPlan {
+    int fused, kernel, tiles, rq_rows, n_rq;
+};
+RqGemmPlan plan_rq_gemm(int64_t M, int64_t N, int K, int block, bool have_workspace);
+
+// X fp16 [M][K] (row stride ldx, no gather) -> Xq, xs (as launch_rotate_quant)
+// and Y (as launch_gemm), in one launch when plan_rq_gemm says so.
+hipError_t launch_rq_gemm(const uint16_t *X, int64_t ldx, int block, uint8_t *Xq, float *xs, const uint8_t *Wq,
+                          const float *ws, const uint16_t *bias, int64_t M, int64_t N, int K, void *Y,
+                          int64_t ldy, void *workspace, hipStream_t stream);
+
+// Bytes of the split schedule's part of the workspace (status words, flags,
+// partial tiles): the allocation-free entry point's scratch holds this much.
+size_t gemm_split_bytes();
 
 // workspace: gemm_workspace_bytes() zero-filled bytes, or nullptr (whole
 // tiles only).  Calls that share a workspace must not overlap in time.

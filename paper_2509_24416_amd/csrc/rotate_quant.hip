@@ -31,30 +31,10 @@
 #include <algorithm>
 
 #include "clq_internal.h"
+#include "rq_device.h"
 
 namespace clq {
 namespace {
-
-constexpr float kMagic = 12582920.0f;  // 1.5 * 2^23 + 8
-
-// n-bit grid of Eq. (1): codes in [-qmax, qmax], qmax = 2^(n-1) - 1; the
-// magic constant 1.5 * 2^23 + 2^(n-1) leaves code + 2^(n-1) in the low n
-// bits of the fma result (bits n..21 clear).
-template <int QB>
-struct Grid {
-    static_assert(QB == 4 || QB == 8, "4- or 8-bit codes");
-    static constexpr float qmax = QB == 4 ? 7.0f : 127.0f;
-    static constexpr float magic = QB == 4 ? 12582920.0f : 12583040.0f;
-};
-
-// Slot of 16-byte chunk i of Hadamard block j inside its block's span in
-// LDS.  Eight consecutive lanes own eight consecutive blocks and read chunk i
-// at the same time; the XOR spreads those reads over distinct banks.
-template <int B>
-__device__ __forceinline__ int chunk_slot(int i, int j) {
-    if constexpr (B == 32) return i ^ ((j >> 1) & 3);
-    else return i ^ (j & 7);
-}
 
 // Activation kernel lane order: for b >= 64 lane t owns block j = t / R of
 // row r = t % R (rows fastest), so that the code stores of consecutive lanes
@@ -68,46 +48,6 @@ template <int B>
 __device__ __forceinline__ int act_slot(int i, int j, int r, int R) {
     if constexpr (rows_fastest<B>()) return i ^ ((j * R + r) & 7);
     else return chunk_slot<B>(i, j);
-}
-
-// Butterfly stage h = 1 straight from fp16 inputs.  The mixed-precision fma
-// reads an f16 half of each source register and rounds u * 1 + s (or
-// u * 1 - s) once to fp32: the value of converting both halves (exact) and
-// adding, bit for bit over all 2^32 pairs of halves, in one instruction per
-// output instead of two conversions and an add per pair.
-__device__ __forceinline__ void stage1_packed(uint32_t w, float &sum, float &dif) {
-    asm("v_fma_mix_f32 %0, %1, 1.0, %1 op_sel:[0,0,1] op_sel_hi:[1,0,1]" : "=v"(sum) : "v"(w));
-    asm("v_fma_mix_f32 %0, %1, 1.0, -%1 op_sel:[0,0,1] op_sel_hi:[1,0,1]" : "=v"(dif) : "v"(w));
-}
-// the same from the low halves of two registers (gathered inputs)
-__device__ __forceinline__ void stage1_pair(uint32_t u, uint32_t v, float &sum, float &dif) {
-    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel_hi:[1,0,1]" : "=v"(sum) : "v"(u), "v"(v));
-    asm("v_fma_mix_f32 %0, %1, 1.0, -%2 op_sel_hi:[1,0,1]" : "=v"(dif) : "v"(u), "v"(v));
-}
-
-// Largest |x| of a block: one three-operand max per pair of elements, in two
-// independent chains (a max is exact, so the order does not matter).
-template <int B>
-__device__ __forceinline__ float block_absmax(const float *x) {
-    float m0 = 0.0f, m1 = 0.0f;
-#pragma unroll
-    for (int i = 0; i < B; i += 4) {
-        m0 = fmaxf(fmaxf(m0, fabsf(x[i])), fabsf(x[i + 1]));
-        m1 = fmaxf(fmaxf(m1, fabsf(x[i + 2])), fabsf(x[i + 3]));
-    }
-    return fmaxf(m0, m1);
-}
-
-// Packs eight quantized words (code + 8 in bits 0..3, bits 4..21 clear) into
-// one dword of two's-complement nibbles, element e at bits 4e..4e+3.
-__device__ __forceinline__ uint32_t pack8(const uint32_t *w) {
-    const uint32_t p01 = (w[1] << 4) | w[0];
-    const uint32_t p23 = (w[3] << 4) | w[2];
-    const uint32_t p45 = (w[5] << 4) | w[4];
-    const uint32_t p67 = (w[7] << 4) | w[6];
-    const uint32_t q03 = (p23 << 8) | p01;  // bits 0..15 clean
-    const uint32_t q47 = (p67 << 8) | p45;
-    return __builtin_amdgcn_perm(q47, q03, 0x05040100u) ^ 0x88888888u;
 }
 
 // Sixteen quantized words (code + 128 in bits 0..7, bits 8..21 clear) into

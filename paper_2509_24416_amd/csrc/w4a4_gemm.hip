@@ -60,6 +60,7 @@
 #include <type_traits>
 
 #include "clq_internal.h"
+#include "rq_device.h"
 
 #define CLQ_LDS __attribute__((address_space(3)))
 
@@ -143,6 +144,15 @@ struct GemmArgs {
     int *status;   // split-k status words (kStatusBytes at the workspace head)
     int spin_limit;   // bound on a wait for a contributor's flag (sleeps)
     int drop_signal;  // test only: contributors never raise their flags
+    // fused rotate+quantize (the two-halves kernel with FB != 0): fp16
+    // activations fx (row stride ldfx) quantized into Xq / xs by the first
+    // n_rq work items (rq_rows rows each), the GEMM tiles after them; qhdr:
+    // queue, finished and epoch words; qflags: one per rotate+quantize item
+    const uint16_t *fx;
+    int64_t ldfx;
+    int rq_rows, n_rq;
+    int *qhdr;
+    int *qflags;
     // squared-error mode: target Y0 fp32 [M][ldy0]; one fp64 partial per
     // wave of every tile, at errp[tile * waves + wave]
     const float *y0;
@@ -752,7 +762,14 @@ using TileHalf64 = Tile<1, 1, 4, 2, 2>;
 // arithmetic as the persistent kernel.
 constexpr int kHalfStages = 4;   // ring depth per half
 
-template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+// FB != 0: the fused variant (rotate+quantize of the activations folded in,
+// Hadamard block FB).  Work items come from an atomic counter in order: the
+// first n_rq items rotate and quantize rq_rows activation rows each and
+// publish them; the rest are the GEMM tiles, each of which first waits for
+// the items covering its token rows.  A tile only ever waits for items taken
+// before its own, by workgroups that are already running and never wait, so
+// the grid cannot deadlock whatever part of it is resident.
+template <class C, bool I32OUT, bool RAGGED, bool BIAS, int FB = 0>
 __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs a)
 {
     static_assert(!(I32OUT && BIAS), "no bias on the integer output");
@@ -773,7 +790,43 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
     const int w8 = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = w8 / C::NW, wm = w8 % C::NW;   // one channel panel per tile: wn = 0
     const int M = a.M, N = a.N, nks = a.K >> 6;
-    const int L = blockIdx.x;
+    int L = blockIdx.x;
+    int e1 = 0;   // fused: this call's epoch + 1, the value of a published item's flag
+    if constexpr (FB != 0) {
+        static_assert(!I32OUT, "the fused variant writes fp16");
+        __shared__ int s_item, s_epoch;
+        if (tid == 0) {
+            s_epoch = __hip_atomic_load(a.qhdr + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_item = __hip_atomic_fetch_add(a.qhdr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        __syncthreads();
+        const int item = s_item;
+        e1 = s_epoch + 1;
+        auto finish = [&]() {
+            // the last workgroup to finish resets the queue for the next call
+            if (tid == 0) {
+                const int done = __hip_atomic_fetch_add(a.qhdr + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (done == (int)gridDim.x - 1) {
+                    __hip_atomic_store(a.qhdr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(a.qhdr + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(a.qhdr + 2, e1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+        };
+        if (item < a.n_rq) {
+            const int64_t row0 = (int64_t)item * a.rq_rows;
+            const int rows = (int)min((int64_t)a.rq_rows, padded_act_rows(M) - row0);
+            rq_rows_coherent<FB>(a.fx, a.ldfx, M, row0, rows, a.K, const_cast<uint8_t *>(a.Xq),
+                                 const_cast<float *>(a.xs), pool);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's codes and scales written through
+            __syncthreads();
+            if (tid == 0) __hip_atomic_store(a.qflags + item, e1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            finish();
+            return;
+        }
+        L = item - a.n_rq;
+        // defer the finish count to the end of the tile (below)
+    }
     int tm, tn;
     {
         const int gsz = kGroupM * a.tiles_n;
@@ -802,13 +855,19 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
     // stage k of this half into slot q; past the end the last stage is
     // loaded again (into a free slot, never read), so every wave issues the
     // same transfers and the wait counts stay fixed
+    // (fused: the activation units were written in this launch, possibly on
+    // another XCD, so they are read device-coherent, past this XCD's L2)
     auto produce = [&](int q, int k) {
         const uint32_t voff = (uint32_t)(min(k, len - 1) * 1024 + lane * 16);
         uint8_t *dst = &ring[half][q][0];
 #pragma unroll
         for (int j = 0; j < C::UPW; ++j) {
             const uint8_t *sp = usrc[j] + voff;
-            __builtin_amdgcn_global_load_lds(sp, (CLQ_LDS void *)(dst + (wm * C::UPW + j) * 1024), 16, 0, 0);
+            CLQ_LDS void *dp = (CLQ_LDS void *)(dst + (wm * C::UPW + j) * 1024);
+            if (FB != 0 && wm * C::UPW + j >= C::W_UNITS)
+                __builtin_amdgcn_global_load_lds(sp, dp, 16, 0, 16);
+            else
+                __builtin_amdgcn_global_load_lds(sp, dp, 16, 0, 0);
         }
     };
     v4u pa[C::FN], pb[C::FM];
@@ -863,6 +922,29 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
     // branch-free, ahead of the transfers), held in registers through the k
     // loop and written to LDS after it, when no transfer into LDS is in
     // flight (an LDS store during the transfers would wait for all of them)
+    if constexpr (FB != 0) {
+        // wait until the items holding this tile's token rows are published
+        if (tid == 0) {
+            const int64_t r0 = (int64_t)tm * C::BM;
+            const int64_t r1 = min(r0 + C::BM, padded_act_rows(M)) - 1;
+            const int i1 = (int)min(r1 / a.rq_rows, (int64_t)a.n_rq - 1);
+            for (int i = (int)(r0 / a.rq_rows); i <= i1; ++i) {
+                int spin = 0;
+                while (__hip_atomic_load(a.qflags + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != e1) {
+                    if (++spin > a.spin_limit) {   // reported, never expected (see above)
+                        const int old = __hip_atomic_fetch_add(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if (old == 0) {
+                            __hip_atomic_store(a.status + 1, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            __hip_atomic_store(a.status + 2, i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+            }
+        }
+        __syncthreads();
+    }
     constexpr int EPR = (EPN + 2 * C::NT - 1) / (2 * C::NT);
     float epv[EPR];
     _Float16 epb[EPR];
@@ -871,7 +953,10 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
         const int e = min(tid + r * 2 * C::NT, EPN - 1);
         const int ec = e & (C::BN - 1), er = max(e - 2 * C::BN, 0);
         const float *esrc = e < 2 * C::BN ? a.ws + min(tn * C::BN + ec, N - 1) : a.xs + min(tm * C::BM + er, M - 1);
-        epv[r] = *esrc;
+        if constexpr (FB != 0)   // token scales written in this launch, possibly on another XCD
+            epv[r] = __hip_atomic_load(esrc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else
+            epv[r] = *esrc;
         epb[r] = (_Float16)0.0f;
         if constexpr (BIAS) epb[r] = reinterpret_cast<const _Float16 *>(a.bias)[min(tn * C::BN + ec, N - 1)];
     }
@@ -1013,6 +1098,16 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
     };
     if (half == 0) epilogue(IC<0>{});
     else epilogue(IC<2>{});
+    if constexpr (FB != 0) {
+        if (tid == 0) {
+            const int done = __hip_atomic_fetch_add(a.qhdr + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (done == (int)gridDim.x - 1) {
+                __hip_atomic_store(a.qhdr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(a.qhdr + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(a.qhdr + 2, e1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    }
 }
 
 // four waves of 128 channels x 64 tokens: 128 channels x 256 tokens per
@@ -1124,10 +1219,18 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split) {
     return p;
 }
 
-size_t gemm_workspace_bytes() {
+// Workspace: status words (the first three for the split-k report, words
+// 4..6 the fused variant's queue, finished count and epoch) | one flag per
+// wave of every persistent workgroup | one partial tile per workgroup | one
+// flag per rotate+quantize item of the fused variant.
+constexpr int kRqFlagInts = 1 << 18;
+
+size_t gemm_split_bytes() {
     const size_t G = (size_t)full_grid();
     return kStatusBytes + G * TCfg::NW * sizeof(int) + G * TCfg::PART_INTS * sizeof(int32_t);
 }
+
+size_t gemm_workspace_bytes() { return gemm_split_bytes() + (size_t)kRqFlagInts * sizeof(int); }
 
 int gemm_spin_limit = kSpinLimit;
 int gemm_drop_signal = 0;
@@ -1184,7 +1287,7 @@ size_t gemm_scratch_bytes() { return kScratchBytes; }
 hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
                                const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
                                int32_t *status, hipStream_t stream) {
-    if (gemm_workspace_bytes() > kScratchBytes) return hipErrorInvalidValue;   // more CUs than the scratch serves
+    if (gemm_split_bytes() > kScratchBytes) return hipErrorInvalidValue;   // more CUs than the scratch serves
     void *sp = nullptr;
     hipError_t e = device_scratch(&sp);
     if (e != hipSuccess) return e;
@@ -1250,6 +1353,94 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
                     : launch_cfg<TCfg, false, true, false>(g, may_split, stream);
     return bias ? launch_cfg<TCfg, false, false, true>(g, may_split, stream)
                 : launch_cfg<TCfg, false, false, false>(g, may_split, stream);
+}
+
+namespace {
+
+template <class C, int FB>
+hipError_t launch_fused(const GemmArgs &g, bool bias, hipStream_t stream) {
+    const dim3 grid((unsigned)(g.n_rq + g.tiles_m * g.tiles_n)), block(2 * C::NT);
+    if (bias)
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, false, false, true, FB>), grid, block, 0, stream, g);
+    else
+        hipLaunchKernelGGL((w4a4_gemm_halves_kernel<C, false, false, false, FB>), grid, block, 0, stream, g);
+    return hipGetLastError();
+}
+
+template <class C>
+hipError_t launch_fused_b(const GemmArgs &g, int block, bool bias, hipStream_t stream) {
+    switch (block) {
+        case 32: return launch_fused<C, 32>(g, bias, stream);
+        case 64: return launch_fused<C, 64>(g, bias, stream);
+        case 128: return launch_fused<C, 128>(g, bias, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+// LDS bytes of the two-halves kernel's ring pool (the fused items stage
+// their fp16 rows there)
+template <class C>
+constexpr int halves_pool_bytes() {
+    return 2 * kHalfStages * C::STAGE_BYTES > 2 * C::NW * 16384 ? 2 * kHalfStages * C::STAGE_BYTES
+                                                                 : 2 * C::NW * 16384;
+}
+
+}  // namespace
+
+RqGemmPlan plan_rq_gemm(int64_t M, int64_t N, int K, int block, bool have_workspace) {
+    RqGemmPlan p{};
+    const GemmPlan g = plan_gemm(M, N, K, false);
+    if (!have_workspace || (g.kernel != 1 && g.kernel != 2) || N % 16 != 0) return p;
+    const int T = g.kernel == 2 ? 2 * TileHalf64::NT : 2 * TileHalf128::NT;
+    const int pool = g.kernel == 2 ? halves_pool_bytes<TileHalf64>() : halves_pool_bytes<TileHalf128>();
+    const int nb = K / block;
+    int R = min(T / nb, pool / (K * 2 + 4));
+    if (R < 1) return p;
+    const int64_t mpad = padded_act_rows(M);
+    const int64_t n_rq = (mpad + R - 1) / R;
+    if (n_rq > kRqFlagInts) return p;
+    p.fused = 1;
+    p.kernel = g.kernel;
+    p.tiles = g.tiles;
+    p.rq_rows = R;
+    p.n_rq = (int)n_rq;
+    return p;
+}
+
+hipError_t launch_rq_gemm(const uint16_t *X, int64_t ldx, int block, uint8_t *Xq, float *xs, const uint8_t *Wq,
+                          const float *ws, const uint16_t *bias, int64_t M, int64_t N, int K, void *Y,
+                          int64_t ldy, void *workspace, hipStream_t stream) {
+    const RqGemmPlan p = plan_rq_gemm(M, N, K, block, workspace != nullptr);
+    if (!p.fused) {   // two launches: rotate+quantize, then the linear
+        hipError_t e = launch_rotate_quant(X, ldx, nullptr, M, padded_act_rows(M), K, block, 1.0f, false, 1.0f,
+                                           Xq, xs, stream);
+        if (e != hipSuccess) return e;
+        return launch_gemm(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, false, workspace, stream);
+    }
+    GemmArgs g{};
+    g.Xq = Xq;
+    g.xs = xs;
+    g.Wq = Wq;
+    g.ws = ws;
+    g.bias = bias;
+    g.Y = Y;
+    g.ldy = ldy;
+    g.M = (int)M;
+    g.N = (int)N;
+    g.K = K;
+    g.tiles_n = (int)((N + TCfg::BN - 1) / TCfg::BN);
+    g.tiles_m = p.tiles / g.tiles_n;
+    uint8_t *wsb = reinterpret_cast<uint8_t *>(workspace);
+    g.status = reinterpret_cast<int *>(wsb);
+    g.qhdr = reinterpret_cast<int *>(wsb) + 4;
+    g.qflags = reinterpret_cast<int *>(wsb + gemm_split_bytes());
+    g.spin_limit = __atomic_load_n(&gemm_spin_limit, __ATOMIC_RELAXED);
+    g.fx = X;
+    g.ldfx = ldx;
+    g.rq_rows = p.rq_rows;
+    g.n_rq = p.n_rq;
+    if (p.kernel == 2) return launch_fused_b<TileHalf64>(g, block, bias != nullptr, stream);
+    return launch_fused_b<TileHalf128>(g, block, bias != nullptr, stream);
 }
 
 int64_t gemm_err_partials(int64_t M, int64_t N) {

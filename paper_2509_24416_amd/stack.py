@@ -7,8 +7,9 @@ qkv -> proj -> fc1 -> fc2 -> next block's qkv; proj reads the first `hidden`
 columns of the qkv output through a row stride (the attention between them
 is not part of this path).  Weights are quantized once at construction and
 stay resident; activation buffers are allocated once and reused by every
-block, so a captured graph replays the whole stack (2 launches per linear)
-with no host work and no allocation.
+block, so a captured graph replays the whole stack with no host work and no
+allocation: two launches per linear, or one where the rotate+quantize of the
+layer's input is folded into its GEMM launch (clq_w4a4_rq_linear).
 
 Swap vectors (the `s` of G = S.H, Sec. 3.3, one per layer input) are either
 gathered by each rotate+quant, or folded upstream: the layer that produces an
@@ -25,7 +26,7 @@ each.
 import torch
 
 from . import (clq_act_bytes, clq_quantize_weights, clq_rotate_quant_act, clq_w4a4_linear,
-               clq_w4a4_workspace_bytes)
+               clq_w4a4_rq_linear, clq_w4a4_workspace_bytes)
 
 LAYERS = ("qkv", "proj", "fc1", "fc2")
 
@@ -39,8 +40,13 @@ class DiTStack:
     producer's output channels by its consumer's swap vector instead of
     gathering in the consumer's rotate+quant."""
 
-    def __init__(self, weights, M, block=64, perm=None, perms=None, fold=False):
+    def __init__(self, weights, M, block=64, perm=None, perms=None, fold=False, fuse=False):
         self.M, self.block = M, block
+        # fuse: each layer's rotate+quantize and GEMM through clq_w4a4_rq_linear
+        # (one launch where its schedule allows; inputs that still gather by
+        # a swap vector take the two launches).  Off by default: on MI355X the
+        # separate launches are faster at every stack size measured.
+        self.fuse = fuse
         W0 = weights[0]["qkv"][0]
         self.hidden = W0.shape[1]
         self.mlp = weights[0]["fc1"][0].shape[0]
@@ -112,8 +118,12 @@ class DiTStack:
                 qw, b = blk[name]
                 x = self._input(j, name)
                 xq = self.xq[qw.K]
-                clq_rotate_quant_act(x, self.block, perm=self.gather[j][name], out=xq, scale_out=self.xs)
-                clq_w4a4_linear(xq, self.xs, qw, b, out=self.out[name], workspace=self.ws)
+                if self.fuse and self.gather[j][name] is None:
+                    clq_w4a4_rq_linear(x, self.block, qw, b, Xq_out=xq, scale_out=self.xs, out=self.out[name],
+                                       workspace=self.ws)
+                else:
+                    clq_rotate_quant_act(x, self.block, perm=self.gather[j][name], out=xq, scale_out=self.xs)
+                    clq_w4a4_linear(xq, self.xs, qw, b, out=self.out[name], workspace=self.ws)
                 if taps is not None and (j, name) in taps:
                     taps[(j, name)] = (x.clone(), self.out[name].clone())
 

@@ -68,6 +68,8 @@ def lib():
     L.clq_debug_get.argtypes = [i32]
     L.clq_debug_get.restype = i64
     L.clq_w4a4_schedule.argtypes = [i64, i64, i64, i32, p]
+    L.clq_w4a4_rq_linear.argtypes = [p, i64, i32, p, p, p, p, p, i64, i64, i64, p, i64, p, ctypes.c_size_t, p]
+    L.clq_w4a4_rq_schedule.argtypes = [i64, i64, i64, i32, i32, p]
     L.clq_diag_mfma_probe_bytes.restype = ctypes.c_size_t
     L.clq_diag_mfma_probe.argtypes = [p, ctypes.c_size_t, i32, i32, p, p]
     return L
@@ -75,7 +77,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 31, names
+    assert len(names) == 33, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -184,7 +186,8 @@ def test_workspace_bytes(lib):
     # 256 bytes of status words, then one partial tile (128 x 256 int32) and
     # four flags per workgroup, two workgroups per compute unit, the grid a
     # multiple of 8
-    n = lib.clq_w4a4_workspace_bytes() - 256
+    # (and 1 MiB of flags for the fused rotate+quantize items at the end)
+    n = lib.clq_w4a4_workspace_bytes() - 256 - (1 << 20)
     per_wg = 128 * 256 * 4 + 4 * 4
     assert n % per_wg == 0 and (n // per_wg) % 8 == 0
 
@@ -238,6 +241,37 @@ def test_mfma_probe_validation(lib):
     assert lib.clq_diag_mfma_probe(A, need, 0, 1, A, None) == ARG
     assert lib.clq_diag_mfma_probe(A, need, 1, 0, A, None) == ARG
     assert lib.clq_diag_mfma_probe(A + 8, need, 1, 1, A, None) == ALIGN
+
+
+def rq_schedule(lib, M, N, K, b, ws=1):
+    info = (ctypes.c_int64 * 4)()
+    assert lib.clq_w4a4_rq_schedule(M, N, K, b, ws, ctypes.cast(info, ctypes.c_void_p)) == OK
+    return list(info)
+
+
+def test_rq_schedule(lib):
+    # fused when the GEMM is the two-halves kernel, N % 16 == 0 and a
+    # workspace is given; rows per item from the workgroup's lanes (one per
+    # Hadamard block) and its LDS pool
+    assert rq_schedule(lib, 1024, 1152, 1152, 64) == [1, 7, 147, 16 * 9]      # 64-token tiles, 128 lanes
+    assert rq_schedule(lib, 1024, 3456, 1152, 64) == [1, 14, 74, 8 * 27]      # 128-token tiles, 256 lanes
+    assert rq_schedule(lib, 1024, 1152, 4608, 64) == [1, 1, 1024, 16 * 9]
+    assert rq_schedule(lib, 1024, 1152, 1152, 32) == [1, 3, 342, 16 * 9]
+    assert rq_schedule(lib, 1024, 1152, 1152, 64, ws=0)[0] == 0               # no workspace: two launches
+    assert rq_schedule(lib, 43200, 3456, 1152, 64)[0] == 0                    # persistent grid: two launches
+    assert rq_schedule(lib, 1024, 1000, 1152, 64)[0] == 0                     # N % 16 != 0
+    info = (ctypes.c_int64 * 4)()
+    assert lib.clq_w4a4_rq_schedule(1024, 1152, 1152, 48, 1, ctypes.cast(info, ctypes.c_void_p)) == BLOCK
+
+
+def test_rq_linear_validation(lib):
+    need = lib.clq_w4a4_workspace_bytes()
+    def call(X=A, ldx=1152, b=64, Xq=A, xs=A, Wq=A, ws=A, bias=None, M=8, N=16, K=1152, Y=A, ldy=16, wsp=None, wsb=0):
+        return lib.clq_w4a4_rq_linear(X, ldx, b, Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, wsp, wsb, None)
+    assert call(X=None) == NULL and call(Xq=None) == NULL and call(ws=None) == NULL
+    assert call(b=48) == BLOCK and call(K=96, ldx=96) == SHAPE and call(ldx=1000) == SHAPE
+    assert call(X=A + 8) == ALIGN and call(ldy=12) == SHAPE
+    assert call(wsp=A, wsb=need - 1) == WORKSPACE
 
 
 def test_debug_knobs(lib):
