@@ -238,6 +238,45 @@ def clq_quantize_weights(W, block, perm=None, clip_ratio=1.0, stream=None):
     return QWeight(wq, ws, N, K, block, perm, clip_ratio)
 
 
+def save_qweight(path, qw):
+    """Writes a quantized weight to a safetensors file: the opaque packed
+    codes, the scales (1/block included), the swap vector if any, and the
+    metadata (N, K, block, clip ratio, bits) keyed to the library version
+    whose layout the codes use."""
+    from safetensors.torch import save_file
+    tensors = {"wq": qw.wq.detach().cpu().contiguous(), "w_scale": qw.w_scale.detach().cpu().contiguous()}
+    if qw.perm is not None:
+        tensors["perm"] = qw.perm.detach().cpu().contiguous()
+    meta = {"format": "clq-qweight", "clq_version": str(clq_version()), "N": str(qw.N), "K": str(qw.K),
+            "block": str(qw.block), "clip_ratio": repr(float(qw.clip_ratio)), "bits": str(qw.bits)}
+    save_file(tensors, path, metadata=meta)
+
+
+def load_qweight(path, device="cuda"):
+    """Reads a file written by save_qweight onto `device`.  Raises ValueError
+    if it was written by a library version with another packed layout or its
+    sizes do not match that layout."""
+    from safetensors import safe_open
+    with safe_open(path, framework="pt") as f:
+        meta = f.metadata() or {}
+        if meta.get("format") != "clq-qweight":
+            raise ValueError(f"{path}: not a CLQ quantized weight")
+        if int(meta["clq_version"]) != clq_version():
+            raise ValueError(f"{path}: written by library version {meta['clq_version']}, "
+                             f"this is version {clq_version()} (the packed layouts differ)")
+        N, K, block, bits = int(meta["N"]), int(meta["K"]), int(meta["block"]), int(meta["bits"])
+        wq = f.get_tensor("wq")
+        ws = f.get_tensor("w_scale")
+        perm = f.get_tensor("perm") if "perm" in f.keys() else None
+    need = clq_weight_bytes(N, K) if bits == 4 else clq_weight8_bytes(N, K)
+    if wq.dtype != torch.uint8 or wq.numel() != need or ws.dtype != torch.float32 or ws.numel() != N or \
+            (perm is not None and (perm.dtype != torch.int32 or perm.numel() != K)):
+        raise ValueError(f"{path}: tensor sizes do not match N={N}, K={K}, bits={bits}")
+    dev = torch.device(device)
+    return QWeight(wq.to(dev), ws.to(dev), N, K, block, None if perm is None else perm.to(dev),
+                   float(meta["clip_ratio"]), bits)
+
+
 def clq_rotate_quant_act(X, block, perm=None, out=None, scale_out=None, stream=None):
     """Online: x~ = FWHT(gather(x, perm)) per token, quantized to int4 codes
     with one fp32 scale per token.  Returns (Xq, x_scale): Xq is the opaque

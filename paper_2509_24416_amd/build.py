@@ -40,11 +40,12 @@ def _run(cmd):
         sys.stderr.write(err + "\n")
 
 
-def build(extra_flags=(), out=LIB):
+def build(extra_flags=(), out=LIB, objdir=None):
     """Compile libclq.so (one object per source, compiled in parallel, then
-    linked); returns its path."""
+    linked); returns its path.  extra_flags go to every compile and to the
+    link."""
     from concurrent.futures import ThreadPoolExecutor
-    objdir = os.path.join(HERE, "_build")
+    objdir = objdir or os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     srcs = sources()
     objs = [os.path.join(objdir, os.path.basename(f) + ".o") for f in srcs]
@@ -54,7 +55,7 @@ def build(extra_flags=(), out=LIB):
         list(ex.map(lambda so: _run([HIPCC, *compile_flags, *extra_flags, "-c", so[0], "-o", so[1]]),
                     zip(srcs, objs)))
     tmp = out + ".tmp"
-    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
+    _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *extra_flags, *objs, "-o", tmp])
     os.replace(tmp, out)
     return out
 

@@ -466,3 +466,22 @@ def test_full_size_layer_sampled(clq, layer):
     # the exact accumulators on the same rows, through the int32 variant
     acc_gpu = clq.clq_w4a4_accum_i32(Xq, xs, qw)
     assert np.array_equal(host(acc_gpu[rows_t]), acc)
+
+
+# ---- serialised quantized weights ------------------------------------------------
+
+def test_qweight_save_load_roundtrip(clq, tmp_path):
+    N, K, block = 200, 1152, 64
+    W = workloads.weights(N, K, seed=91)
+    perm = workloads.random_perm(K, seed=92)
+    qw = clq.clq_quantize_weights(dev(W), block, dev(perm), clip_ratio=0.9)
+    path = str(tmp_path / "w.safetensors")
+    clq.save_qweight(path, qw)
+    back = clq.load_qweight(path)
+    assert (back.N, back.K, back.block, back.bits, back.clip_ratio) == (N, K, block, 4, qw.clip_ratio)
+    assert torch.equal(back.wq.cpu(), qw.wq.cpu()) and torch.equal(back.w_scale.cpu(), qw.w_scale.cpu())
+    assert torch.equal(back.perm.cpu(), qw.perm.cpu())
+    # the reloaded weight drives the linear exactly as the original
+    X = workloads.activations(64, K, "L1", seed=93)
+    Xq, xs = clq.clq_rotate_quant_act(dev(X), block, dev(perm))
+    assert np.array_equal(host(clq.clq_w4a4_accum_i32(Xq, xs, back)), host(clq.clq_w4a4_accum_i32(Xq, xs, qw)))
