@@ -97,6 +97,17 @@ __device__ __forceinline__ v4i widen16(uint32_t d0, uint32_t d1) {
                (int)(d0 & 0xF0F0F0F0u), (int)(d1 & 0xF0F0F0F0u)};
 }
 
+// two fp16 outputs fma(p, w, bias) rounded once from fp32 operands and a
+// packed fp16 bias pair (low half: first output), no separate conversions
+__device__ __forceinline__ uint32_t fma_mix2(float p0, float w0, float p1, float w1, uint32_t b) {
+    uint32_t r;
+    asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixhi_f16 %0, %4, %5, %3 op_sel:[0,0,1] op_sel_hi:[0,0,1]"
+        : "=&v"(r)
+        : "v"(p0), "v"(w0), "v"(b), "v"(p1), "v"(w1));
+    return r;
+}
+
 constexpr int kStages = 5;   // ring depth
 constexpr int kGroupM = 4;          // token panels per tile group (L2 reuse of channel panels)
 constexpr int kSpinLimit = 1 << 22;  // bound on a split-tile wait (about a second)
@@ -542,13 +553,23 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
         }
 #pragma unroll
         for (int fm = 0; fm < C::FM; ++fm) mrow[fm] = tm * C::BM + (wm * C::FM + fm) * 32 + (lane & 31);
+        // fp16 output: the lane's row pointers at its first channel, formed
+        // once per tile (a fragment's channels are a constant offset on them)
+        const int nl = tn * C::BN + wn * C::FN * 32 + h16;
+        uint16_t *rowp[C::FM];
+        float xsc[C::FM];
+#pragma unroll
+        for (int fm = 0; fm < C::FM; ++fm) {
+            rowp[fm] = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)mrow[fm] * a.ldy + nl;
+            xsc[fm] = xsm[fm] * (1.0f / 256.0f);   // accumulators hold 256 * sum
+        }
         // channel operands outer, tokens inner: each channel scale and bias
         // is loaded once and dies after its fragments
         static_for<0, C::FN>([&](auto fc) {
             constexpr int fn = decltype(fc)::value;
-            const int n0 = tn * C::BN + (wn * C::FN + fn) * 32 + h16;
+            const int n0 = nl + fn * 32;
             v4f w4[4];
-            v8h b8[2];
+            v4u b8[2];
             if constexpr (!I32OUT) {
                 // one asm block: the reads and their wait, so no use can be
                 // scheduled between them
@@ -571,24 +592,24 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
             // (element reads of the asm results stay typed: no bit casts of
             // vector elements, which this compiler mis-vectorizes)
             float wsv[16];
-            h2v bw[8];
+            uint32_t bw[8];   // bias pairs, packed fp16 (low half: even channel)
             if constexpr (!I32OUT) {
 #pragma unroll
                 for (int v = 0; v < 16; ++v) wsv[v] = w4[v / 4][v % 4];
             }
             if constexpr (!BIAS || I32OUT) {
 #pragma unroll
-                for (int v = 0; v < 8; ++v) bw[v] = h2v{(_Float16)0.0f, (_Float16)0.0f};
+                for (int v = 0; v < 8; ++v) bw[v] = 0u;
             } else if constexpr (RAGGED) {
 #pragma unroll
                 for (int v = 0; v < 16; v += 2) {
                     const int na = min(n0 + v, N - 1), nb = min(n0 + v + 1, N - 1);
-                    const _Float16 *bh = reinterpret_cast<const _Float16 *>(a.bias);
-                    bw[v / 2] = h2v{bh[na], bh[nb]};
+                    const uint16_t *bh = a.bias;
+                    bw[v / 2] = (uint32_t)bh[na] | ((uint32_t)bh[nb] << 16);
                 }
             } else {
 #pragma unroll
-                for (int v = 0; v < 8; ++v) bw[v] = h2v{b8[v / 4][2 * (v % 4)], b8[v / 4][2 * (v % 4) + 1]};
+                for (int v = 0; v < 8; ++v) bw[v] = b8[v / 4][v % 4];
             }
 #pragma unroll
             for (int fm = 0; fm < C::FM; ++fm) {
@@ -636,16 +657,10 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
                     }
                 } else {
                     uint32_t hv[8];
-                    const float xsc = xsm[fm] * (1.0f / 256.0f);   // accumulators hold 256 * sum
 #pragma unroll
-                    for (int v = 0; v < 16; v += 2) {
-                        const float p0 = (float)x[v] * xsc, p1 = (float)x[v + 1] * xsc;
-                        h2v h;
-                        h[0] = (_Float16)__builtin_fmaf(p0, wsv[v], (float)bw[v / 2][0]);
-                        h[1] = (_Float16)__builtin_fmaf(p1, wsv[v + 1], (float)bw[v / 2][1]);
-                        hv[v / 2] = __builtin_bit_cast(uint32_t, h);
-                    }
-                    uint16_t *dst = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)m * a.ldy + n0;
+                    for (int v = 0; v < 16; v += 2)
+                        hv[v / 2] = fma_mix2((float)x[v] * xsc[fm], wsv[v], (float)x[v + 1] * xsc[fm], wsv[v + 1], bw[v / 2]);
+                    uint16_t *dst = rowp[fm] + fn * 32;
                     if (m < M && n0 < N) {
                         if (!RAGGED || n0 + 16 <= N) {
                             reinterpret_cast<v4u *>(dst)[0] = v4u{hv[0], hv[1], hv[2], hv[3]};
