@@ -43,6 +43,7 @@ Prints ONE JSON line:
 """
 import argparse
 import json
+import math
 import os
 import sys
 import threading
@@ -720,6 +721,90 @@ def bench_stack(args, clq, torch, dev):
     print(json.dumps(out), flush=True)
 
 
+# Shapes for the schedule sweep: token counts from 512 to 32768 against
+# layer widths other than the block workloads' (square 2048 and 5120, a
+# 2560 -> 10240 expansion and its 10240 -> 2560 projection), plus the 1152 /
+# 4608 PixArt widths at token counts the block workloads do not use.
+SWEEP_KN = [(2048, 2048), (5120, 5120), (2560, 10240), (10240, 2560), (1152, 4608), (4608, 1152)]
+SWEEP_M = [512, 1536, 3072, 6144, 12288, 24576]
+SCHEDULES = {1: "persistent", 2: "persistent_whole_tiles", 3: "halves128", 4: "halves64"}
+
+
+def bench_gemm_schedule(args, clq, torch, dev):
+    """The GEMM's automatic kernel choice against every forced schedule (the
+    CLQ_DEBUG_GEMM_SCHEDULE knob: persistent with and without split-k, the
+    two-halves kernel on 128- and 64-token tiles) on shapes outside the block
+    workloads.  HIP events around `reps` back-to-back launches per schedule,
+    after warmup; every schedule computes the same result.  value = geometric
+    mean over the shapes of (fastest forced time / automatic time): 1.0 when
+    the automatic choice is always the fastest."""
+    reps = max(5, args.steps // 25)
+    ws = torch.zeros(clq.clq_w4a4_workspace_bytes(), dtype=torch.uint8, device=dev)
+    shapes = [(M, K, N) for K, N in SWEEP_KN for M in SWEEP_M]
+    if args.sweep_block_shapes:
+        shapes = [(l.M, l.K, l.N) for wl in (workloads.C2, workloads.C3, workloads.C4) for l in wl.layers]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    records, ratios = [], []
+    try:
+        for M, K, N in shapes:
+            W = torch.from_numpy(workloads.weights(N, K, seed=N + K)).to(dev)
+            qw = clq.clq_quantize_weights(W, 64)
+            X = torch.from_numpy(workloads.activations(M, K, "L1", seed=M + K)).to(dev)
+            Xq, xs = clq.clq_rotate_quant_act(X, 64)
+            Y = torch.empty((M, N), dtype=torch.float16, device=dev)
+            # every schedule warmed up, then three rounds over all of
+            # them; the median round per schedule (launches timed later
+            # in a sequence read faster while the clock settles)
+            forces = []
+            for force in (0, 1, 2, 3, 4):
+                clq.clq_debug_set(3, force)
+                plan = clq.clq_w4a4_schedule(M, N, K)
+                if force >= 3 and plan["kernel"] == 0:
+                    continue   # k loop too short for the two-halves kernel
+                if force == 0:
+                    auto_plan = plan
+                forces.append(force)
+                for _ in range(5):
+                    clq.clq_w4a4_linear(Xq, xs, qw, out=Y, workspace=ws)
+            rounds = {f: [] for f in forces}
+            for _ in range(3):
+                for force in forces:
+                    clq.clq_debug_set(3, force)
+                    e0.record()
+                    for _ in range(reps):
+                        clq.clq_w4a4_linear(Xq, xs, qw, out=Y, workspace=ws)
+                    e1.record()
+                    e1.synchronize()
+                    rounds[force].append(e0.elapsed_time(e1) * 1e3 / reps)
+            clq.clq_debug_set(3, 0)
+            times = {("auto" if f == 0 else SCHEDULES[f]): round(sorted(v)[1], 2) for f, v in rounds.items()}
+            forced = {k: v for k, v in times.items() if k != "auto"}
+            best = min(forced, key=forced.get)
+            ratio = forced[best] / times["auto"]
+            ratios.append(ratio)
+            records.append({"M": M, "N": N, "K": K, "auto_kernel": ["persistent", "halves128", "halves64"][auto_plan["kernel"]],
+                            "auto_split": auto_plan["split_stages"] > 0, "us": times, "fastest_forced": best,
+                            "fastest_over_auto": round(ratio, 4),
+                            "auto_TOPS": round(2.0 * M * N * K / (times["auto"] * 1e-6) / 1e12, 1)})
+            print(f"bench: gemm_schedule {M}x{N}x{K} {times}", file=sys.stderr, flush=True)
+            del X, Xq, xs, Y, W, qw
+    finally:
+        clq.clq_debug_set(3, 0)
+    gm = math.exp(sum(math.log(r) for r in ratios) / len(ratios))
+    worst = min(records, key=lambda r: r["fastest_over_auto"])
+    out = {
+        "metric": "GEMM schedule heuristics: fastest forced schedule time / automatic schedule time (geometric mean)",
+        "value": round(gm, 4), "unit": "ratio", "n_gpus": 1, "steps": reps, "warmup": 3,
+        "higher_is_better": True, "scaling": "none", "vs_baseline": None, "dtype": "int4", "data": "synthetic",
+        "config": {"workload": "gemm_schedule_sweep_block_shapes" if args.sweep_block_shapes else "gemm_schedule_sweep",
+                   "block": 64, "shapes": [list(x) for x in shapes], "parallelism": "none (one GPU)"},
+        "shapes": len(records), "auto_fastest_or_within_2pct": sum(r["fastest_over_auto"] >= 0.98 for r in records),
+        "worst": {k: worst[k] for k in ("M", "N", "K", "auto_kernel", "fastest_forced", "fastest_over_auto")},
+        "records": records, "gpu": torch.cuda.get_device_name(dev),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -736,12 +821,16 @@ def main():
     ap.add_argument("--workload", default="video_block",
                     choices=["video_block", "pixart_block", "flux_block", "video_block_w4a8", "video_block_w8a8",
                              "pixart_block_w4a8", "pixart_block_w8a8", "obs_calibration", "clps_search",
-                             "dit_stack"],
+                             "dit_stack", "gemm_schedule"],
                     help="video_block: the W4A4 hot path on the video DiT block, M = 43200 (default); "
                          "pixart_block (M = 8192) and flux_block (width 3072, M = 4608, block 128): the same "
                          "on the other block configurations; *_w4a8 / *_w8a8: 8-bit activations (and "
                          "weights); obs_calibration: the OBS channel-score pass; clps_search: the CLPS "
-                         "clip search; dit_stack: the 28-block stack, one HIP graph per step")
+                         "clip search; dit_stack: the 28-block stack, one HIP graph per step; "
+                         "gemm_schedule: the GEMM's automatic kernel choice against every forced schedule "
+                         "on shapes outside the block workloads")
+    ap.add_argument("--sweep-block-shapes", action="store_true",
+                    help="gemm_schedule: sweep the block workloads' own layer shapes instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 5 times (reference for the HBM "
                          "byte counters) and exit")
@@ -774,6 +863,9 @@ def main():
         return
     if args.workload == "dit_stack":
         bench_stack(args, clq, torch, dev)
+        return
+    if args.workload == "gemm_schedule":
+        bench_gemm_schedule(args, clq, torch, dev)
         return
 
     base = args.workload.split("_w")[0]

@@ -399,12 +399,21 @@ clq_status clq_clps_search(const void *X, int64_t ldx, const void *W, const floa
  *   CLQ_DEBUG_SPLIT_DROP_SIGNAL 1: split-k contributors never signal, so every
  *                               owner's wait runs out (tests of the failure
  *                               report only: outputs are then wrong).
+ *   CLQ_DEBUG_GEMM_SCHEDULE     the W4A4 GEMM's kernel choice: 0 automatic
+ *                               (default); 1 the persistent kernel with its
+ *                               split-k rule; 2 the persistent kernel, whole
+ *                               tiles only; 3 the two-halves kernel on
+ *                               128-token tiles; 4 on 64-token tiles (3 and 4
+ *                               fall back to automatic when K < 256).  Every
+ *                               choice gives the same results; for measuring
+ *                               the schedule heuristics.
  * clq_debug_set returns CLQ_ERR_ARG for an unknown knob or a value out of
  * range; clq_debug_get returns the current value, or -1 for an unknown knob. */
 typedef enum {
     CLQ_DEBUG_SYNC = 0,
     CLQ_DEBUG_SPLIT_SPIN_LIMIT = 1,
-    CLQ_DEBUG_SPLIT_DROP_SIGNAL = 2
+    CLQ_DEBUG_SPLIT_DROP_SIGNAL = 2,
+    CLQ_DEBUG_GEMM_SCHEDULE = 3
 } clq_debug_knob;
 
 clq_status clq_debug_set(int32_t knob, int64_t value);

@@ -134,6 +134,7 @@ hipError_t launch_mfma_probe(const void *ops, int iters, int *sink, int grid, hi
 // contributors from signalling; read at each launch.
 extern int gemm_spin_limit;
 extern int gemm_drop_signal;
+extern int gemm_force_schedule;   // 0 automatic, 1..4 a forced GEMM kernel choice (debug knob)
 
 // The W4A4 GEMM's schedule for a shape.  kernel: 0 the persistent kernel
 // (256-token tiles), 1 / 2 the two-halves kernel with 128- / 64-token tiles;
@@ -141,8 +142,13 @@ extern int gemm_drop_signal;
 // first rounds); sk: k-stages split over the grid; grid: workgroups.
 struct GemmPlan {
     int kernel, tiles_m, tiles, dp, sk, grid;
+    bool may_split;   // persistent kernel: whether the launch may split along k
 };
+// force: the schedule knob's value (0 automatic); the overload without it
+// reads the knob
 GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split);
+GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split, int force);
+int gemm_schedule_knob();
 
 // Rotate+quantize folded into the GEMM (the two-halves kernel's fused
 // variant): fused = 0 when the shape or arguments take two launches instead.
@@ -167,6 +173,10 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
                        const float *ws, const uint16_t *bias, int64_t M, int64_t N,
                        int K, void *Y, int64_t ldy, bool i32out, void *workspace,
                        hipStream_t stream);
+hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
+                       const float *ws, const uint16_t *bias, int64_t M, int64_t N,
+                       int K, void *Y, int64_t ldy, bool i32out, void *workspace,
+                       hipStream_t stream, int force);
 
 // The same product, reduced to the squared error against an fp32 target:
 // partials[t] (t < gemm_err_partials(M, N)) receives the fp64 sum of

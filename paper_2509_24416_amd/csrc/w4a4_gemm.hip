@@ -805,7 +805,15 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
     const int w8 = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = w8 / C::NW, wm = w8 % C::NW;   // one channel panel per tile: wn = 0
     const int M = a.M, N = a.N, nks = a.K >> 6;
-    int L = blockIdx.x;
+    // tile order: workgroups are dealt to the 8 XCDs round-robin; each XCD
+    // takes a contiguous run of tiles (in the grouped order below), so the
+    // operand panels a run shares stay in that XCD's L2
+    int L;
+    {
+        const int G = gridDim.x, x = blockIdx.x & 7, j = blockIdx.x >> 3;
+        const int per = G >> 3, rem = G & 7;
+        L = x * per + min(x, rem) + j;
+    }
     int e1 = 0;   // fused: this call's epoch + 1, the value of a published item's flag
     if constexpr (FB != 0) {
         static_assert(!I32OUT, "the fused variant writes fp16");
@@ -1202,20 +1210,34 @@ hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
 
 }  // namespace
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split) {
+int gemm_schedule_knob() { return __atomic_load_n(&gemm_force_schedule, __ATOMIC_RELAXED); }
+
+GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split) { return plan_gemm(M, N, K, may_split, gemm_schedule_knob()); }
+
+// force: 0 automatic, 1 persistent, 2 persistent whole tiles, 3 / 4 the
+// two-halves kernel on 128- / 64-token tiles (the debug knob)
+GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split, int force) {
     GemmPlan p{};
     const int tiles_n = (int)((N + TCfg::BN - 1) / TCfg::BN);
     const int ntiles = (int)((M + TCfg::BM - 1) / TCfg::BM) * tiles_n;
-    // at most 1.25 256-token tiles per compute unit and a k loop worth
-    // halving: the two-halves kernel.  Just past one tile per CU the
-    // persistent kernel doubles up on a few CUs while the rest idle; the
-    // two-halves kernel fills one round of two workgroups per CU and runs a
-    // short second round on the remaining quarter at most.
-    if (4 * ntiles <= 5 * device_cus() && (K >> 6) >= kHalvesMinStages) {
+    const bool halves_ok = (K >> 6) >= kHalvesMinStages;
+    // the two-halves kernel: at most 1.25 256-token tiles per compute unit
+    // (just past one tile per CU the persistent kernel doubles up on a few
+    // CUs while the rest idle; the two-halves kernel fills one round of two
+    // workgroups per CU and runs a short second round on the remaining
+    // quarter at most), or long k loops (K >= 2048) unless the layer is
+    // more than four times wider than deep.  On such loops its 128-token
+    // tiles with the k range split between two halves of the workgroup
+    // beat the persistent kernel at every tile count measured, 2-16% (the
+    // schedule sweep over 36 shapes from 512 to 24576 tokens); wide, shallow
+    // layers keep the persistent kernel's grouped weight reuse.
+    const bool deep = K >= 2048 && N < 4 * (int64_t)K;
+    const bool halves = halves_ok && (force >= 3 || (force == 0 && (4 * ntiles <= 5 * device_cus() || deep)));
+    if (halves) {
         // 128-token tiles (two four-wave workgroups per compute unit), or 64
         // while those would fill at most half the compute units
         const int tm128 = (int)((M + TileHalf128::BM - 1) / TileHalf128::BM);
-        if (2 * tm128 * tiles_n <= device_cus()) {
+        if (force == 4 || (force != 3 && 2 * tm128 * tiles_n <= device_cus())) {
             p.kernel = 2;
             p.tiles_m = (int)((M + TileHalf64::BM - 1) / TileHalf64::BM);
         } else {
@@ -1230,7 +1252,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split) {
     p.kernel = 0;
     p.tiles_m = (int)((M + TCfg::BM - 1) / TCfg::BM);
     p.tiles = ntiles;
-    plan_persistent(ntiles, K >> 6, may_split, p.dp, p.sk, p.grid);
+    p.may_split = may_split && force != 2;
+    plan_persistent(ntiles, K >> 6, p.may_split, p.dp, p.sk, p.grid);
     return p;
 }
 
@@ -1248,6 +1271,7 @@ size_t gemm_split_bytes() {
 size_t gemm_workspace_bytes() { return gemm_split_bytes() + (size_t)kRqFlagInts * sizeof(int); }
 
 int gemm_spin_limit = kSpinLimit;
+int gemm_force_schedule = 0;
 int gemm_drop_signal = 0;
 
 // ---- the allocation-free GEMM entry point's scratch ---------------------------
@@ -1306,7 +1330,8 @@ hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t
     void *sp = nullptr;
     hipError_t e = device_scratch(&sp);
     if (e != hipSuccess) return e;
-    const GemmPlan pl = plan_gemm(M, N, K, true);
+    const int force = gemm_schedule_knob();
+    const GemmPlan pl = plan_gemm(M, N, K, true, force);
     const int split = pl.sk > 0;
     if (split) {
         // status words and flags start at zero on every split call
@@ -1315,7 +1340,7 @@ hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t
                            reinterpret_cast<int *>(sp), nwords);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    e = launch_gemm(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, false, sp, stream);
+    e = launch_gemm(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, false, sp, stream, force);
     if (e != hipSuccess || status == nullptr) return e;
     hipLaunchKernelGGL(status_copy_kernel, dim3(1), dim3(64), 0, stream, reinterpret_cast<const int *>(sp), status,
                        split);
@@ -1325,6 +1350,12 @@ hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t
 hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
                        const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
                        bool i32out, void *workspace, hipStream_t stream) {
+    return launch_gemm(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, i32out, workspace, stream, gemm_schedule_knob());
+}
+
+hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                       const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy,
+                       bool i32out, void *workspace, hipStream_t stream, int force) {
     GemmArgs g{};
     g.Xq = Xq;
     g.xs = xs;
@@ -1347,8 +1378,8 @@ hipError_t launch_gemm(const uint8_t *Xq, const float *xs, const uint8_t *Wq, co
     g.part = workspace ? reinterpret_cast<int32_t *>(wsb + kStatusBytes + G * TCfg::NW * sizeof(int)) : nullptr;
     g.spin_limit = __atomic_load_n(&gemm_spin_limit, __ATOMIC_RELAXED);
     g.drop_signal = __atomic_load_n(&gemm_drop_signal, __ATOMIC_RELAXED);
-    const bool may_split = workspace != nullptr;
-    const GemmPlan pl = plan_gemm(M, N, K, may_split);
+    const GemmPlan pl = plan_gemm(M, N, K, workspace != nullptr, force);
+    const bool may_split = pl.may_split;
     if (pl.kernel == 2) {
         g.tiles_m = pl.tiles_m;
         return launch_halves<TileHalf64>(g, i32out, bias != nullptr, N % 16 != 0, stream);

@@ -218,17 +218,28 @@ def test_schedule(lib):
     assert schedule(lib, 4352, 2048, 2432)[:2] == [1, 34 * 16]
     # few tiles: 64-token tiles
     assert schedule(lib, 1024, 1152, 1152)[:2] == [2, 16 * 9]
-    # the 28-block stack's fc2 at 16384 tokens: 576 tiles, every k-stage split
-    k, tiles, dp, sk, grid = schedule(lib, 16384, 1152, 4608)
-    assert (k, tiles, dp, sk, grid) == (0, 576, 0, 576 * 72, 512)
-    assert schedule(lib, 16384, 1152, 4608, ws=0) == [0, 576, 576, 0, 512]
+    # long k loops (K >= 2048, N < 4 K): the two-halves kernel at any tile
+    # count -- the 28-block stack's fc2 at 16384 tokens, the video block's
+    # fc2 (43200 tokens), three of the FLUX-style block's linears
+    assert schedule(lib, 16384, 1152, 4608)[:2] == [1, 128 * 9]
+    assert schedule(lib, 43200, 1152, 4608)[:2] == [1, 338 * 9]
+    for N, K in ((9216, 3072), (3072, 3072), (3072, 12288)):
+        assert schedule(lib, 4608, N, K)[:2] == [1, 36 * (N // 128)]
+    # wide, shallow layers (N >= 4 K) keep the persistent kernel: the
+    # FLUX-style fc1, 12288 x 10240 x 2560
+    assert schedule(lib, 4608, 12288, 3072)[:2] == [0, 18 * 96]
+    assert schedule(lib, 12288, 10240, 2560)[0] == 0
+    # 576 tiles of 30 stages: every k-stage split
+    k, tiles, dp, sk, grid = schedule(lib, 16384, 1152, 1920)
+    assert (k, tiles, dp, sk, grid) == (0, 576, 0, 576 * 30, 512)
+    assert schedule(lib, 16384, 1152, 1920, ws=0) == [0, 576, 576, 0, 512]
     # 600 tiles of 24 stages: both rounds split, 28.1 stages per workgroup
     assert schedule(lib, 6400, 3072, 1536) == [0, 600, 0, 600 * 24, 512]
     # 1100 tiles: one whole round first, the last 588 tiles split
     assert schedule(lib, 11264, 3200, 1536) == [0, 1100, 512, 588 * 24, 512]
     # the PixArt block linears (M = 8192) and the video ones (M = 43200)
     # take whole tiles on the persistent grid
-    for M, N, K in ((8192, 3456, 1152), (8192, 4608, 1152), (43200, 3456, 1152), (43200, 1152, 4608)):
+    for M, N, K in ((8192, 3456, 1152), (8192, 4608, 1152), (43200, 3456, 1152), (43200, 4608, 1152)):
         k, tiles, dp, sk, grid = schedule(lib, M, N, K)
         assert k == 0 and sk == 0 and dp == tiles
 
@@ -290,6 +301,34 @@ def test_debug_knobs(lib):
         assert lib.clq_debug_set(DROP, 0) == OK
         assert lib.clq_debug_set(SYNC, 0) == OK
     assert lib.clq_debug_get(SYNC) == 0
+
+
+def test_schedule_knob(lib):
+    SCHED = 3
+    assert lib.clq_debug_get(SCHED) == 0
+    assert lib.clq_debug_set(SCHED, -1) == ARG and lib.clq_debug_set(SCHED, 5) == ARG
+    try:
+        # 1: persistent with its split rule; 2: persistent, whole tiles only
+        assert lib.clq_debug_set(SCHED, 1) == OK and lib.clq_debug_get(SCHED) == 1
+        assert schedule(lib, 1024, 1152, 1152) == [0, 36, 36, 0, 40]
+        assert schedule(lib, 16384, 1152, 4608) == [0, 576, 0, 576 * 72, 512]
+        assert lib.clq_debug_set(SCHED, 2) == OK
+        assert schedule(lib, 16384, 1152, 4608) == [0, 576, 576, 0, 512]
+        # 3 / 4: the two-halves kernel on 128- / 64-token tiles, any tile count
+        assert lib.clq_debug_set(SCHED, 3) == OK
+        assert schedule(lib, 43200, 3456, 1152)[:2] == [1, 338 * 27]
+        assert schedule(lib, 1024, 1152, 1152)[:2] == [1, 8 * 9]
+        assert lib.clq_debug_set(SCHED, 4) == OK
+        assert schedule(lib, 43200, 3456, 1152)[:2] == [2, 675 * 27]
+        # k loops too short to halve (K < 256) keep the automatic choice
+        assert schedule(lib, 1024, 1152, 192)[0] == 0
+        # the fused path follows the GEMM's schedule
+        assert rq_schedule(lib, 1024, 1152, 1152, 64)[0] == 1
+        assert lib.clq_debug_set(SCHED, 2) == OK
+        assert rq_schedule(lib, 1024, 1152, 1152, 64)[0] == 0
+    finally:
+        assert lib.clq_debug_set(SCHED, 0) == OK
+    assert schedule(lib, 1024, 1152, 1152)[:2] == [2, 16 * 9]
 
 
 def test_accum_and_unswizzle_validation(lib):

@@ -175,9 +175,9 @@ def test_accum_i32_bitexact(clq, M, N, K, workspace):
 # with one workspace: the split sums equal the whole-tile sums bit for bit
 # and the oracle's on sampled rows.  (6400, 3072, 1536): 600 tiles, both
 # rounds split; (6300, 3000, 1536): the same with ragged edges; (11264,
-# 3200, 1536): one whole round, then 588 split tiles; (16384, 1152, 4608):
-# the 28-block stack's fc2 at 16384 tokens.
-SPLIT_SHAPES = [(6400, 3072, 1536), (6300, 3000, 1536), (11264, 3200, 1536), (16384, 1152, 4608)]
+# 3200, 1536): one whole round, then 588 split tiles; (16384, 1152, 1920):
+# 576 tiles of 30 stages, every stage split.
+SPLIT_SHAPES = [(6400, 3072, 1536), (6300, 3000, 1536), (11264, 3200, 1536), (16384, 1152, 1920)]
 
 
 @pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
@@ -485,3 +485,43 @@ def test_qweight_save_load_roundtrip(clq, tmp_path):
     X = workloads.activations(64, K, "L1", seed=93)
     Xq, xs = clq.clq_rotate_quant_act(dev(X), block, dev(perm))
     assert np.array_equal(host(clq.clq_w4a4_accum_i32(Xq, xs, back)), host(clq.clq_w4a4_accum_i32(Xq, xs, qw)))
+
+
+# Every schedule the GEMM can take (the debug knob forces one: the persistent
+# kernel with and without its split rule, the two-halves kernel on 128- and
+# 64-token tiles) gives the same exact integer sums, and fp16 outputs within
+# the tolerance of the oracle, on shapes that the automatic choice sends to
+# each of them: few tiles, a ragged channel edge, a split-k shape and a
+# large one.
+FORCED_SHAPES = [(1024, 1152, 1152), (300, 1000, 640), (4096, 3456, 1152), (16384, 1152, 4608), (8192, 4608, 1152)]
+
+
+@pytest.mark.parametrize("M,N,K", FORCED_SHAPES)
+def test_forced_schedules_agree(clq, M, N, K):
+    block = 64
+    X = workloads.activations(M, K, "L1", seed=M + 1)
+    W = workloads.weights(N, K, seed=N + 1)
+    b = workloads.bias(N, seed=N + 2)
+    qw = clq.clq_quantize_weights(dev(W), block)
+    Xq, xs = clq.clq_rotate_quant_act(dev(X), block)
+    rows = np.unique(np.r_[0:3, M // 2, M - 3:M])
+    r = oracle.linear(X[rows], W, b, block)
+    ref = None
+    try:
+        for force in (0, 1, 2, 3, 4):
+            clq.clq_debug_set(3, force)
+            plan = clq.clq_w4a4_schedule(M, N, K)
+            expect = {1: 0, 2: 0, 3: 1, 4: 2}.get(force)
+            assert expect is None or plan["kernel"] == expect, (force, plan)
+            ws = torch.zeros(clq.clq_w4a4_workspace_bytes(), dtype=torch.uint8, device="cuda")
+            acc = host(clq.clq_w4a4_accum_i32(Xq, xs, qw, workspace=ws))
+            Y = host(clq.clq_w4a4_linear(Xq, xs, qw, dev(b), workspace=ws))
+            assert clq.clq_w4a4_workspace_status(ws) == [0, 0, 0]
+            if ref is None:
+                ref = acc
+                assert np.array_equal(acc[rows], r["acc"])
+            else:
+                assert np.array_equal(acc, ref), force
+            assert oracle.err_metric(Y[rows].astype(np.float64), r["y64"], r["p64"], b) <= TOL, force
+    finally:
+        clq.clq_debug_set(3, 0)
