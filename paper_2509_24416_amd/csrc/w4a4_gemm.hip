@@ -1136,6 +1136,8 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
 // four waves of 128 channels x 64 tokens: 128 channels x 256 tokens per
 // workgroup, two workgroups per compute unit
 using TCfg = Tile<1, 4, 4, 2, 2>;
+// the schedule counts channel tiles once for every kernel
+static_assert(TCfg::BN == TileHalf128::BN && TCfg::BN == TileHalf64::BN, "one channel-tile width");
 
 int device_cus() {
     static int cus = 0;
