@@ -1227,13 +1227,14 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split, int force) {
     // (just past one tile per CU the persistent kernel doubles up on a few
     // CUs while the rest idle; the two-halves kernel fills one round of two
     // workgroups per CU and runs a short second round on the remaining
-    // quarter at most), or long k loops (K >= 2048) unless the layer is
-    // more than four times wider than deep.  On such loops its 128-token
-    // tiles with the k range split between two halves of the workgroup
-    // beat the persistent kernel at every tile count measured, 2-16% (the
-    // schedule sweep over 36 shapes from 512 to 24576 tokens); wide, shallow
-    // layers keep the persistent kernel's grouped weight reuse.
-    const bool deep = K >= 2048 && N < 4 * (int64_t)K;
+    // quarter at most), or long k loops (K >= 2048).  On such loops its
+    // 128-token tiles with the k range split between two halves of the
+    // workgroup beat the persistent kernel at every tile count measured,
+    // 2-16% (the schedule sweep over 36 shapes from 512 to 24576 tokens),
+    // except on layers more than four times wider than deep at more than 8
+    // tiles per compute unit, where the persistent kernel's grouped weight
+    // reuse wins.
+    const bool deep = K >= 2048 && (N < 4 * (int64_t)K || ntiles <= 8 * device_cus());
     const bool halves = halves_ok && (force >= 3 || (force == 0 && (4 * ntiles <= 5 * device_cus() || deep)));
     if (halves) {
         // 128-token tiles (two four-wave workgroups per compute unit), or 64
@@ -1264,6 +1265,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int K, bool may_split, int force) {
 // wave of every persistent workgroup | one partial tile per workgroup | one
 // flag per rotate+quantize item of the fused variant.
 constexpr int kRqFlagInts = 1 << 18;
+constexpr int kFusedMinRows = 4;   // rows per rotate+quantize item of the fused variant
 
 size_t gemm_split_bytes() {
     const size_t G = (size_t)full_grid();
@@ -1443,7 +1445,9 @@ RqGemmPlan plan_rq_gemm(int64_t M, int64_t N, int K, int block, bool have_worksp
     const int pool = g.kernel == 2 ? halves_pool_bytes<TileHalf64>() : halves_pool_bytes<TileHalf128>();
     const int nb = K / block;
     int R = min(T / nb, pool / (K * 2 + 4));
-    if (R < 1) return p;
+    // items of fewer rows leave most of a workgroup idle on a latency-bound
+    // load: long rows take the two launches
+    if (R < kFusedMinRows) return p;
     const int64_t mpad = padded_act_rows(M);
     const int64_t n_rq = (mpad + R - 1) / R;
     if (n_rq > kRqFlagInts) return p;

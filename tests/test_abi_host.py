@@ -220,15 +220,16 @@ def test_schedule(lib):
     assert schedule(lib, 1024, 1152, 1152)[:2] == [2, 16 * 9]
     # long k loops (K >= 2048, N < 4 K): the two-halves kernel at any tile
     # count -- the 28-block stack's fc2 at 16384 tokens, the video block's
-    # fc2 (43200 tokens), three of the FLUX-style block's linears
+    # fc2 (43200 tokens), the FLUX-style block's linears
     assert schedule(lib, 16384, 1152, 4608)[:2] == [1, 128 * 9]
     assert schedule(lib, 43200, 1152, 4608)[:2] == [1, 338 * 9]
     for N, K in ((9216, 3072), (3072, 3072), (3072, 12288)):
         assert schedule(lib, 4608, N, K)[:2] == [1, 36 * (N // 128)]
-    # wide, shallow layers (N >= 4 K) keep the persistent kernel: the
-    # FLUX-style fc1, 12288 x 10240 x 2560
-    assert schedule(lib, 4608, 12288, 3072)[:2] == [0, 18 * 96]
-    assert schedule(lib, 12288, 10240, 2560)[0] == 0
+    # wide, shallow layers (N >= 4 K) too up to 8 tiles of 256 tokens per
+    # CU (the FLUX-style fc1: 6.75), the persistent kernel beyond
+    assert schedule(lib, 4608, 12288, 3072)[:2] == [1, 36 * 96]
+    assert schedule(lib, 6144, 10240, 2560)[:2] == [1, 48 * 80]
+    assert schedule(lib, 12288, 10240, 2560)[:2] == [0, 48 * 80]
     # 576 tiles of 30 stages: every k-stage split
     k, tiles, dp, sk, grid = schedule(lib, 16384, 1152, 1920)
     assert (k, tiles, dp, sk, grid) == (0, 576, 0, 576 * 30, 512)
@@ -266,8 +267,10 @@ def test_rq_schedule(lib):
     # Hadamard block) and its LDS pool
     assert rq_schedule(lib, 1024, 1152, 1152, 64) == [1, 7, 147, 16 * 9]      # 64-token tiles, 128 lanes
     assert rq_schedule(lib, 1024, 3456, 1152, 64) == [1, 14, 74, 8 * 27]      # 128-token tiles, 256 lanes
-    assert rq_schedule(lib, 1024, 1152, 4608, 64) == [1, 1, 1024, 16 * 9]
-    assert rq_schedule(lib, 1024, 1152, 1152, 32) == [1, 3, 342, 16 * 9]
+    assert rq_schedule(lib, 1024, 1152, 4608, 64) == [0, 0, 0, 0]             # items of < 4 rows: two launches
+    assert rq_schedule(lib, 1024, 1152, 2048, 64) == [1, 4, 256, 16 * 9]      # 32 blocks a row, 128 lanes: 4 rows
+    assert rq_schedule(lib, 1024, 1152, 1152, 32) == [0, 0, 0, 0]             # 36 blocks, 128 lanes: 3 rows
+    assert rq_schedule(lib, 1024, 3456, 1152, 32) == [1, 7, 147, 8 * 27]      # 256 lanes: 7 rows
     assert rq_schedule(lib, 1024, 1152, 1152, 64, ws=0)[0] == 0               # no workspace: two launches
     assert rq_schedule(lib, 43200, 3456, 1152, 64)[0] == 0                    # persistent grid: two launches
     assert rq_schedule(lib, 1024, 1000, 1152, 64)[0] == 0                     # N % 16 != 0
