@@ -23,8 +23,10 @@
  *   - All data pointers are DEVICE pointers (hipMalloc'd or equivalent) unless
  *     stated; fp16 means IEEE binary16 stored as 2-byte values.
  *   - The caller owns and allocates every buffer.  The library allocates no
- *     device memory, keeps no global state on the device, never synchronises,
- *     and never writes to its inputs.  Each call validates its arguments on the host,
+ *     device memory, keeps no global state on the device (except the fixed
+ *     scratch array of clq_w4a4_linear_noalloc), never synchronises (except
+ *     in the synchronous debug mode, CLQ_DEBUG_SYNC), and never writes to
+ *     its inputs.  Each call validates its arguments on the host,
  *     then enqueues its kernels on `stream` and returns; results are
  *     available once the stream reaches that point.
  *   - On a validation error nothing is enqueued and the error code is
