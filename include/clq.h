@@ -243,6 +243,57 @@ clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K,
 clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K,
                              void *Xq_canonical, hipStream_t stream);
 
+/* ---- W4A4 with the codes stored as fp6 (the same Sec. 3.1 Eq. (1) 4-bit
+ * grid and Sec. 3.3 rotation; a different storage of the codes) -----------
+ * gfx950 has no 4-bit integer matrix instruction.  Its fp6 format e2m3 holds
+ * every code -7..7 exactly, and its fp6 matrix instruction multiplies at
+ * twice the int8 rate; a product of two codes is an integer of magnitude at
+ * most 49, so fp32 accumulation of any k loop up to 32768 codes is exact.
+ * These entry points compute exactly what their int4 counterparts compute
+ * (same codes, scales, integer sums and epilogue), with Xq / Wq in an opaque
+ * fp6 layout of 24 bytes per 32 codes (1.5 times the packed int4 bytes).
+ * clq_w4a4_linear_f6 needs no workspace and runs whole tiles only; K >= 128.
+ * The two layouts convert one way with clq_f6_from_int4, and back to
+ * canonical packed codes with clq_unswizzle_f6. */
+size_t clq_weight_bytes_f6(int64_t N, int64_t K);   /* 0 if the shape is invalid */
+size_t clq_act_bytes_f6(int64_t M, int64_t K);      /* 0 if the shape is invalid */
+
+/* As clq_quantize_weights; Wq receives clq_weight_bytes_f6(N, K) bytes. */
+clq_status clq_quantize_weights_f6(const void *W, const int32_t *perm, int64_t N,
+                                   int64_t K, int32_t block, float clip_ratio,
+                                   void *Wq, float *w_scale, hipStream_t stream);
+
+/* As clq_rotate_quant_act; Xq receives clq_act_bytes_f6(M, K) bytes. */
+clq_status clq_rotate_quant_act_f6(const void *X, int64_t ldx, const int32_t *perm,
+                                   int64_t M, int64_t K, int32_t block, void *Xq,
+                                   float *x_scale, hipStream_t stream);
+
+/* As clq_w4a4_linear on the fp6 layouts, without a workspace (Eq. (1): the
+ * integer product times x_scale[m] and w_scale[n], plus bias).  K >= 128;
+ * the output rule is clq_w4a4_linear's, with acc exact for every K. */
+clq_status clq_w4a4_linear_f6(const void *Xq, const float *x_scale, const void *Wq,
+                              const float *w_scale, const void *bias, int64_t M,
+                              int64_t N, int64_t K, void *Y, int64_t ldy,
+                              hipStream_t stream);
+
+/* Diagnostic: the exact integer sums of the fp6 operands as int32 [M][N],
+ * row stride ldacc (elements, a multiple of 4).  K >= 128. */
+clq_status clq_w4a4_accum_f6(const void *Xq, const void *Wq, int64_t M, int64_t N,
+                             int64_t K, int32_t *acc, int64_t ldacc, hipStream_t stream);
+
+/* Diagnostic: canonical packed codes (the clq_unswizzle_* convention, uint8
+ * [rows][K/2], 16-byte aligned) of an fp6 operand; weights = 1 for a
+ * clq_quantize_weights_f6 buffer, 0 for a clq_rotate_quant_act_f6 buffer. */
+clq_status clq_unswizzle_f6(const void *q6, int64_t rows, int64_t K, int32_t weights,
+                            void *canonical, hipStream_t stream);
+
+/* Converts a packed int4 buffer (clq_quantize_weights with weights = 1, or
+ * clq_rotate_quant_act with weights = 0; rows N or M) into the fp6 layout,
+ * the padding rows included: q6 receives clq_weight_bytes_f6 or
+ * clq_act_bytes_f6 bytes.  Reads q4 only. */
+clq_status clq_f6_from_int4(const void *q4, int64_t rows, int64_t K, int32_t weights,
+                            void *q6, hipStream_t stream);
+
 /* ---- 8-bit settings: W4A8 and W8A8 (Sec. 4.1 runs the method at W8A8,
  * W4A8 and W4A4; Sec. 3.1 Eq. (1) with n = 8) -------------------------------
  * The same rotation and quantizer with qmax = 127: q = clamp(rne(x~ * r),

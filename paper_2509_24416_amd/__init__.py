@@ -89,13 +89,25 @@ _lib.clq_diag_mfma_probe_bytes.argtypes = []
 _lib.clq_diag_mfma_probe.argtypes = [_p, ctypes.c_size_t, _i32, _i32, _p, _p]
 _lib.clq_debug_get.argtypes = [_i32]
 _lib.clq_debug_get.restype = _i64
+_lib.clq_weight_bytes_f6.restype = ctypes.c_size_t
+_lib.clq_weight_bytes_f6.argtypes = [_i64, _i64]
+_lib.clq_act_bytes_f6.restype = ctypes.c_size_t
+_lib.clq_act_bytes_f6.argtypes = [_i64, _i64]
+_lib.clq_quantize_weights_f6.argtypes = [_p, _p, _i64, _i64, _i32, _f32, _p, _p, _p]
+_lib.clq_rotate_quant_act_f6.argtypes = [_p, _i64, _p, _i64, _i64, _i32, _p, _p, _p]
+_lib.clq_w4a4_linear_f6.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i64, _p]
+_lib.clq_w4a4_accum_f6.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _p]
+_lib.clq_unswizzle_f6.argtypes = [_p, _i64, _i64, _i32, _p, _p]
+_lib.clq_f6_from_int4.argtypes = [_p, _i64, _i64, _i32, _p, _p]
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
            "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
            "clq_quantize_weights8", "clq_a8_linear", "clq_a8_accum_i32", "clq_unswizzle_act8",
            "clq_unswizzle_weights8", "clq_clps_search", "clq_w4a4_workspace_status", "clq_debug_set",
            "clq_w4a4_schedule", "clq_w4a4_linear_noalloc", "clq_diag_mfma_probe",
-           "clq_w4a4_rq_linear", "clq_w4a4_rq_schedule"):
+           "clq_w4a4_rq_linear", "clq_w4a4_rq_schedule", "clq_quantize_weights_f6",
+           "clq_rotate_quant_act_f6", "clq_w4a4_linear_f6", "clq_w4a4_accum_f6", "clq_unswizzle_f6",
+           "clq_f6_from_int4"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -107,7 +119,9 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_clps_workspace_bytes", "clq_clps_search", "clq_w4a4_workspace_status",
            "clq_debug_set", "clq_debug_get", "clq_w4a4_schedule", "clq_w4a4_linear_noalloc",
            "clq_diag_mfma_probe_bytes", "clq_diag_mfma_probe", "clq_w4a4_rq_linear",
-           "clq_w4a4_rq_schedule")
+           "clq_w4a4_rq_schedule", "clq_weight_bytes_f6", "clq_act_bytes_f6", "clq_quantize_weights_f6",
+           "clq_rotate_quant_act_f6", "clq_w4a4_linear_f6", "clq_w4a4_accum_f6", "clq_unswizzle_f6",
+           "clq_f6_from_int4")
 
 CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
 
@@ -217,7 +231,7 @@ class QWeight:
     block: int
     perm: torch.Tensor = None
     clip_ratio: float = 1.0
-    bits: int = 4           # 4: clq_quantize_weights, 8: clq_quantize_weights8
+    bits: int = 4           # 4: clq_quantize_weights, 6: clq_quantize_weights_f6, 8: clq_quantize_weights8
 
 
 def clq_quantize_weights(W, block, perm=None, clip_ratio=1.0, stream=None):
@@ -369,6 +383,8 @@ def clq_w4a4_linear(Xq, x_scale, qw, bias=None, out=None, stream=None, workspace
     workspace: None (the per-device default), False (none), or a zero-filled
     uint8 tensor of clq_w4a4_workspace_bytes() bytes."""
     M = _check_xq(Xq, x_scale, qw.K)
+    if qw.bits != 4:
+        raise ValueError("qw must come from clq_quantize_weights (use clq_w4a4_linear_f6 for fp6 weights)")
     if bias is not None:
         _dev(bias, "bias", torch.float16)
         if bias.shape != (qw.N,) or not bias.is_contiguous():
@@ -587,6 +603,123 @@ def clq_quantize_weights8(W, block, perm=None, clip_ratio=1.0, stream=None):
     _check(_lib.clq_quantize_weights8(_ptr(W), _ptr(perm), N, K, block, clip_ratio, _ptr(wq), _ptr(ws),
                                       _stream(stream)), "clq_quantize_weights8")
     return QWeight(wq, ws, N, K, block, perm, clip_ratio, 8)
+
+
+# ---- W4A4 with the codes stored as fp6 (e2m3) --------------------------------------
+
+def clq_weight_bytes_f6(N, K):
+    return int(_lib.clq_weight_bytes_f6(N, K))
+
+
+def clq_act_bytes_f6(M, K):
+    return int(_lib.clq_act_bytes_f6(M, K))
+
+
+def clq_quantize_weights_f6(W, block, perm=None, clip_ratio=1.0, stream=None):
+    """clq_quantize_weights with the codes stored as fp6 (QWeight.bits == 6):
+    the same codes and scales."""
+    _dev(W, "W", torch.float16)
+    if W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be a contiguous 2-D [N, K] tensor")
+    N, K = W.shape
+    perm = _perm(perm, K)
+    nbytes = clq_weight_bytes_f6(N, K)
+    if nbytes == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_quantize_weights_f6")
+    wq = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
+    ws = torch.empty(N, dtype=torch.float32, device=W.device)
+    _check(_lib.clq_quantize_weights_f6(_ptr(W), _ptr(perm), N, K, block, clip_ratio,
+                                        _ptr(wq), _ptr(ws), _stream(stream)), "clq_quantize_weights_f6")
+    return QWeight(wq, ws, N, K, block, perm, clip_ratio, bits=6)
+
+
+def clq_rotate_quant_act_f6(X, block, perm=None, out=None, scale_out=None, stream=None):
+    """clq_rotate_quant_act with the codes stored as fp6: (Xq, x_scale), Xq
+    uint8 [clq_act_bytes_f6(M, K)]."""
+    _dev(X, "X", torch.float16)
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D [M, K] with unit column stride")
+    M, K = X.shape
+    perm = _perm(perm, K)
+    nbytes = clq_act_bytes_f6(M, K)
+    if nbytes == 0:
+        raise ClqError(CLQ_ERR_SHAPE, "clq_rotate_quant_act_f6")
+    Xq = out if out is not None else torch.empty(nbytes, dtype=torch.uint8, device=X.device)
+    xs = scale_out if scale_out is not None else torch.empty(M, dtype=torch.float32, device=X.device)
+    _dev(Xq, "Xq", torch.uint8)
+    _dev(xs, "x_scale", torch.float32)
+    if Xq.numel() < nbytes or not Xq.is_contiguous() or xs.numel() < M:
+        raise ValueError("Xq / x_scale buffers are too small")
+    _check(_lib.clq_rotate_quant_act_f6(_ptr(X), X.stride(0), _ptr(perm), M, K, block, _ptr(Xq),
+                                        _ptr(xs), _stream(stream)), "clq_rotate_quant_act_f6")
+    return Xq, xs
+
+
+def _check_f6(Xq, x_scale, qw):
+    _dev(Xq, "Xq", torch.uint8)
+    _dev(x_scale, "x_scale", torch.float32)
+    if qw.bits != 6:
+        raise ValueError("qw must come from clq_quantize_weights_f6 or clq_qweight_f6")
+    M = x_scale.shape[0]
+    if not Xq.is_contiguous() or Xq.numel() < clq_act_bytes_f6(M, qw.K):
+        raise ValueError("Xq must be the contiguous buffer clq_rotate_quant_act_f6 produced for "
+                         "these M and K")
+    return M
+
+
+def clq_w4a4_linear_f6(Xq, x_scale, qw, bias=None, out=None, stream=None):
+    """clq_w4a4_linear on the fp6 layouts (no workspace): fp16 [M, N]."""
+    M = _check_f6(Xq, x_scale, qw)
+    if bias is not None:
+        _dev(bias, "bias", torch.float16)
+        if bias.shape != (qw.N,) or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous fp16 [N] tensor")
+    if out is None:
+        out = torch.empty((M, (qw.N + 7) // 8 * 8), dtype=torch.float16, device=Xq.device)[:, :qw.N]
+    Y = out
+    _dev(Y, "Y", torch.float16)
+    if Y.dim() != 2 or Y.stride(1) != 1 or Y.shape != (M, qw.N):
+        raise ValueError("Y must be 2-D [M, N] with unit column stride")
+    _check(_lib.clq_w4a4_linear_f6(_ptr(Xq), _ptr(x_scale), _ptr(qw.wq), _ptr(qw.w_scale), _ptr(bias),
+                                   M, qw.N, qw.K, _ptr(Y), Y.stride(0), _stream(stream)), "clq_w4a4_linear_f6")
+    return Y
+
+
+def clq_w4a4_accum_f6(Xq, x_scale, qw, out=None, stream=None):
+    """The exact integer sums of the fp6 operands, int32 [M, N] (diagnostic)."""
+    M = _check_f6(Xq, x_scale, qw)
+    if out is None:
+        out = torch.empty((M, (qw.N + 3) // 4 * 4), dtype=torch.int32, device=Xq.device)[:, :qw.N]
+    _dev(out, "acc", torch.int32)
+    _check(_lib.clq_w4a4_accum_f6(_ptr(Xq), _ptr(qw.wq), M, qw.N, qw.K, _ptr(out), out.stride(0),
+                                  _stream(stream)), "clq_w4a4_accum_f6")
+    return out
+
+
+def clq_unswizzle_f6(q6, rows, K, weights, stream=None):
+    """Canonical packed codes uint8 [rows, K/2] of an fp6 buffer (diagnostic)."""
+    out = torch.empty((rows, K // 2), dtype=torch.uint8, device=q6.device)
+    _check(_lib.clq_unswizzle_f6(_ptr(q6), rows, K, 1 if weights else 0, _ptr(out), _stream(stream)),
+           "clq_unswizzle_f6")
+    return out
+
+
+def clq_f6_from_int4(q4, rows, K, weights, stream=None):
+    """The fp6 layout of a packed int4 buffer (weights: clq_quantize_weights,
+    else clq_rotate_quant_act)."""
+    nbytes = clq_weight_bytes_f6(rows, K) if weights else clq_act_bytes_f6(rows, K)
+    q6 = torch.empty(nbytes, dtype=torch.uint8, device=q4.device)
+    _check(_lib.clq_f6_from_int4(_ptr(q4), rows, K, 1 if weights else 0, _ptr(q6), _stream(stream)),
+           "clq_f6_from_int4")
+    return q6
+
+
+def clq_qweight_f6(qw, stream=None):
+    """An int4 QWeight (clq_quantize_weights) converted to the fp6 layout."""
+    if qw.bits != 4:
+        raise ValueError("qw must come from clq_quantize_weights")
+    return QWeight(clq_f6_from_int4(qw.wq, qw.N, qw.K, True, stream), qw.w_scale, qw.N, qw.K, qw.block,
+                   qw.perm, qw.clip_ratio, bits=6)
 
 
 def _check_xq8(Xq8, x_scale, K):

@@ -10,10 +10,11 @@
 
 #include "../../include/clq.h"
 #include "clq_internal.h"
+#include "f6_codes.h"
 
 namespace {
 
-constexpr int kVersion = 7;
+constexpr int kVersion = 8;
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxRows = 2147483647;
 
@@ -289,6 +290,91 @@ clq_status clq_unswizzle_weights(const void *Wq, int64_t N, int64_t K, void *Wq_
     if (!aligned(Wq, 16) || !aligned(Wq_canonical, 8)) return CLQ_ERR_ALIGN;
     return done(stream, clq::launch_unswizzle(static_cast<const uint8_t *>(Wq), N, (int)K,
                                           static_cast<uint8_t *>(Wq_canonical), stream));
+}
+
+size_t clq_weight_bytes_f6(int64_t N, int64_t K) {
+    if (check_rows(N) != CLQ_OK || check_k(K) != CLQ_OK) return 0;
+    return (size_t)clq::f6_operand_bytes(clq::padded_rows(N), K);
+}
+
+size_t clq_act_bytes_f6(int64_t M, int64_t K) {
+    if (check_rows(M) != CLQ_OK || check_k(K) != CLQ_OK) return 0;
+    return (size_t)clq::f6_operand_bytes(clq::padded_act_rows(M), K);
+}
+
+clq_status clq_quantize_weights_f6(const void *W, const int32_t *perm, int64_t N, int64_t K,
+                                   int32_t block, float clip_ratio, void *Wq, float *w_scale,
+                                   hipStream_t stream) {
+    if (!W || !Wq || !w_scale) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (!(clip_ratio >= 0x1p-24f && clip_ratio <= 1.0f)) return CLQ_ERR_ARG;
+    if (!aligned(W, 16) || !aligned(Wq, 16) || !aligned(w_scale, 4) || (perm && !aligned(perm, 4)))
+        return CLQ_ERR_ALIGN;
+    return done(stream, clq::launch_rotate_quant(
+        static_cast<const uint16_t *>(W), K, perm, N, clq::padded_rows(N), (int)K, block,
+        clip_ratio, true, 1.0f / (float)block, static_cast<uint8_t *>(Wq), w_scale, stream, 6));
+}
+
+clq_status clq_rotate_quant_act_f6(const void *X, int64_t ldx, const int32_t *perm, int64_t M,
+                                   int64_t K, int32_t block, void *Xq, float *x_scale,
+                                   hipStream_t stream) {
+    if (!X || !Xq || !x_scale) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if ((s = check_block(K, block)) != CLQ_OK) return s;
+    if (ldx < K || ldx % 8 != 0) return CLQ_ERR_SHAPE;
+    if (!aligned(X, 16) || !aligned(Xq, 16) || !aligned(x_scale, 4) || (perm && !aligned(perm, 4)))
+        return CLQ_ERR_ALIGN;
+    return done(stream, clq::launch_rotate_quant(static_cast<const uint16_t *>(X), ldx, perm, M,
+                                             clq::padded_act_rows(M), (int)K, block, 1.0f, false,
+                                             1.0f, static_cast<uint8_t *>(Xq), x_scale, stream, 6));
+}
+
+clq_status clq_w4a4_linear_f6(const void *Xq, const float *x_scale, const void *Wq, const float *w_scale,
+                              const void *bias, int64_t M, int64_t N, int64_t K, void *Y, int64_t ldy,
+                              hipStream_t stream) {
+    if (!x_scale || !w_scale) return CLQ_ERR_NULL;
+    clq_status s = check_gemm(Xq, Wq, M, N, K, Y, ldy, 8);
+    if (s != CLQ_OK) return s;
+    if (K < 128) return CLQ_ERR_SHAPE;
+    if (!aligned(x_scale, 4) || !aligned(w_scale, 4) || (bias && !aligned(bias, 2))) return CLQ_ERR_ALIGN;
+    return done(stream, clq::launch_gemm_f6(static_cast<const uint8_t *>(Xq), x_scale, static_cast<const uint8_t *>(Wq),
+                                            w_scale, static_cast<const uint16_t *>(bias), M, N, (int)K, Y, ldy, false,
+                                            stream));
+}
+
+clq_status clq_w4a4_accum_f6(const void *Xq, const void *Wq, int64_t M, int64_t N, int64_t K, int32_t *acc,
+                             int64_t ldacc, hipStream_t stream) {
+    clq_status s = check_gemm(Xq, Wq, M, N, K, acc, ldacc, 4);
+    if (s != CLQ_OK) return s;
+    if (K < 128) return CLQ_ERR_SHAPE;
+    return done(stream, clq::launch_gemm_f6(static_cast<const uint8_t *>(Xq), nullptr, static_cast<const uint8_t *>(Wq),
+                                            nullptr, nullptr, M, N, (int)K, acc, ldacc, true, stream));
+}
+
+clq_status clq_unswizzle_f6(const void *q6, int64_t rows, int64_t K, int32_t weights, void *canonical,
+                            hipStream_t stream) {
+    if (!q6 || !canonical) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(rows)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (weights != 0 && weights != 1) return CLQ_ERR_ARG;
+    if (!aligned(q6, 16) || !aligned(canonical, 16)) return CLQ_ERR_ALIGN;
+    return done(stream, clq::launch_unswizzle_f6(static_cast<const uint8_t *>(q6), rows, (int)K, weights != 0,
+                                                 static_cast<uint8_t *>(canonical), stream));
+}
+
+clq_status clq_f6_from_int4(const void *q4, int64_t rows, int64_t K, int32_t weights, void *q6,
+                            hipStream_t stream) {
+    if (!q4 || !q6) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(rows)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (weights != 0 && weights != 1) return CLQ_ERR_ARG;
+    if (!aligned(q4, 16) || !aligned(q6, 16)) return CLQ_ERR_ALIGN;
+    const int64_t prows = weights ? clq::padded_rows(rows) : clq::padded_act_rows(rows);
+    return done(stream, clq::launch_repack_f6(static_cast<const uint8_t *>(q4), prows / 32 * (K / 64),
+                                              static_cast<uint8_t *>(q6), stream));
 }
 
 clq_status clq_unswizzle_act(const void *Xq, int64_t M, int64_t K, void *Xq_canonical,

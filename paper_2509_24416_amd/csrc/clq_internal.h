@@ -71,7 +71,8 @@ __host__ __device__ inline int64_t q8_piece_offset(int64_t u, int rho, int64_t c
     return ((u * (K >> 6) + (c >> 1)) * 2 + q) * 1024 + (32 * (c & 1) + rho) * 16;
 }
 
-// bits: 4 (packed int4 layouts above) or 8 (int8 layout).  alpha_dev, when
+// bits: 4 (packed int4 layouts above), 6 (the 4-bit grid in the fp6 layout
+// of f6_codes.h) or 8 (int8 layout).  alpha_dev, when
 // given, holds the weights' clip ratio in device memory (alpha is then unused).
 // batch > 1 (weights with alpha_dev only): batch quantizations of the same
 // rows, quantization y with clip ratio alpha_dev[y] into out + y * out_stride
@@ -185,6 +186,17 @@ int64_t gemm_err_partials(int64_t M, int64_t N);
 hipError_t launch_gemm_err(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
                            int64_t M, int64_t N, int K, const float *Y0, int64_t ldy0, double *partials,
                            hipStream_t stream);
+
+// fp6 (e2m3) code layouts: packed int4 units (1 KB) of weights or
+// activations converted unit for unit into fp6 units (1536 bytes, same lane
+// map), and the W4A4 GEMM on them (whole tiles, K >= 128).
+hipError_t launch_repack_f6(const uint8_t *in, int64_t units, uint8_t *out, hipStream_t stream);
+// canonical packed int4 codes [rows][K/2] of an fp6 operand
+hipError_t launch_unswizzle_f6(const uint8_t *q6, int64_t rows, int K, bool weights, uint8_t *out,
+                               hipStream_t stream);
+hipError_t launch_gemm_f6(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                          const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy, bool i32out,
+                          hipStream_t stream);
 
 // OBS calibration (batch mean, channel outlier scores, column swap).
 // metric: 0 abs-max, 1 range, 2 peak-to-average ratio, 3 top-k mean,

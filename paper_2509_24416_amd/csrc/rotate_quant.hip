@@ -32,6 +32,7 @@
 
 #include "clq_internal.h"
 #include "rq_device.h"
+#include "f6_codes.h"
 
 namespace clq {
 namespace {
@@ -200,6 +201,24 @@ rotate_quant_kernel(const uint16_t *__restrict__ X, int64_t ldx,
         return;
     }
 
+    if constexpr (QB == 6) {
+        // fp6 layout: the codes as exact floats, six dwords per 32 codes
+        const int rho = WEIGHT ? wq_rho((int)(grow & 31)) : (int)(grow & 31);
+#pragma unroll
+        for (int i = 0; i < B; ++i) {
+            float v = __builtin_fmaf(x[i], rc, kMagic);
+            if constexpr (WEIGHT) v = __builtin_amdgcn_fmed3f(v, kMagic - 7.0f, kMagic + 7.0f);
+            x[i] = v - kMagic;
+        }
+#pragma unroll
+        for (int c = 0; c < B / 32; ++c) {
+            const int64_t c32 = (int64_t)j * (B / 32) + c;
+            uint32_t w6[6];
+            f6_from_codes(&x[32 * c], w6);
+            f6_store(out + f6_unit_offset(grow >> 5, c32, K), f6_lane(c32, rho), w6);
+        }
+        return;
+    }
     uint32_t words[B / 8];
 #pragma unroll
     for (int g = 0; g < B / 8; ++g) {
@@ -368,6 +387,19 @@ rq_act_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__rest
             store_q8<B, false>(x, rc, grow, j, K, out);
             continue;
         }
+        if constexpr (QB == 6) {
+            // the codes as exact floats, in place (x is dead after this)
+#pragma unroll
+            for (int e = 0; e < B; ++e) x[e] = __builtin_fmaf(x[e], rc, kMagic) - kMagic;
+#pragma unroll
+            for (int c = 0; c < B / 32; ++c) {
+                const int64_t c32 = (int64_t)j * (B / 32) + c;
+                uint32_t w6[6];
+                f6_from_codes(&x[32 * c], w6);
+                f6_store(out + f6_unit_offset(grow >> 5, c32, K), f6_lane(c32, (int)(grow & 31)), w6);
+            }
+            continue;
+        }
         uint32_t words[B / 8];
 #pragma unroll
         for (int g = 0; g < B / 8; ++g) {
@@ -474,6 +506,19 @@ rq_rows8_kernel(const uint16_t *__restrict__ X, int64_t ldx, const int32_t *__re
         if constexpr (QB == 8) {
             store_q8<B, false>(x, rc, grow, j, K, out);
         } else {
+            if constexpr (QB == 6) {
+                // the codes as exact floats, in place (x is reloaded after this)
+#pragma unroll
+                for (int e = 0; e < B; ++e) x[e] = __builtin_fmaf(x[e], rc, kMagic) - kMagic;
+#pragma unroll
+                for (int c = 0; c < B / 32; ++c) {
+                    const int64_t c32 = (int64_t)j * (B / 32) + c;
+                    uint32_t w6[6];
+                    f6_from_codes(&x[32 * c], w6);
+                    f6_store(out + f6_unit_offset(grow >> 5, c32, K), f6_lane(c32, (int)(grow & 31)), w6);
+                }
+                return;
+            }
             uint32_t words[B / 8];
 #pragma unroll
             for (int g = 0; g < B / 8; ++g) {
@@ -748,7 +793,42 @@ hipError_t launch_rotate_quant(const uint16_t *X, int64_t ldx, const int32_t *pe
     if (bits == 4)
         return launch_rq_bits<4>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
                                  out, scale, stream, alpha_dev, batch, out_stride, scale_stride);
+    if (bits == 6)
+        return launch_rq_bits<6>(X, ldx, perm, rows, rows_alloc, K, block, alpha, weight_mode, post_scale,
+                                 out, scale, stream, alpha_dev, batch, out_stride, scale_stride);
     return hipErrorInvalidValue;
+}
+
+namespace {
+
+// canonical packed int4 codes [rows][K/2] of an fp6 operand (weights: the
+// fragment-row order undone): one thread per 32-code chunk
+__global__ void unswizzle_f6_kernel(const uint8_t *__restrict__ q6, int64_t rows, int K, bool weights,
+                                    uint8_t *__restrict__ out) {
+    const int64_t cpr = K / 32;
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= rows * cpr) return;
+    const int64_t r = idx / cpr, c32 = idx - r * cpr;
+    const int rho = weights ? wq_rho((int)(r & 31)) : (int)(r & 31);
+    const uint8_t *unit = q6 + f6_unit_offset(r >> 5, c32, K);
+    const int l = f6_lane(c32, rho);
+    const uint4 a = *reinterpret_cast<const uint4 *>(unit + l * 16);
+    const uint2 b = *reinterpret_cast<const uint2 *>(unit + f6_tail_offset(l));
+    const uint32_t w[6] = {a.x, a.y, a.z, a.w, b.x, b.y};
+    uint32_t d[4];
+    nibbles_from_f6(w, d);
+    *reinterpret_cast<uint4 *>(out + r * (K / 2) + c32 * 16) = make_uint4(d[0], d[1], d[2], d[3]);
+}
+
+}  // namespace
+
+hipError_t launch_unswizzle_f6(const uint8_t *q6, int64_t rows, int K, bool weights, uint8_t *out,
+                               hipStream_t stream) {
+    const int64_t total = rows * (K / 32);
+    if (total == 0) return hipSuccess;
+    hipLaunchKernelGGL(unswizzle_f6_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, q6, rows, K,
+                       weights, out);
+    return hipGetLastError();
 }
 
 hipError_t launch_unswizzle(const uint8_t *Wq, int64_t N, int K, uint8_t *out,

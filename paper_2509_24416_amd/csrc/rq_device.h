@@ -17,12 +17,13 @@ constexpr float kMagic = 12582920.0f;  // 1.5 * 2^23 + 8
 
 // n-bit grid of Eq. (1): codes in [-qmax, qmax], qmax = 2^(n-1) - 1; the
 // magic constant 1.5 * 2^23 + 2^(n-1) leaves code + 2^(n-1) in the low n
-// bits of the fma result (bits n..21 clear).
+// bits of the fma result (bits n..21 clear).  QB = 6 is the 4-bit grid with
+// its codes stored as fp6 (e2m3) instead of nibbles.
 template <int QB>
 struct Grid {
-    static_assert(QB == 4 || QB == 8, "4- or 8-bit codes");
-    static constexpr float qmax = QB == 4 ? 7.0f : 127.0f;
-    static constexpr float magic = QB == 4 ? 12582920.0f : 12583040.0f;
+    static_assert(QB == 4 || QB == 6 || QB == 8, "4-bit codes (as nibbles or fp6) or 8-bit codes");
+    static constexpr float qmax = QB == 8 ? 127.0f : 7.0f;
+    static constexpr float magic = QB == 8 ? 12583040.0f : 12582920.0f;
 };
 
 // Slot of 16-byte chunk i of Hadamard block j inside its block's span in

@@ -1,0 +1,534 @@
+// W4A4 GEMM on the fp6 matrix cores of gfx950, with the dequantising
+// epilogue fused (CLQ, arXiv 2509.24416: the integer product of the W4A4
+// codes, rescaled by the per-token activation scale and the per-channel
+// weight scale of Eq. (1), plus bias).
+//
+// Codes carried as fp6.  gfx950 has no 4-bit integer matrix instruction.  Its
+// fp6 format e2m3 (1 sign, 2 exponent, 3 mantissa bits, bias 1) holds every
+// code of the 4-bit grid, -7..7, exactly, and v_mfma_f32_32x32x64_f8f6f4 on
+// two fp6 operands multiplies them at twice the int8 instruction's rate.
+// Each product of two codes is an integer of magnitude at most 49, and every
+// partial sum of a k loop shorter than 2^24 / 49 codes is an integer below
+// 2^24, which fp32 holds exactly: the accumulators are the exact integers
+// sum_k qa * qw, whatever the order of the additions.
+//
+// fp6 code layout (weights and activations): the unit and lane map of the
+// packed int4 layouts (32 rows x 64 codes per unit, lane l = 32h + rho
+// holding codes 32h .. 32h+31 of fragment row rho; weights with their
+// fragment-row order, so that accumulator element v of lane l is channel
+// 16 (l / 32) + v of the fragment), 24 bytes per lane: code i of the lane's
+// 32 at bits 6i .. 6i+5 of its 192 bits (f6_codes.h).  A unit is 1536
+// bytes: lane l's first 16 bytes at 16 l, its last 8 after the first 1 KB
+// (aligned LDS reads of 16 and 8 bytes; the transfer into LDS is one 16-byte
+// load per lane for the first 1 KB and one 16-byte load on 32 lanes for the
+// rest).  Units are stored [row unit][k unit].
+//
+// The kernel is the persistent W4A4 kernel's pipeline (see w4a4_gemm.hip)
+// with 1536-byte units, one matrix instruction per fragment and k-stage of
+// 64 codes, no operand widening, and a 4-slot ring: the slot of stage s is
+// refilled with stage s + 4 in iteration s, its contents having been read
+// into registers in iteration s - 1 (the workgroup barrier of iteration s
+// orders those reads before the transfer).  Whole tiles only.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <type_traits>
+
+#include "clq_internal.h"
+#include "f6_codes.h"
+
+#define CLQ_LDS __attribute__((address_space(3)))
+
+namespace clq {
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+template <int Q> using IC = std::integral_constant<int, Q>;
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)reinterpret_cast<size_t>((CLQ_LDS const void *)p);
+}
+template <int OFF>
+__device__ __forceinline__ v4u lds_read16(uint32_t addr) {
+    v4u v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+    return v;
+}
+template <int OFF>
+__device__ __forceinline__ v2u lds_read8(uint32_t addr) {
+    v2u v;
+    asm volatile("ds_read_b64 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "n"(OFF));
+    return v;
+}
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<I + 1, N>(f);
+    }
+}
+
+// two fp16 outputs fma(p, w, bias) rounded once from fp32 operands and a
+// packed fp16 bias pair (low half: first output)
+__device__ __forceinline__ uint32_t fma_mix2(float p0, float w0, float p1, float w1, uint32_t b) {
+    uint32_t r;
+    asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel_hi:[0,0,1]\n\t"
+        "v_fma_mixhi_f16 %0, %4, %5, %3 op_sel:[0,0,1] op_sel_hi:[0,0,1]"
+        : "=&v"(r)
+        : "v"(p0), "v"(w0), "v"(b), "v"(p1), "v"(w1));
+    return r;
+}
+
+constexpr int kUnit = kF6Unit;  // bytes of a 32 x 64 fp6 unit
+constexpr int kNS = 4;          // ring slots
+constexpr int kGroupM = 8;      // token panels per tile group (L2 reuse of channel panels)
+constexpr int kWN = 1, kWM = 4, kFN = 4, kFM = 2;
+constexpr int kNW = kWN * kWM, kNT = kNW * 64;
+constexpr int kBN = kWN * kFN * 32, kBM = kWM * kFM * 32;
+constexpr int kWUnits = kBN / 32, kXUnits = kBM / 32, kUnits = kWUnits + kXUnits;
+constexpr int kUPW = kUnits / kNW;          // units per wave and stage
+constexpr int kVPW = 2 * kUPW;              // transfers per wave and stage
+constexpr int kSlot = kUnits * kUnit;
+static_assert(kUnits % kNW == 0, "units split evenly over waves");
+
+struct F6Args {
+    const uint8_t *Xq;
+    const float *xs;
+    const uint8_t *Wq;
+    const float *ws;
+    const uint16_t *bias;
+    void *Y;
+    int64_t ldy;
+    int M, N, K, tiles_m, tiles_n;
+};
+
+struct Seg {
+    int j, L, k;
+};
+
+template <bool I32OUT, bool RAGGED, bool BIAS>
+__global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
+{
+    constexpr int NS = kNS;
+    constexpr bool BIAS_CH = BIAS && !RAGGED && !I32OUT;
+    constexpr int XS_CH = kBM / 64, WS_CH = kBN / 64, B_CH = kBN / 128;
+    constexpr int E_CH = I32OUT ? 0 : XS_CH + WS_CH + (BIAS_CH ? B_CH : 0);
+    constexpr int EPW = (E_CH + kNW - 1) / kNW;
+    constexpr int E_XS = 0, E_WS = E_XS + kBM * 4, E_B = E_WS + kBN * 4;
+    constexpr int E_BYTES = I32OUT ? 16 : E_B + (BIAS_CH ? kBN * 2 : 0);
+    __shared__ __align__(16) uint8_t ring0[kSlot], ring1[kSlot], ring2[kSlot], ring3[kSlot];
+    __shared__ __align__(16) uint8_t ebuf[NS][E_BYTES];
+    auto slot = [&](auto qc) -> uint8_t * {
+        constexpr int q = decltype(qc)::value;
+        if constexpr (q == 0) return ring0;
+        else if constexpr (q == 1) return ring1;
+        else if constexpr (q == 2) return ring2;
+        else return ring3;
+    };
+
+    const int M = a.M, N = a.N, nks = a.K >> 6;
+    const int G = gridDim.x, gx = G >> 3, xcd = blockIdx.x & 7, jw = blockIdx.x >> 3;
+    const int ntiles = a.tiles_m * a.tiles_n;
+    const int per = ntiles >> 3, rem = ntiles & 7;
+    const int cnt = per + (xcd < rem ? 1 : 0);
+    const int dstart = xcd * per + min(xcd, rem);
+    const int my_tiles = jw < cnt ? (cnt - jw + gx - 1) / gx : 0;
+    const int total = my_tiles * nks;
+    if (total == 0) return;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave;   // one channel panel per tile
+    const int wunits_total = (int)(padded_rows(N) >> 5);
+    const int xunits_total = (int)(padded_act_rows(M) >> 5);
+
+    auto coords = [&](int L, int &tm, int &tn) {
+        const int gsz = kGroupM * a.tiles_n;
+        const int g = L / gsz, r = L - g * gsz;
+        const int m0 = g * kGroupM;
+        const int gm = min(a.tiles_m - m0, kGroupM);
+        tn = r / gm;
+        tm = m0 + (r - tn * gm);
+    };
+    auto next_seg = [&](Seg &c) {
+        ++c.j;
+        c.L = dstart + jw + c.j * gx;
+        c.k = 0;
+    };
+
+    // ---- producer -------------------------------------------------------------
+    Seg pc{-1, 0, 0};
+    next_seg(pc);
+    int p_s = 0;
+    const uint8_t *usrc[kUPW];
+    const uint8_t *esrc[EPW > 0 ? EPW : 1];
+    int edst[EPW > 0 ? EPW : 1];
+    auto p_setup = [&]() {
+        int tm, tn;
+        coords(pc.L, tm, tn);
+#pragma unroll
+        for (int j = 0; j < kUPW; ++j) {
+            const int u = wave * kUPW + j;
+            if (u < kWUnits) {
+                const int ug = min(tn * kWUnits + u, wunits_total - 1);
+                usrc[j] = a.Wq + (int64_t)ug * nks * kUnit;
+            } else {
+                const int ux = min(tm * kXUnits + (u - kWUnits), xunits_total - 1);
+                usrc[j] = a.Xq + (int64_t)ux * nks * kUnit;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < EPW; ++j) {
+            const int c = wave * EPW + j;
+            if (c < XS_CH) {
+                esrc[j] = reinterpret_cast<const uint8_t *>(a.xs + min(tm * kBM + c * 64 + lane, M - 1));
+                edst[j] = E_XS + c * 256;
+            } else if (c < XS_CH + WS_CH || c >= E_CH) {
+                const int w = (c - XS_CH) % WS_CH;
+                esrc[j] = reinterpret_cast<const uint8_t *>(a.ws + min(tn * kBN + w * 64 + lane, N - 1));
+                edst[j] = E_WS + w * 256;
+            } else {
+                const int b = c - XS_CH - WS_CH;
+                esrc[j] = reinterpret_cast<const uint8_t *>(reinterpret_cast<const uint32_t *>(a.bias) +
+                                                            min(tn * (kBN / 2) + b * 64 + lane, N / 2 - 1));
+                edst[j] = E_B + b * 256;
+            }
+        }
+    };
+    p_setup();
+    int e_next = 0;        // stage whose production carries the next tile's epilogue operands
+    unsigned phist = 0;    // 1 bit per production call: epilogue operands issued
+    auto produce = [&](auto qc) {
+        // the tile's epilogue operands go out with its first stage, ahead of
+        // the units (the wait counts below rely on that order)
+        int e_now = 0;
+        if (EPW > 0 && pc.k == 0 && p_s == e_next) {
+            uint8_t *ed = &ebuf[pc.j % NS][0];
+#pragma unroll
+            for (int j = 0; j < EPW; ++j)
+                __builtin_amdgcn_global_load_lds(esrc[j], (CLQ_LDS void *)(ed + edst[j]), 4, 0, 0);
+            e_now = 1;
+            e_next = -1;
+        }
+        phist = (phist << 1) | e_now;
+        uint8_t *dst = slot(qc);
+        const uint32_t voff = (uint32_t)(pc.k * kUnit + lane * 16);
+#pragma unroll
+        for (int j = 0; j < kUPW; ++j)
+            __builtin_amdgcn_global_load_lds(usrc[j] + voff, (CLQ_LDS void *)(dst + (wave * kUPW + j) * kUnit), 16, 0, 0);
+        // the units' last 512 bytes: 16 bytes on each of lanes 0..31
+        if (lane < 32) {
+#pragma unroll
+            for (int j = 0; j < kUPW; ++j)
+                __builtin_amdgcn_global_load_lds(usrc[j] + voff + 1024,
+                                                 (CLQ_LDS void *)(dst + (wave * kUPW + j) * kUnit + 1024), 16, 0, 0);
+        }
+        if (p_s < total - 1) {
+            ++p_s;
+            if (++pc.k == nks) {
+                next_seg(pc);
+                p_setup();
+                e_next = p_s;
+            }
+        }
+    };
+
+    // ---- consumer -------------------------------------------------------------
+    // operands of one stage: 16 + 8 bytes of each of the wave's 4 channel and
+    // 2 token units
+    v4u ra[kFN], rb[kFM];
+    v2u sa[kFN], sb[kFM];
+    v8i opa[kFN], opb[kFM];
+    const uint32_t wl0 = (uint32_t)(lane * 16), wl1 = (uint32_t)f6_tail_offset(lane);
+    auto read_stage = [&](auto qc) {
+        uint32_t b16 = wl0, b8 = wl1;
+        asm volatile("" : "+v"(b16), "+v"(b8));
+        b16 += lds_addr(slot(qc));
+        b8 += lds_addr(slot(qc));
+        // this wave's token units: the offset exceeds the 16-bit immediate
+        // range for the later waves, so it goes into the address
+        const uint32_t xo = (uint32_t)((kWUnits + wm * kFM) * kUnit);
+        const uint32_t bx16 = b16 + xo, bx8 = b8 + xo;
+        static_for<0, kFN>([&](auto f) {
+            constexpr int o = decltype(f)::value * kUnit;
+            ra[f] = lds_read16<o>(b16);
+            sa[f] = lds_read8<o>(b8);
+        });
+        static_for<0, kFM>([&](auto f) {
+            constexpr int o = decltype(f)::value * kUnit;
+            rb[f] = lds_read16<o>(bx16);
+            sb[f] = lds_read8<o>(bx8);
+        });
+    };
+    auto stage_ready = [&]() {
+        static_assert(kFN == 4 && kFM == 2, "operand list below");
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]), "+v"(rb[1]),
+                       "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]), "+v"(sb[1]));
+    };
+    auto take_operands = [&]() {
+#pragma unroll
+        for (int f = 0; f < kFN; ++f)
+            opa[f] = v8i{(int)ra[f][0], (int)ra[f][1], (int)ra[f][2], (int)ra[f][3], (int)sa[f][0], (int)sa[f][1], 0, 0};
+#pragma unroll
+        for (int f = 0; f < kFM; ++f)
+            opb[f] = v8i{(int)rb[f][0], (int)rb[f][1], (int)rb[f][2], (int)rb[f][3], (int)sb[f][0], (int)sb[f][1], 0, 0};
+    };
+    v16f acc[kFN][kFM];
+    auto zero_acc = [&]() {
+#pragma unroll
+        for (int fn = 0; fn < kFN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < kFM; ++fm) acc[fn][fm] = v16f{};
+    };
+    // format codes 2, 2: both operands fp6 e2m3; no block scales
+    auto mma = [&]() {
+#pragma unroll
+        for (int fn = 0; fn < kFN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < kFM; ++fm)
+                acc[fn][fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opa[fn], opb[fm], acc[fn][fm], 2, 2, 0, 0, 0, 0);
+    };
+
+    // ---- epilogue: lane owns token m and 16 consecutive channels ----------------
+    const int h16 = (lane >> 5) * 16;
+    auto epilogue = [&](int L, int sj) {
+        int tm, tn;
+        coords(L, tm, tn);
+        uint32_t lx = (uint32_t)((wm * kFM * 32 + (lane & 31)) * 4);
+        uint32_t lw = (uint32_t)(h16 * 4);
+        asm volatile("" : "+v"(lx), "+v"(lw));
+        const uint32_t sbase = lds_addr(&ebuf[0][0]) + (uint32_t)((sj % NS) * E_BYTES);
+        const uint32_t axs = sbase + E_XS + lx, aws = sbase + E_WS + lw, ab = sbase + E_B + lw / 2;
+        float xsm[kFM];
+        int mrow[kFM];
+        if constexpr (!I32OUT) {
+            static_assert(kFM == 2, "two token scales per lane");
+            asm volatile("ds_read_b32 %0, %2\n\tds_read_b32 %1, %2 offset:128\n\ts_waitcnt lgkmcnt(0)"
+                         : "=&v"(xsm[0]), "=&v"(xsm[1]) : "v"(axs));
+        }
+#pragma unroll
+        for (int fm = 0; fm < kFM; ++fm) mrow[fm] = tm * kBM + (wm * kFM + fm) * 32 + (lane & 31);
+        const int nl = tn * kBN + h16;
+        uint16_t *rowp[kFM];
+#pragma unroll
+        for (int fm = 0; fm < kFM; ++fm) rowp[fm] = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)mrow[fm] * a.ldy + nl;
+        static_for<0, kFN>([&](auto fc) {
+            constexpr int fn = decltype(fc)::value;
+            const int n0 = nl + fn * 32;
+            v4f w4[4];
+            v4u b8[2];
+            if constexpr (!I32OUT) {
+                asm volatile(
+                    "ds_read_b128 %0, %4 offset:%6\n\t"
+                    "ds_read_b128 %1, %4 offset:%7\n\t"
+                    "ds_read_b128 %2, %4 offset:%8\n\t"
+                    "ds_read_b128 %3, %4 offset:%9\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=&v"(w4[0]), "=&v"(w4[1]), "=&v"(w4[2]), "=&v"(w4[3])
+                    : "v"(aws), "v"(ab), "n"(fn * 128), "n"(fn * 128 + 16), "n"(fn * 128 + 32), "n"(fn * 128 + 48));
+                if constexpr (BIAS_CH)
+                    asm volatile(
+                        "ds_read_b128 %0, %2 offset:%3\n\t"
+                        "ds_read_b128 %1, %2 offset:%4\n\t"
+                        "s_waitcnt lgkmcnt(0)"
+                        : "=&v"(b8[0]), "=&v"(b8[1])
+                        : "v"(ab), "n"(fn * 64), "n"(fn * 64 + 16));
+            }
+            float wsv[16];
+            uint32_t bw[8];
+            if constexpr (!I32OUT) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) wsv[v] = w4[v / 4][v % 4];
+            }
+            if constexpr (!BIAS || I32OUT) {
+#pragma unroll
+                for (int v = 0; v < 8; ++v) bw[v] = 0u;
+            } else if constexpr (RAGGED) {
+#pragma unroll
+                for (int v = 0; v < 16; v += 2) {
+                    const int na = min(n0 + v, N - 1), nb = min(n0 + v + 1, N - 1);
+                    bw[v / 2] = (uint32_t)a.bias[na] | ((uint32_t)a.bias[nb] << 16);
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < 8; ++v) bw[v] = b8[v / 4][v % 4];
+            }
+#pragma unroll
+            for (int fm = 0; fm < kFM; ++fm) {
+                const int m = mrow[fm];
+                const v16f &x = acc[fn][fm];
+                if constexpr (I32OUT) {
+                    int32_t *dst = reinterpret_cast<int32_t *>(a.Y) + (int64_t)m * a.ldy + n0;
+                    if (m < M && n0 < N) {
+                        if (!RAGGED || n0 + 16 <= N) {
+#pragma unroll
+                            for (int q4 = 0; q4 < 4; ++q4)
+                                reinterpret_cast<v4i *>(dst)[q4] =
+                                    v4i{(int)x[4 * q4], (int)x[4 * q4 + 1], (int)x[4 * q4 + 2], (int)x[4 * q4 + 3]};
+                        } else {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v)
+                                if (n0 + v < N) dst[v] = (int)x[v];
+                        }
+                    }
+                } else {
+                    uint32_t hv[8];
+#pragma unroll
+                    for (int v = 0; v < 16; v += 2)
+                        hv[v / 2] = fma_mix2(x[v] * xsm[fm], wsv[v], x[v + 1] * xsm[fm], wsv[v + 1], bw[v / 2]);
+                    uint16_t *dst = rowp[fm] + fn * 32;
+                    if (m < M && n0 < N) {
+                        if (!RAGGED || n0 + 16 <= N) {
+                            reinterpret_cast<v4u *>(dst)[0] = v4u{hv[0], hv[1], hv[2], hv[3]};
+                            reinterpret_cast<v4u *>(dst)[1] = v4u{hv[4], hv[5], hv[6], hv[7]};
+                        } else {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v)
+                                if (n0 + v < N) dst[v] = (uint16_t)(hv[v >> 1] >> (16 * (v & 1)));
+                        }
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+
+    // Stage s+1 has landed once at most the VMEM instructions issued after
+    // its last transfer are outstanding (completion is in issue order): the
+    // two later productions, with their epilogue operand transfers if any.
+    // Epilogue stores are not counted, which only makes the wait stricter.
+    constexpr int W0 = 2 * kVPW;
+    auto landed_wait = [&]() {
+        switch (__builtin_popcount(phist & 3u)) {
+            case 0: asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W0) : "memory"); break;
+            case 1: asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W0 + EPW) : "memory"); break;
+            default: asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(W0 + 2 * EPW) : "memory"); break;
+        }
+    };
+
+    // ---- pipeline ---------------------------------------------------------------
+    // prologue: stages 0..3 in flight, stage 0 read into registers
+    produce(IC<0>{});
+    produce(IC<1>{});
+    produce(IC<2>{});
+    produce(IC<3>{});
+    // stage 0 landed: the three later productions may be outstanding
+    switch (__builtin_popcount(phist & 7u)) {
+        case 0: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(3 * kVPW) : "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(3 * kVPW + EPW) : "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(3 * kVPW + 2 * EPW) : "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(3 * kVPW + 3 * EPW) : "memory"); break;
+    }
+    read_stage(IC<0>{});
+    stage_ready();
+    zero_acc();
+
+    Seg cc{-1, 0, 0};
+    next_seg(cc);
+    int s = 0;
+    auto iter = [&](auto qc) -> bool {
+        constexpr int q = decltype(qc)::value;
+        constexpr IC<(q + 1) % NS> nqc{};
+        take_operands();
+        landed_wait();
+        // slot q held stage s, read into registers last iteration: refill it
+        // with stage s + 4 (the producer's next)
+        if (s + 1 < total) read_stage(nqc);
+        produce(qc);
+        __builtin_amdgcn_sched_barrier(0);
+        mma();
+        __builtin_amdgcn_sched_barrier(0);
+        stage_ready();
+        if (cc.k == nks - 1) {
+            epilogue(cc.L, cc.j);
+            zero_acc();
+            if (s + 1 < total) next_seg(cc);
+        } else {
+            ++cc.k;
+        }
+        ++s;
+        return s < total;
+    };
+    while (iter(IC<0>{}) && iter(IC<1>{}) && iter(IC<2>{}) && iter(IC<3>{})) {
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// ---- format conversion: packed int4 units -> fp6 units ---------------------------
+// One thread per lane slot: its 16 bytes (32 nibbles) become its six fp6
+// dwords (the code order of f6_codes.h).
+__global__ void repack_f6_kernel(const uint8_t *__restrict__ in, uint8_t *__restrict__ out, int64_t slots) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= slots) return;
+    const int64_t unit = t >> 6;
+    const int l = (int)(t & 63);
+    const v4u src = *reinterpret_cast<const v4u *>(in + unit * 1024 + l * 16);
+    const uint32_t d[4] = {src[0], src[1], src[2], src[3]};
+    uint32_t w[6];
+    f6_from_nibbles(d, w);
+    f6_store(out + unit * kF6Unit, l, w);
+}
+
+int f6_device_cus() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+    }
+    return cus;
+}
+
+}  // namespace
+
+hipError_t launch_repack_f6(const uint8_t *in, int64_t units, uint8_t *out, hipStream_t stream) {
+    const int64_t slots = units * 64;
+    if (slots == 0) return hipSuccess;
+    hipLaunchKernelGGL(repack_f6_kernel, dim3((unsigned)((slots + 255) / 256)), dim3(256), 0, stream, in, out, slots);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_f6(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
+                          const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy, bool i32out,
+                          hipStream_t stream) {
+    F6Args g{};
+    g.Xq = Xq;
+    g.xs = xs;
+    g.Wq = Wq;
+    g.ws = ws;
+    g.bias = bias;
+    g.Y = Y;
+    g.ldy = ldy;
+    g.M = (int)M;
+    g.N = (int)N;
+    g.K = K;
+    g.tiles_m = (int)((M + kBM - 1) / kBM);
+    g.tiles_n = (int)((N + kBN - 1) / kBN);
+    const int ntiles = g.tiles_m * g.tiles_n;
+    const int full = (f6_device_cus() * 2 + 7) / 8 * 8;
+    const int grid = std::max(8, (std::min(ntiles, full) + 7) / 8 * 8);
+    const bool ragged = N % 16 != 0 || (bias && reinterpret_cast<uintptr_t>(bias) % 4 != 0);
+    const dim3 gd((unsigned)grid), bd(kNT);
+    if (i32out) {
+        if (ragged) hipLaunchKernelGGL((f6_gemm_kernel<true, true, false>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_kernel<true, false, false>), gd, bd, 0, stream, g);
+    } else if (ragged) {
+        if (bias) hipLaunchKernelGGL((f6_gemm_kernel<false, true, true>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_kernel<false, true, false>), gd, bd, 0, stream, g);
+    } else {
+        if (bias) hipLaunchKernelGGL((f6_gemm_kernel<false, false, true>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_kernel<false, false, false>), gd, bd, 0, stream, g);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace clq

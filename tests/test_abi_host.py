@@ -72,12 +72,22 @@ def lib():
     L.clq_w4a4_rq_schedule.argtypes = [i64, i64, i64, i32, i32, p]
     L.clq_diag_mfma_probe_bytes.restype = ctypes.c_size_t
     L.clq_diag_mfma_probe.argtypes = [p, ctypes.c_size_t, i32, i32, p, p]
+    L.clq_weight_bytes_f6.restype = ctypes.c_size_t
+    L.clq_weight_bytes_f6.argtypes = [i64, i64]
+    L.clq_act_bytes_f6.restype = ctypes.c_size_t
+    L.clq_act_bytes_f6.argtypes = [i64, i64]
+    L.clq_quantize_weights_f6.argtypes = [p, p, i64, i64, i32, f32, p, p, p]
+    L.clq_rotate_quant_act_f6.argtypes = [p, i64, p, i64, i64, i32, p, p, p]
+    L.clq_w4a4_linear_f6.argtypes = [p, p, p, p, p, i64, i64, i64, p, i64, p]
+    L.clq_w4a4_accum_f6.argtypes = [p, p, i64, i64, i64, p, i64, p]
+    L.clq_unswizzle_f6.argtypes = [p, i64, i64, i32, p, p]
+    L.clq_f6_from_int4.argtypes = [p, i64, i64, i32, p, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 33, names
+    assert len(names) == 41, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -89,7 +99,7 @@ def test_binding_names_match_header():
 
 
 def test_version_and_strings(lib):
-    assert lib.clq_version() == 7
+    assert lib.clq_version() == 8
     for code in range(8):
         s = lib.clq_status_string(code).decode()
         assert s.startswith("CLQ")
@@ -447,3 +457,54 @@ def test_clps_validation(lib):
     assert cs(er=A + 4) == ALIGN
     assert cs(Y0=A + 2) == ALIGN
     assert cs(wsb=need - 1) == WORKSPACE
+
+
+def test_f6_sizes(lib):
+    assert lib.clq_weight_bytes_f6(1152, 1152) == 1152 * 1152 * 3 // 4
+    assert lib.clq_weight_bytes_f6(1, 64) == 64 * 64 * 3 // 4        # rows padded to 64
+    assert lib.clq_act_bytes_f6(45, 256) == 64 * 256 * 3 // 4        # rows padded to 32
+    assert lib.clq_act_bytes_f6(43200, 1152) == 43200 * 1152 * 3 // 4
+    assert lib.clq_weight_bytes_f6(0, 64) == 0
+    assert lib.clq_act_bytes_f6(8, 96) == 0
+
+
+def test_f6_validation(lib):
+    def rq6(X=A, ldx=1152, perm=None, M=4, K=1152, block=64, Xq=A, xs=A):
+        return lib.clq_rotate_quant_act_f6(X, ldx, perm, M, K, block, Xq, xs, None)
+    assert rq6(X=None) == NULL
+    assert rq6(M=0) == SHAPE
+    assert rq6(ldx=1000) == SHAPE
+    assert rq6(block=16) == BLOCK
+    assert rq6(Xq=A + 8) == ALIGN
+
+    def qw6(W=A, perm=None, N=8, K=1152, block=64, clip=1.0, Wq=A, ws=A):
+        return lib.clq_quantize_weights_f6(W, perm, N, K, block, clip, Wq, ws, None)
+    assert qw6(ws=None) == NULL
+    assert qw6(K=1000) == SHAPE
+    assert qw6(block=48) == BLOCK
+    assert qw6(clip=1.5) == ARG
+    assert qw6(W=MIS) == ALIGN
+
+    def lin6(Xq=A, xs=A, Wq=A, ws=A, bias=None, M=4, N=8, K=1152, Y=A, ldy=8):
+        return lib.clq_w4a4_linear_f6(Xq, xs, Wq, ws, bias, M, N, K, Y, ldy, None)
+    assert lin6(Xq=None) == NULL
+    assert lin6(xs=None) == NULL
+    assert lin6(K=64) == SHAPE          # k loops of two stages or more
+    assert lin6(K=96) == SHAPE
+    assert lin6(ldy=4) == SHAPE
+    assert lin6(ldy=12) == SHAPE        # fp16 rows: a multiple of 8 elements
+    assert lin6(Y=A + 8) == ALIGN
+    assert lin6(bias=A + 1) == ALIGN
+
+    def acc6(Xq=A, Wq=A, M=4, N=8, K=1152, acc=A, ldacc=8):
+        return lib.clq_w4a4_accum_f6(Xq, Wq, M, N, K, acc, ldacc, None)
+    assert acc6(acc=None) == NULL
+    assert acc6(K=64) == SHAPE
+    assert acc6(ldacc=10) == SHAPE      # int32 rows: a multiple of 4 elements
+    assert lib.clq_unswizzle_f6(None, 4, 1152, 0, A, None) == NULL
+    assert lib.clq_unswizzle_f6(A, 4, 1152, 2, A, None) == ARG
+    assert lib.clq_unswizzle_f6(A, 4, 1000, 0, A, None) == SHAPE
+    assert lib.clq_unswizzle_f6(A, 4, 1152, 1, A + 8, None) == ALIGN
+    assert lib.clq_f6_from_int4(A, 0, 1152, 0, A, None) == SHAPE
+    assert lib.clq_f6_from_int4(A, 4, 1152, 3, A, None) == ARG
+    assert lib.clq_f6_from_int4(A + 4, 4, 1152, 1, A, None) == ALIGN
