@@ -485,6 +485,12 @@ size_t clq_diag_mfma_probe_bytes(void);
 clq_status clq_diag_mfma_probe(const void *ops, size_t ops_bytes, int32_t iters, int32_t grid,
                                int32_t *sink, hipStream_t stream);
 
+/* The same loop on the fp6 matrix instruction (the clq_*_f6 path's): each
+ * workgroup runs iters x 16 x 4 v_mfma_f32_32x32x64_f8f6f4 on e2m3 codes
+ * of random int4 codes (2 x 32 x 32 x 64 ops each).  Same arguments. */
+clq_status clq_diag_mfma_probe_f6(const void *ops, size_t ops_bytes, int32_t iters, int32_t grid,
+                                  int32_t *sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

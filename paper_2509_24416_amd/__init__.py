@@ -87,6 +87,7 @@ _lib.clq_w4a4_rq_schedule.argtypes = [_i64, _i64, _i64, _i32, _i32, _p]
 _lib.clq_diag_mfma_probe_bytes.restype = ctypes.c_size_t
 _lib.clq_diag_mfma_probe_bytes.argtypes = []
 _lib.clq_diag_mfma_probe.argtypes = [_p, ctypes.c_size_t, _i32, _i32, _p, _p]
+_lib.clq_diag_mfma_probe_f6.argtypes = [_p, ctypes.c_size_t, _i32, _i32, _p, _p]
 _lib.clq_debug_get.argtypes = [_i32]
 _lib.clq_debug_get.restype = _i64
 _lib.clq_weight_bytes_f6.restype = ctypes.c_size_t
@@ -107,7 +108,7 @@ for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_w4a4_schedule", "clq_w4a4_linear_noalloc", "clq_diag_mfma_probe",
            "clq_w4a4_rq_linear", "clq_w4a4_rq_schedule", "clq_quantize_weights_f6",
            "clq_rotate_quant_act_f6", "clq_w4a4_linear_f6", "clq_w4a4_accum_f6", "clq_unswizzle_f6",
-           "clq_f6_from_int4"):
+           "clq_f6_from_int4", "clq_diag_mfma_probe_f6"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -121,7 +122,7 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_diag_mfma_probe_bytes", "clq_diag_mfma_probe", "clq_w4a4_rq_linear",
            "clq_w4a4_rq_schedule", "clq_weight_bytes_f6", "clq_act_bytes_f6", "clq_quantize_weights_f6",
            "clq_rotate_quant_act_f6", "clq_w4a4_linear_f6", "clq_w4a4_accum_f6", "clq_unswizzle_f6",
-           "clq_f6_from_int4")
+           "clq_f6_from_int4", "clq_diag_mfma_probe_f6")
 
 CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
 
@@ -176,6 +177,18 @@ def clq_diag_mfma_probe(ops, iters, grid, sink, stream=None):
     _check(_lib.clq_diag_mfma_probe(_ptr(ops), ops.numel(), iters, grid, _ptr(sink), _stream(stream)),
            "clq_diag_mfma_probe")
     return grid * iters * 64 * 2 * 32 ** 3
+
+
+def clq_diag_mfma_probe_f6(ops, iters, grid, sink, stream=None):
+    """clq_diag_mfma_probe on the fp6 matrix instruction; returns the ops it
+    performs (2 x 32 x 32 x 64 per instruction)."""
+    _dev(ops, "ops", torch.uint8)
+    _dev(sink, "sink", torch.int32)
+    if sink.numel() < grid * 256:
+        raise ValueError("sink needs grid * 256 elements")
+    _check(_lib.clq_diag_mfma_probe_f6(_ptr(ops), ops.numel(), iters, grid, _ptr(sink), _stream(stream)),
+           "clq_diag_mfma_probe_f6")
+    return grid * iters * 64 * 2 * 32 * 32 * 64
 
 
 def clq_w4a4_schedule(M, N, K, with_workspace=True):

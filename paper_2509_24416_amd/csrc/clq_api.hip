@@ -175,6 +175,15 @@ clq_status clq_diag_mfma_probe(const void *ops, size_t ops_bytes, int32_t iters,
     return done(stream, clq::launch_mfma_probe(ops, iters, sink, grid, stream));
 }
 
+clq_status clq_diag_mfma_probe_f6(const void *ops, size_t ops_bytes, int32_t iters, int32_t grid, int32_t *sink,
+                                  hipStream_t stream) {
+    if (!ops || !sink) return CLQ_ERR_NULL;
+    if (ops_bytes < clq::mfma_probe_bytes()) return CLQ_ERR_WORKSPACE;
+    if (iters < 1 || grid < 1 || grid > 65536) return CLQ_ERR_ARG;
+    if (!aligned(ops, 16) || !aligned(sink, 4)) return CLQ_ERR_ALIGN;
+    return done(stream, clq::launch_mfma_probe_f6(ops, iters, sink, grid, stream));
+}
+
 clq_status clq_debug_set(int32_t knob, int64_t value) {
     switch (knob) {
         case CLQ_DEBUG_SYNC:

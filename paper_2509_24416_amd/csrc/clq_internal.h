@@ -130,6 +130,8 @@ hipError_t launch_gemm_noalloc(const uint8_t *Xq, const float *xs, const uint8_t
 // bytes; sink receives one int per lane (grid * 256).
 size_t mfma_probe_bytes();
 hipError_t launch_mfma_probe(const void *ops, int iters, int *sink, int grid, hipStream_t stream);
+// the same on the fp6 matrix instruction (16 MFMAs of 32x32x64 per iteration)
+hipError_t launch_mfma_probe_f6(const void *ops, int iters, int *sink, int grid, hipStream_t stream);
 
 // Split-k wait bound (sleeps) and the test-only switch that stops
 // contributors from signalling; read at each launch.

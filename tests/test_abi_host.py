@@ -82,12 +82,13 @@ def lib():
     L.clq_w4a4_accum_f6.argtypes = [p, p, i64, i64, i64, p, i64, p]
     L.clq_unswizzle_f6.argtypes = [p, i64, i64, i32, p, p]
     L.clq_f6_from_int4.argtypes = [p, i64, i64, i32, p, p]
+    L.clq_diag_mfma_probe_f6.argtypes = [p, ctypes.c_size_t, i32, i32, p, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 41, names
+    assert len(names) == 42, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -508,3 +509,8 @@ def test_f6_validation(lib):
     assert lib.clq_f6_from_int4(A, 0, 1152, 0, A, None) == SHAPE
     assert lib.clq_f6_from_int4(A, 4, 1152, 3, A, None) == ARG
     assert lib.clq_f6_from_int4(A + 4, 4, 1152, 1, A, None) == ALIGN
+    nb = lib.clq_diag_mfma_probe_bytes()
+    assert lib.clq_diag_mfma_probe_f6(None, nb, 1, 1, A, None) == NULL
+    assert lib.clq_diag_mfma_probe_f6(A, nb - 1, 1, 1, A, None) == WORKSPACE
+    assert lib.clq_diag_mfma_probe_f6(A, nb, 0, 1, A, None) == ARG
+    assert lib.clq_diag_mfma_probe_f6(A, nb, 1, 1, A + 2, None) == ALIGN
