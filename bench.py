@@ -10,7 +10,10 @@ Default workload: the video DiT block, hidden 1152, MLP 4608, 16 latent
 frames x 30 x 45 patches x batch 2 -> M = 43200 tokens, Hadamard block 64
 (the largest per-layer shapes; rotate+quant's bandwidth-bound regime).
 `--workload pixart_block` (M = 8192) and `flux_block` (width 3072, M = 4608,
-block 128) time the other block configurations the same way.
+block 128) time the other block configurations the same way.  `--codes fp6`
+runs the same W4A4 step with the 4-bit codes stored as fp6 (e2m3) and the
+GEMM on the fp6 matrix instruction (clq_rotate_quant_act_f6 /
+clq_w4a4_linear_f6); its roofline is priced against the fp6 peak.
 
 Prints ONE JSON line:
   value      effective TOPS of the step = sum(2 M N K) / step time, the step
@@ -33,15 +36,18 @@ Prints ONE JSON line:
              steps right after the timed loop (its first second dropped:
              the readings trail the load)
   ceilings   measured ceilings beside the nominal peaks: a 1 GiB device copy
-             (HBM) and the library's matrix-core probe loop (int8 MFMA on
-             int4-shaped operands, two workgroups per compute unit), with the
-             clock and power during the probe; roofline.frac_of_measured_ceiling
-             and rotate_quant.*_frac_of_copy_ceiling divide by them
+             (HBM) and the library's matrix-core probe loops (int8 MFMA on
+             int4-shaped operands, and fp6 MFMA on the same codes as fp6; two
+             workgroups per compute unit), with the clock and power during
+             each probe; roofline.frac_of_measured_ceiling (against the probe
+             of the instruction the GEMM issues) and
+             rotate_quant.*_frac_of_copy_ceiling divide by them
   cpu_baseline  the CPU oracle timed on the host cores on a bounded sample
              of the same workload (token rows of every layer), plus one
              thread on a smaller sample
-  extra      the PixArt block (M = 8192) and the 28-block stack at 16384
-             tokens, timed the same way (context, not the headline)
+  extra      the other code storage on the same block, the PixArt block
+             (M = 8192) with both, and the 28-block stack at 16384 tokens,
+             timed the same way (context, not the headline)
 """
 import argparse
 import json
@@ -60,31 +66,36 @@ import numpy as np  # noqa: E402
 import workloads  # noqa: E402
 
 INT8_PEAK_TOPS = 5000.0      # dense int8 MFMA, MI355X (5.0 POP/s)
+FP6_PEAK_TOPS = 10100.0      # dense fp6 / fp4 MFMA, MI355X (10.1 PFLOP/s)
 HBM_PEAK_GBPS = 8000.0       # HBM3E, MI355X
 TRAFFIC_FILES = {
-    "video_block_m43200_h1152_b64": os.path.join(ROOT, "profiles", "gemm_traffic_video_block_m43200.txt"),
-    "flux_block_m4608_h3072_b128": os.path.join(ROOT, "profiles", "gemm_traffic_flux_block_m4608.txt"),
+    ("video_block_m43200_h1152_b64", "int4"): os.path.join(ROOT, "profiles", "gemm_traffic_video_block_m43200.txt"),
+    ("flux_block_m4608_h3072_b128", "int4"): os.path.join(ROOT, "profiles", "gemm_traffic_flux_block_m4608.txt"),
+    ("video_block_m43200_h1152_b64", "fp6"): os.path.join(ROOT, "profiles", "gemm_f6_traffic_video_block_m43200.txt"),
 }
 BLOCKS = {"video_block": workloads.C4, "pixart_block": workloads.C2, "flux_block": workloads.C3}
 
 
-def rq_bytes(l, abits=4):
+def rq_bytes(l, abits=4, codes="int4"):
     """Algorithmic HBM bytes of one rotate+quant launch: read M*K fp16, write
-    M*K/2 packed int4 codes (M*K int8 codes for 8-bit activations) and M fp32
-    scales."""
-    return l.M * (2 * l.K + (l.K // 2 if abits == 4 else l.K) + 4)
+    M*K/2 packed int4 codes (3*M*K/4 as fp6 codes, M*K int8 codes for 8-bit
+    activations) and M fp32 scales."""
+    out = (l.K // 2 if codes == "int4" else 3 * l.K // 4) if abits == 4 else l.K
+    return l.M * (2 * l.K + out + 4)
 
 
 def gemm_ops(l):
     return 2 * l.M * l.N * l.K
 
 
-def rq_kernel_name(l, abits=4):
+def rq_kernel_name(l, abits=4, codes="int4"):
     """The activation kernel the library runs for this layer: the 8-row
-    kernel for rows of 2048..5120 codes at block 64, else the batched one."""
+    kernel for rows of 2048..5120 codes at block 64, else the batched one
+    (code-width template argument 6: the 4-bit codes written as fp6)."""
+    qb = 6 if (abits == 4 and codes == "fp6") else abits
     if l.block == 64 and 2048 <= l.K <= 5120:
-        return f"rq_rows8_kernel<64, {abits}, false>"
-    return f"rq_act_kernel<{l.block}, {abits}, false>"
+        return f"rq_rows8_kernel<64, {qb}, false>"
+    return f"rq_act_kernel<{l.block}, {qb}, false>"
 
 
 def load_traffic(path, kernel_src_sha):
@@ -103,12 +114,13 @@ def load_traffic(path, kernel_src_sha):
     return float(vals["bytes_per_launch"])
 
 
-def kernel_sha():
+def kernel_sha(codes="int4"):
     """Hash of the GEMM kernel's source (the kernel the traffic figures
     describe)."""
     import hashlib
     h = hashlib.sha256()
-    h.update(open(os.path.join(ROOT, "paper_2509_24416_amd", "csrc", "w4a4_gemm.hip"), "rb").read())
+    src = "w4a4_gemm.hip" if codes == "int4" else "w4a4_f6.hip"
+    h.update(open(os.path.join(ROOT, "paper_2509_24416_amd", "csrc", src), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -278,8 +290,9 @@ def cpu_baseline(layers, inputs, budget_s=15.0, wbits=4, abits=4):
 
 
 def bench_block(wl, args, clq, torch, dev, wbits=4, abits=4, steps=None, warmup=None, cold_reps=None,
-                sample_clocks=True, clock_s=2.5):
-    """Times the hot path over the four linears of a DiT block workload.
+                sample_clocks=True, clock_s=2.5, codes="int4"):
+    """Times the hot path over the four linears of a DiT block workload
+    (codes: "int4", or "fp6" for the W4A4 path with its codes stored as fp6).
     Returns a dict of measurements (see the module docstring)."""
     steps = args.steps if steps is None else steps
     warmup = args.warmup if warmup is None else warmup
@@ -287,7 +300,10 @@ def bench_block(wl, args, clq, torch, dev, wbits=4, abits=4, steps=None, warmup=
     layers = list(wl.layers)
     inputs = {l.name: workloads.layer_inputs(l) for l in layers}
     quant_w = clq.clq_quantize_weights if wbits == 4 else clq.clq_quantize_weights8
-    if abits == 4:
+    if abits == 4 and codes == "fp6":
+        quant_w = clq.clq_quantize_weights_f6
+        act_bytes, rq_fn, lin_fn = clq.clq_act_bytes_f6, clq.clq_rotate_quant_act_f6, clq.clq_w4a4_linear_f6
+    elif abits == 4:
         act_bytes, rq_fn, lin_fn = clq.clq_act_bytes, clq.clq_rotate_quant_act, clq.clq_w4a4_linear
     else:
         act_bytes, rq_fn, lin_fn = clq.clq_act8_bytes, clq.clq_rotate_quant_act8, clq.clq_a8_linear
@@ -424,33 +440,38 @@ def measure_ceilings(clq, torch, dev, seconds=1.0):
     ops = torch.randint(0, 256, (clq.clq_diag_mfma_probe_bytes(),), dtype=torch.uint8, device=dev)
     grid = 2 * torch.cuda.get_device_properties(dev).multi_processor_count
     sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
-    n = clq.clq_diag_mfma_probe(ops, 200, grid, sink)   # warm up, and size the timed launches
-    torch.cuda.synchronize()
-    t = time.perf_counter()
-    clq.clq_diag_mfma_probe(ops, 200, grid, sink)
-    torch.cuda.synchronize()
-    t = time.perf_counter() - t
-    iters = max(200, int(200 * (seconds / 4) / max(t, 1e-6)))
-    sampler = ClockSampler(torch, dev)
-    with sampler:
-        for _ in range(4):   # brings the clock to its loaded state (and the readings up to date)
-            clq.clq_diag_mfma_probe(ops, iters, grid, sink)
-        e0.record()
-        for _ in range(4):
-            n = clq.clq_diag_mfma_probe(ops, iters, grid, sink)
-        e1.record()
-        e1.synchronize()
-    ms = e0.elapsed_time(e1) / 4
-    out["mfma_probe_TOPS"] = round(n / (ms * 1e-3) / 1e12, 1)
-    out["mfma_probe_frac_of_nominal"] = round(n / (ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)
-    out["mfma_probe_ms"] = round(ms, 3)
-    out["mfma_probe_clocks"] = sampler.summary(settle_s=1.0)
-    out["mfma_probe_note"] = ("v_mfma_i32_32x32x32_i8 loop on random int4 codes widened to 16 q, "
-                              f"{grid} workgroups x 4 waves, 8 accumulators per wave, no memory traffic")
+    probes = [("mfma_probe", clq.clq_diag_mfma_probe, INT8_PEAK_TOPS,
+               "v_mfma_i32_32x32x32_i8 loop on random int4 codes widened to 16 q"),
+              ("mfma_f6_probe", clq.clq_diag_mfma_probe_f6, FP6_PEAK_TOPS,
+               "v_mfma_f32_32x32x64_f8f6f4 (fp6 e2m3 operands) loop on random int4 codes as fp6")]
+    for key, probe, peak, what in probes:
+        n = probe(ops, 200, grid, sink)   # warm up, and size the timed launches
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        probe(ops, 200, grid, sink)
+        torch.cuda.synchronize()
+        t = time.perf_counter() - t
+        iters = max(200, int(200 * (seconds / 4) / max(t, 1e-6)))
+        sampler = ClockSampler(torch, dev)
+        with sampler:
+            for _ in range(4):   # brings the clock to its loaded state (and the readings up to date)
+                probe(ops, iters, grid, sink)
+            e0.record()
+            for _ in range(4):
+                n = probe(ops, iters, grid, sink)
+            e1.record()
+            e1.synchronize()
+        ms = e0.elapsed_time(e1) / 4
+        out[f"{key}_TOPS"] = round(n / (ms * 1e-3) / 1e12, 1)
+        out[f"{key}_frac_of_nominal"] = round(n / (ms * 1e-3) / 1e12 / peak, 4)
+        out[f"{key}_ms"] = round(ms, 3)
+        out[f"{key}_clocks"] = sampler.summary(settle_s=1.0)
+        out[f"{key}_note"] = (f"{what}, {grid} workgroups x 4 waves, 8 accumulators per wave, "
+                              "no memory traffic")
     return out
 
 
-def block_summary(wl, r, abits=4):
+def block_summary(wl, r, abits=4, codes="int4"):
     """Compact per-layer and per-kernel figures of a bench_block result."""
     layers = r["layers"]
     value = r["total_ops"] / (r["ms_per_step"] * 1e-3) / 1e12
@@ -462,10 +483,11 @@ def block_summary(wl, r, abits=4):
             "M": l.M, "K": l.K, "N": l.N,
             "gemm_us": pct(r["gm_t"][:, i] * 1e3), "gemm_TOPS": round(gemm_ops(l) / (r["gemm_ms"][i] * 1e-3) / 1e12, 1),
             "gemm_cold_us": round(float(r["cold_gemm"][i]) * 1e3, 2) if np.isfinite(r["cold_gemm"][i]) else None,
-            "rq_kernel": rq_kernel_name(l, abits),
-            "rq_us": pct(r["rq_t"][:, i] * 1e3), "rq_GBps": round(rq_bytes(l, abits) / (r["rq_ms"][i] * 1e-3) / 1e9, 1),
+            "rq_kernel": rq_kernel_name(l, abits, codes),
+            "rq_us": pct(r["rq_t"][:, i] * 1e3),
+            "rq_GBps": round(rq_bytes(l, abits, codes) / (r["rq_ms"][i] * 1e-3) / 1e9, 1),
             "rq_cold_us": round(float(r["cold_rq"][i]) * 1e3, 2) if np.isfinite(r["cold_rq"][i]) else None,
-            "rq_cold_GBps": (round(rq_bytes(l, abits) / (r["cold_rq"][i] * 1e-3) / 1e9, 1)
+            "rq_cold_GBps": (round(rq_bytes(l, abits, codes) / (r["cold_rq"][i] * 1e-3) / 1e9, 1)
                              if np.isfinite(r["cold_rq"][i]) else None)}
     return dict(value=value, gemm_avg_ms=gemm_avg_ms, ops_launch=ops_launch, per=per)
 
@@ -831,6 +853,9 @@ def main():
                          "clip search; dit_stack: the 28-block stack, one HIP graph per step; "
                          "gemm_schedule: the GEMM's automatic kernel choice against every forced schedule "
                          "on shapes outside the block workloads")
+    ap.add_argument("--codes", default="int4", choices=["int4", "fp6"],
+                    help="W4A4 operand storage: int4 (nibble-packed, int8 matrix instructions; default) or fp6 "
+                         "(the same codes as e2m3, fp6 matrix instructions)")
     ap.add_argument("--sweep-block-shapes", action="store_true",
                     help="gemm_schedule: sweep the block workloads' own layer shapes instead")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -876,25 +901,36 @@ def main():
         wbits, abits = 4, 8
     elif args.workload.endswith("_w8a8"):
         wbits, abits = 8, 8
+    codes = args.codes
+    if codes == "fp6" and (wbits, abits) != (4, 4):
+        print("bench.py: --codes fp6 applies to the W4A4 workloads only", file=sys.stderr)
+        sys.exit(2)
     wl = BLOCKS[base]
-    print(f"bench: {wl.name} W{wbits}A{abits}: {args.warmup} warmup + {args.steps} timed steps",
+    print(f"bench: {wl.name} W{wbits}A{abits} ({codes} codes): {args.warmup} warmup + {args.steps} timed steps",
           file=sys.stderr, flush=True)
-    r = bench_block(wl, args, clq, torch, dev, wbits, abits, sample_clocks=not args.no_clocks)
-    sm = block_summary(wl, r, abits)
+    r = bench_block(wl, args, clq, torch, dev, wbits, abits, sample_clocks=not args.no_clocks, codes=codes)
+    sm = block_summary(wl, r, abits, codes)
     layers = r["layers"]
     achieved = sm["ops_launch"] / (sm["gemm_avg_ms"] * 1e-3) / 1e12
-    rq_avg_bytes = sum(rq_bytes(l, abits) for l in layers) / len(layers)
+    rq_avg_bytes = sum(rq_bytes(l, abits, codes) for l in layers) / len(layers)
     rq_achieved = rq_avg_bytes / (float(r["rq_ms"].mean()) * 1e-3) / 1e9
-    cold_bytes = sum(rq_bytes(l, abits) for l in layers)
+    cold_bytes = sum(rq_bytes(l, abits, codes) for l in layers)
     cold_rq_total = float(np.nansum(r["cold_rq"]))
     cold_gbps = cold_bytes / (cold_rq_total * 1e-3) / 1e9 if cold_rq_total > 0 else 0.0
-    traffic = load_traffic(TRAFFIC_FILES.get(wl.name), kernel_sha()) if (wbits, abits) == (4, 4) else None
-    plans = [clq.clq_w4a4_schedule(l.M, l.N, l.K) for l in layers] if abits == 4 else None
-    if abits == 4:
+    traffic = (load_traffic(TRAFFIC_FILES.get((wl.name, codes)), kernel_sha(codes))
+               if (wbits, abits) == (4, 4) else None)
+    plans = [clq.clq_w4a4_schedule(l.M, l.N, l.K) for l in layers] if (abits == 4 and codes == "int4") else None
+    if codes == "fp6":
+        gemm_name = "f6_gemm_kernel (mean over the 4 linears)"
+    elif abits == 4:
         kinds = sorted({("w4a4_gemm_kernel" if p["kernel"] == 0 else "w4a4_gemm_halves_kernel") for p in plans})
         gemm_name = " / ".join(kinds) + " (mean over the 4 linears)"
     else:
         gemm_name = f"a8_gemm_kernel<{wbits}> (mean over the 4 linears)"
+    # the roofline prices a launch against the peak of the matrix
+    # instruction it issues: int8 for the int4 path (codes widened to int8),
+    # fp6 for the fp6-stored codes
+    peak = FP6_PEAK_TOPS if codes == "fp6" else INT8_PEAK_TOPS
     setting = f"W{wbits}A{abits}"
     out = {
         "metric": f"{setting} linear effective TOPS + % int8-MFMA peak; rotate+quant HBM GB/s",
@@ -907,17 +943,23 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int4" if (wbits, abits) == (4, 4) else ("int4 x int8" if wbits == 4 else "int8"),
+        "dtype": ("fp6" if codes == "fp6" else "int4") if (wbits, abits) == (4, 4) else
+                 ("int4 x int8" if wbits == 4 else "int8"),
         "data": "synthetic",
-        "config": {"workload": wl.name + ("" if (wbits, abits) == (4, 4) else f"_{setting.lower()}"),
+        "config": {"workload": wl.name + ("" if (wbits, abits) == (4, 4) else f"_{setting.lower()}")
+                   + ("_fp6codes" if codes == "fp6" else ""),
+                   "codes": codes,
                    "M": layers[0].M, "hidden": layers[0].K, "mlp": layers[2].N,
                    "block": layers[0].block, "layers": {l.name.split(".")[1]: [l.K, l.N] for l in layers},
                    "parallelism": "none (one GPU)"},
         "pct_int8_peak": round(100 * sm["value"] / INT8_PEAK_TOPS, 2),
         "step_ms_percentiles": pct(r["step_ms"]),
         "roofline": {"kernel": gemm_name, "bound": "mfma", "achieved": round(achieved, 1),
-                     "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / INT8_PEAK_TOPS, 4),
+                     "peak": peak, "unit": "TFLOP/s",
+                     "peak_instruction": ("fp6 MFMA (dense 10.1 PFLOP/s)" if codes == "fp6"
+                                          else "int8 MFMA (dense 5.0 POP/s)"),
+                     "frac": round(achieved / peak, 4),
+                     "frac_of_int8_peak": round(achieved / INT8_PEAK_TOPS, 4),
                      "traffic": traffic, "avg_launch_us": round(sm["gemm_avg_ms"] * 1e3, 2),
                      "ops_per_launch": sm["ops_launch"],
                      "launch_us_percentiles": pct(r["gm_t"].mean(axis=1) * 1e3)},
@@ -925,7 +967,7 @@ def main():
         # 512 MB read flush); the in-step figure has each launch follow the
         # previous linear's GEMM, whose output lines are still being written
         # back, so it measures the pipeline rather than the kernel
-        "rotate_quant": {"kernels": {l.name: rq_kernel_name(l, abits) for l in layers}, "bound": "hbm",
+        "rotate_quant": {"kernels": {l.name: rq_kernel_name(l, abits, codes) for l in layers}, "bound": "hbm",
                          "basis": "cold cache, all four launches" if cold_rq_total > 0 else "in step",
                          "achieved": round(cold_gbps if cold_rq_total > 0 else rq_achieved, 1),
                          "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -944,7 +986,8 @@ def main():
         print("bench: measured ceilings", file=sys.stderr, flush=True)
         ceil = measure_ceilings(clq, torch, dev)
         out["ceilings"] = ceil
-        out["roofline"]["frac_of_measured_ceiling"] = round(achieved / ceil["mfma_probe_TOPS"], 4)
+        out["roofline"]["frac_of_measured_ceiling"] = round(
+            achieved / ceil["mfma_f6_probe_TOPS" if codes == "fp6" else "mfma_probe_TOPS"], 4)
         out["rotate_quant"]["frac_of_copy_ceiling"] = round(out["rotate_quant"]["achieved"] / ceil["hbm_copy_GBps"], 4)
         out["rotate_quant"]["in_step_frac_of_copy_ceiling"] = round(rq_achieved / ceil["hbm_copy_GBps"], 4)
     if not args.no_cpu_baseline:
@@ -952,21 +995,26 @@ def main():
     r = None
     if not args.no_extra and (wbits, abits) == (4, 4):
         extra = {}
-        for name in ("video_block", "pixart_block"):
-            if name == base:
+        for name, c2 in (("video_block", "int4"), ("video_block", "fp6"), ("pixart_block", "int4"),
+                         ("pixart_block", "fp6")):
+            if (name, c2) == (base, codes):
                 continue
             wl2 = BLOCKS[name]
-            print(f"bench: extra {wl2.name}", file=sys.stderr, flush=True)
+            key = wl2.name + ("_fp6codes" if c2 == "fp6" else "")
+            print(f"bench: extra {key}", file=sys.stderr, flush=True)
             r2 = bench_block(wl2, args, clq, torch, dev, steps=max(20, args.steps // 2),
-                             warmup=max(20, args.warmup // 2), cold_reps=0, sample_clocks=False)
-            s2 = block_summary(wl2, r2)
-            extra[wl2.name] = {"value_TOPS": round(s2["value"], 2), "ms_per_step": round(r2["ms_per_step"], 5),
-                               "step_ms_percentiles": pct(r2["step_ms"]),
-                               "gemm_avg_us": round(s2["gemm_avg_ms"] * 1e3, 2),
-                               "gemm_frac": round(s2["ops_launch"] / (s2["gemm_avg_ms"] * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
-                               "per_layer": {k: {"gemm_us": v["gemm_us"]["median"], "gemm_TOPS": v["gemm_TOPS"],
-                                                 "rq_us": v["rq_us"]["median"], "rq_GBps": v["rq_GBps"]}
-                                             for k, v in s2["per"].items()}}
+                             warmup=max(20, args.warmup // 2), cold_reps=0, sample_clocks=False, codes=c2)
+            s2 = block_summary(wl2, r2, codes=c2)
+            g_tops = s2["ops_launch"] / (s2["gemm_avg_ms"] * 1e-3) / 1e12
+            extra[key] = {"codes": c2, "value_TOPS": round(s2["value"], 2),
+                          "ms_per_step": round(r2["ms_per_step"], 5),
+                          "step_ms_percentiles": pct(r2["step_ms"]),
+                          "gemm_avg_us": round(s2["gemm_avg_ms"] * 1e3, 2),
+                          "gemm_frac": round(g_tops / (FP6_PEAK_TOPS if c2 == "fp6" else INT8_PEAK_TOPS), 4),
+                          "gemm_frac_of_int8_peak": round(g_tops / INT8_PEAK_TOPS, 4),
+                          "per_layer": {k: {"gemm_us": v["gemm_us"]["median"], "gemm_TOPS": v["gemm_TOPS"],
+                                            "rq_us": v["rq_us"]["median"], "rq_GBps": v["rq_GBps"]}
+                                        for k, v in s2["per"].items()}}
             del r2
         print("bench: extra dit_stack m16384", file=sys.stderr, flush=True)
         extra["dit_stack_28x4_m16384_h1152_b64"] = stack_point(clq, torch, dev, 16384, 64, steps=20)

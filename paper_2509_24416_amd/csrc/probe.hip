@@ -68,8 +68,8 @@ __global__ void __launch_bounds__(256, 2) mfma_probe_f6_kernel(const uint32_t *_
         const uint32_t *q = p + 64 * 4;
         const uint32_t dp[4] = {p[0], p[1], p[2], p[3]}, dq[4] = {q[0], q[1], q[2], q[3]};
         uint32_t wp[6], wq[6];
-        f6_from_nibbles(dp, wp);   // a random nibble is -8..7; -8 has no fp6 code here and
-        f6_from_nibbles(dq, wq);   // comes out as -7.5, which only shifts the sums
+        f6_from_nibbles(dp, wp);   // a random nibble is -8..7; -8 is off the code grid and
+        f6_from_nibbles(dq, wq);   // comes out as 0, which only changes the sums
         a[i] = v8i{(int)wp[0], (int)wp[1], (int)wp[2], (int)wp[3], (int)wp[4], (int)wp[5], 0, 0};
         b[i] = v8i{(int)wq[0], (int)wq[1], (int)wq[2], (int)wq[3], (int)wq[4], (int)wq[5], 0, 0};
     }

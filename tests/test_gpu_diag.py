@@ -32,3 +32,24 @@ def test_mfma_probe_runs_and_is_deterministic(clq):
     clq.clq_diag_mfma_probe(ops, 4, grid, s2)
     torch.cuda.synchronize()
     assert not np.array_equal(a, s2.cpu().numpy())
+
+
+def test_mfma_probe_f6_runs_and_is_deterministic(clq):
+    g = torch.Generator(device="cpu").manual_seed(6)
+    ops = torch.randint(0, 256, (clq.clq_diag_mfma_probe_bytes(),), dtype=torch.uint8, generator=g).cuda()
+    grid = 8
+    s1 = torch.zeros(grid * 256, dtype=torch.int32, device="cuda")
+    s2 = torch.zeros_like(s1)
+    n = clq.clq_diag_mfma_probe_f6(ops, 3, grid, s1)
+    clq.clq_diag_mfma_probe_f6(ops, 3, grid, s2)
+    torch.cuda.synchronize()
+    assert n == grid * 3 * 64 * 2 * 32 * 32 * 64
+    a, b = s1.cpu().numpy(), s2.cpu().numpy()
+    # each lane stores the float sum of its accumulators: integer-valued
+    # (products of codes on the integer grid, exact in fp32) and finite
+    f = a.view(np.float32)
+    assert np.array_equal(a, b) and np.count_nonzero(a) > a.size // 2
+    assert np.all(np.isfinite(f)) and np.array_equal(f, np.round(f))
+    clq.clq_diag_mfma_probe_f6(ops, 4, grid, s2)
+    torch.cuda.synchronize()
+    assert not np.array_equal(a, s2.cpu().numpy())
