@@ -299,7 +299,9 @@ __global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
 
     // ---- epilogue: lane owns token m and 16 consecutive channels ----------------
     const int h16 = (lane >> 5) * 16;
-    auto epilogue = [&](int L, int sj) {
+    // always inlined: an outlined epilogue takes the accumulators by reference
+    // (through memory) and the ragged-shape instances then spill
+    auto epilogue = [&](int L, int sj) __attribute__((always_inline)) {
         int tm, tn;
         coords(L, tm, tn);
         uint32_t lx = (uint32_t)((wm * kFM * 32 + (lane & 31)) * 4);
@@ -434,7 +436,7 @@ __global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
     Seg cc{-1, 0, 0};
     next_seg(cc);
     int s = 0;
-    auto iter = [&](auto qc) -> bool {
+    auto iter = [&](auto qc) __attribute__((always_inline)) -> bool {
         constexpr int q = decltype(qc)::value;
         constexpr IC<(q + 1) % NS> nqc{};
         take_operands();
