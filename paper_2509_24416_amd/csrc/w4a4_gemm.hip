@@ -155,6 +155,7 @@ struct GemmArgs {
     int *status;   // split-k status words (kStatusBytes at the workspace head)
     int spin_limit;   // bound on a wait for a contributor's flag (sleeps)
     int drop_signal;  // test only: contributors never raise their flags
+    int full_grid;    // two workgroups on every compute unit (the uneven deal applies only then)
     // fused rotate+quantize (the two-halves kernel with FB != 0): fp16
     // activations fx (row stride ldfx) quantized into Xq / xs by the first
     // n_rq work items (rq_rows rows each), the GEMM tiles after them; qhdr:
@@ -210,7 +211,21 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
     const int per = dp >> 3, rem = dp & 7;
     const int cnt = per + (xcd < rem ? 1 : 0);
     const int dstart = xcd * per + min(xcd, rem);
-    const int my_dp = jw < cnt ? (cnt - jw + gx - 1) / gx : 0;
+    // Uneven deal on a full grid of whole tiles (several rounds): the two
+    // workgroups on a compute unit do not progress at the same rate (the one
+    // placed first, jw < gx / 2 in dispatch order, wins the issue arbitration
+    // and finishes a tile in about two thirds of the other's time), so the
+    // later one gets about 40% of the unit's tiles: nb rounds for every
+    // workgroup, the remaining rr tiles for the first half only.
+    const int H = gx >> 1;
+    const bool asym = S == 0 && G == a.full_grid && cnt >= 4 * gx;
+    int nb = 0, rr = 0;
+    if (asym) {
+        nb = min(cnt / gx, (cnt * 2 * 40 + gx * 50) / (gx * 100));
+        rr = cnt - nb * gx;
+    }
+    const int my_dp = !asym ? (jw < cnt ? (cnt - jw + gx - 1) / gx : 0)
+                            : nb + (jw < H && jw < rr ? (rr - jw + H - 1) / H : 0);
     const int sk_a = rank * S / G, sk_b = (rank + 1) * S / G;
     const int total = my_dp * nks + (sk_b - sk_a);
     if (total == 0) return;
@@ -234,7 +249,7 @@ __global__ void __launch_bounds__(C::NT, C::WGS) w4a4_gemm_kernel(GemmArgs a)
     auto next_seg = [&](Seg &c) {
         ++c.j;
         if (c.j < my_dp) {
-            c.L = dstart + jw + c.j * gx;
+            c.L = !asym || c.j < nb ? dstart + jw + c.j * gx : dstart + nb * gx + jw + (c.j - nb) * H;
             c.kb = 0;
             c.ke = nks;
         } else {
@@ -1206,6 +1221,7 @@ template <class C, bool I32OUT, bool RAGGED, bool BIAS, bool ERR = false>
 hipError_t launch_cfg(GemmArgs g, bool may_split, hipStream_t stream) {
     int grid;
     plan_persistent(g.tiles_m * g.tiles_n, g.K >> 6, may_split, g.dp, g.sk, grid);
+    g.full_grid = full_grid();
     hipLaunchKernelGGL((w4a4_gemm_kernel<C, I32OUT, RAGGED, BIAS, ERR>), dim3((unsigned)grid), dim3(C::NT), 0, stream, g);
     return hipGetLastError();
 }
