@@ -658,11 +658,11 @@ def stack_weights(torch, dev, nb=28):
     return _STACK_W[nb]
 
 
-def stack_point(clq, torch, dev, M, b, steps, perms=None, fold=False, eager=False, fuse=False):
+def stack_point(clq, torch, dev, M, b, steps, perms=None, fold=False, eager=False, fuse=False, codes="int4"):
     """One stack configuration: graph replays timed back to back, plus
     single-replay percentiles (events at replay boundaries)."""
     from paper_2509_24416_amd.stack import DiTStack
-    st = DiTStack(stack_weights(torch, dev), M, b, perms=perms, fold=fold, fuse=fuse)
+    st = DiTStack(stack_weights(torch, dev), M, b, perms=perms, fold=fold, fuse=fuse, codes=codes)
     x = torch.from_numpy(workloads.activations(M, 1152, "L1", 500)).to(dev)
     st.forward(x)
     st.capture()
@@ -706,9 +706,9 @@ def bench_stack(args, clq, torch, dev):
     of resident int4 weights), rotate+quant + W4A4 GEMM per linear, replayed
     as one HIP graph.  value = effective TOPS at M = 4096 tokens, block 64;
     M = 1024 / 16384, the eager step, the Hadamard block sweep 32 / 64 / 128
-    at every M, and the stack with each input's rotate+quantize folded into
-    its GEMM launch where the schedule allows (clq_w4a4_rq_linear) are
-    reported beside it."""
+    at every M, the stack with each input's rotate+quantize folded into its
+    GEMM launch where the schedule allows (clq_w4a4_rq_linear), and the stack
+    on the fp6 storage of the codes are reported beside it."""
     nb = 28
     res, fused = {}, {}
     for M in (4096, 1024, 16384):
@@ -719,6 +719,12 @@ def bench_stack(args, clq, torch, dev):
         # the same stack with each rotate+quantize folded into its GEMM launch
         # where the schedule allows (clq_w4a4_rq_linear)
         fused[M] = stack_point(clq, torch, dev, M, 64, max(5, args.steps // 4), fuse=True)
+    # the same stack on the fp6 storage of the codes, block 64
+    fp6 = {}
+    for M in (4096, 1024, 16384):
+        print(f"bench: dit_stack M={M} block=64 fp6 codes", file=sys.stderr, flush=True)
+        fp6[M] = stack_point(clq, torch, dev, M, 64, args.steps if M == 4096 else max(5, args.steps // 4),
+                             codes="fp6")
     # one swap vector per layer input (random stand-ins for OBS outputs):
     # gathered by every rotate+quant, or folded into the producing layers
     from paper_2509_24416_amd.stack import LAYERS
@@ -739,6 +745,7 @@ def bench_stack(args, clq, torch, dev):
                    "launches_per_step": 2 * 4 * nb, "parallelism": "none (one GPU)"},
         "per_M_block": {f"M{M}_b{b}": v for (M, b), v in res.items()},
         "fused_block64": {f"M{M}": v for M, v in fused.items()},
+        "fp6codes_block64": {f"M{M}": v for M, v in fp6.items()},
         "swap_vectors_m4096": swap,
         "gpu": torch.cuda.get_device_name(dev),
     }
@@ -1018,6 +1025,8 @@ def main():
             del r2
         print("bench: extra dit_stack m16384", file=sys.stderr, flush=True)
         extra["dit_stack_28x4_m16384_h1152_b64"] = stack_point(clq, torch, dev, 16384, 64, steps=20)
+        extra["dit_stack_28x4_m16384_h1152_b64_fp6codes"] = stack_point(clq, torch, dev, 16384, 64, steps=20,
+                                                                         codes="fp6")
         out["extra"] = extra
     print(json.dumps(out), flush=True)
 

@@ -70,7 +70,6 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
-typedef _Float16 h2v __attribute__((ext_vector_type(2)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 template <int Q> using IC = std::integral_constant<int, Q>;
@@ -105,6 +104,17 @@ __device__ __forceinline__ uint32_t fma_mix2(float p0, float w0, float p1, float
         "v_fma_mixhi_f16 %0, %4, %5, %3 op_sel:[0,0,1] op_sel_hi:[0,0,1]"
         : "=&v"(r)
         : "v"(p0), "v"(w0), "v"(b), "v"(p1), "v"(w1));
+    return r;
+}
+
+// the same with fp32 bias operands (each exactly an fp16 value), so that
+// every kernel's outputs are rounded by the same instruction
+__device__ __forceinline__ uint32_t fma_mix2f(float p0, float w0, float b0, float p1, float w1, float b1) {
+    uint32_t r;
+    asm("v_fma_mixlo_f16 %0, %1, %2, %3\n\t"
+        "v_fma_mixhi_f16 %0, %4, %5, %6"
+        : "=&v"(r)
+        : "v"(p0), "v"(w0), "v"(b0), "v"(p1), "v"(w1), "v"(b1));
     return r;
 }
 
@@ -1115,10 +1125,7 @@ __global__ void __launch_bounds__(2 * C::NT, 2) w4a4_gemm_halves_kernel(GemmArgs
 #pragma unroll
             for (int v = 0; v < 16; v += 2) {
                 const float p0 = (float)x[v] * xsc, p1 = (float)x[v + 1] * xsc;
-                h2v hh;
-                hh[0] = (_Float16)__builtin_fmaf(p0, wsv[v], bw[v]);
-                hh[1] = (_Float16)__builtin_fmaf(p1, wsv[v + 1], bw[v + 1]);
-                hv[v / 2] = __builtin_bit_cast(uint32_t, hh);
+                hv[v / 2] = fma_mix2f(p0, wsv[v], bw[v], p1, wsv[v + 1], bw[v + 1]);
             }
             uint16_t *dst = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)m * a.ldy + n0;
             if (m < M && n0 < N) {

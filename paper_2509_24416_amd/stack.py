@@ -19,13 +19,18 @@ and the consumer's rotate+quant reads it in order.  Each output channel is
 computed independently, so the folded stack produces the same bits.  The
 stack's first input has no producer inside the stack and keeps its gather.
 
+codes="fp6" runs every linear on the fp6 storage of the same codes
+(clq_rotate_quant_act_f6 + clq_w4a4_linear_f6); the fp16 outputs are the
+same bits as with int4 storage.
+
 Paper: "CLQ" (arXiv 2509.24416) -- the method quantizes every linear of the
 DiT blocks (Sec. 4.1, W4A4), with the online rotation of Sec. 3.3 in front of
 each.
 """
 import torch
 
-from . import (clq_act_bytes, clq_quantize_weights, clq_rotate_quant_act, clq_w4a4_linear,
+from . import (clq_act_bytes, clq_act_bytes_f6, clq_quantize_weights, clq_quantize_weights_f6,
+               clq_rotate_quant_act, clq_rotate_quant_act_f6, clq_w4a4_linear, clq_w4a4_linear_f6,
                clq_w4a4_rq_linear, clq_w4a4_workspace_bytes)
 
 LAYERS = ("qkv", "proj", "fc1", "fc2")
@@ -38,9 +43,16 @@ class DiTStack:
     (int32 [K]) for every layer input, or perms: one dict per block mapping a
     layer name to its input's swap vector (or None).  fold: reorder each
     producer's output channels by its consumer's swap vector instead of
-    gathering in the consumer's rotate+quant."""
+    gathering in the consumer's rotate+quant.  codes: "int4" (default) or
+    "fp6" (the codes stored as fp6 for the fp6 matrix instructions; not with
+    fuse)."""
 
-    def __init__(self, weights, M, block=64, perm=None, perms=None, fold=False, fuse=False):
+    def __init__(self, weights, M, block=64, perm=None, perms=None, fold=False, fuse=False, codes="int4"):
+        if codes not in ("int4", "fp6"):
+            raise ValueError(f"codes must be 'int4' or 'fp6', not {codes!r}")
+        if codes == "fp6" and fuse:
+            raise ValueError("the fused launch takes int4 codes only")
+        self.codes = codes
         self.M, self.block = M, block
         # fuse: each layer's rotate+quantize and GEMM through clq_w4a4_rq_linear
         # (one launch where its schedule allows; inputs that still gather by
@@ -81,15 +93,17 @@ class DiTStack:
                 if r is not None:   # one-time reorder of the layer's parameters
                     W = W.index_select(0, r.long()).contiguous()
                     b = None if b is None else b.index_select(0, r.long()).contiguous()
-                q[name] = (clq_quantize_weights(W, block, perm=perms[j][name]), b)
+                quant = clq_quantize_weights_f6 if codes == "fp6" else clq_quantize_weights
+                q[name] = (quant(W, block, perm=perms[j][name]), b)
             self.blocks.append(q)
         h, f = self.hidden, self.mlp
         f16 = dict(dtype=torch.float16, device=dev)
         self.x_in = torch.empty((M, h), **f16)
         self.out = {"qkv": torch.empty((M, 3 * h), **f16), "proj": torch.empty((M, h), **f16),
                     "fc1": torch.empty((M, f), **f16), "fc2": torch.empty((M, h), **f16)}
-        self.xq = {h: torch.empty(clq_act_bytes(M, h), dtype=torch.uint8, device=dev),
-                   f: torch.empty(clq_act_bytes(M, f), dtype=torch.uint8, device=dev)}
+        act_bytes = clq_act_bytes_f6 if codes == "fp6" else clq_act_bytes
+        self.xq = {h: torch.empty(act_bytes(M, h), dtype=torch.uint8, device=dev),
+                   f: torch.empty(act_bytes(M, f), dtype=torch.uint8, device=dev)}
         self.xs = torch.empty(M, dtype=torch.float32, device=dev)
         # the GEMM workspace of this stack: every launch (eager or replayed)
         # runs in the order of one stream, so one is enough
@@ -118,7 +132,10 @@ class DiTStack:
                 qw, b = blk[name]
                 x = self._input(j, name)
                 xq = self.xq[qw.K]
-                if self.fuse and self.gather[j][name] is None:
+                if self.codes == "fp6":
+                    clq_rotate_quant_act_f6(x, self.block, perm=self.gather[j][name], out=xq, scale_out=self.xs)
+                    clq_w4a4_linear_f6(xq, self.xs, qw, b, out=self.out[name])
+                elif self.fuse and self.gather[j][name] is None:
                     clq_w4a4_rq_linear(x, self.block, qw, b, Xq_out=xq, scale_out=self.xs, out=self.out[name],
                                        workspace=self.ws)
                 else:

@@ -518,10 +518,13 @@ def test_forced_schedules_agree(clq, M, N, K):
             Y = host(clq.clq_w4a4_linear(Xq, xs, qw, dev(b), workspace=ws))
             assert clq.clq_w4a4_workspace_status(ws) == [0, 0, 0]
             if ref is None:
-                ref = acc
+                ref, refY = acc, Y
                 assert np.array_equal(acc[rows], r["acc"])
             else:
                 assert np.array_equal(acc, ref), force
+                # every kernel rounds the same products with the same
+                # instruction: the fp16 outputs agree bit for bit too
+                assert np.array_equal(Y.view(np.uint16), refY.view(np.uint16)), force
             assert oracle.err_metric(Y[rows].astype(np.float64), r["y64"], r["p64"], b) <= TOL, force
     finally:
         clq.clq_debug_set(3, 0)

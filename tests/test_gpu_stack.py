@@ -58,7 +58,7 @@ def stack_weights(nblocks, M, block):
     return wl, host_w
 
 
-def build(nblocks, M, block):
+def build(nblocks, M, block, codes="int4"):
     from paper_2509_24416_amd.stack import DiTStack
     wl, host_w = stack_weights(nblocks, M, block)
     weights = []
@@ -69,12 +69,13 @@ def build(nblocks, M, block):
             blk[l.name.split(".")[1]] = (dev(W), dev(b))
         weights.append(blk)
     x = workloads.activations(M, wl.layers[0].K, "L1", wl.layers[0].seed)
-    return DiTStack(weights, M, block), host_w, x
+    return DiTStack(weights, M, block, codes=codes), host_w, x
 
 
-@pytest.mark.parametrize("M,block", [(1024, 64), (300, 32), (512, 128)])
-def test_layers_match_oracle_on_their_inputs(clq, M, block):
-    st, host_w, x = build(3, M, block)
+@pytest.mark.parametrize("M,block,codes", [(1024, 64, "int4"), (300, 32, "int4"), (512, 128, "int4"),
+                                           (300, 32, "fp6"), (512, 128, "fp6")])
+def test_layers_match_oracle_on_their_inputs(clq, M, block, codes):
+    st, host_w, x = build(3, M, block, codes)
     taps = {(0, "qkv"): None, (0, "proj"): None, (1, "fc1"): None, (1, "fc2"): None, (2, "qkv"): None,
             (2, "fc2"): None}
     st.forward(dev(x), taps=taps)
@@ -171,3 +172,29 @@ def test_swap_folded_upstream_matches_gather(clq, M, block):
         assert np.array_equal(xf.view(np.uint16), want.view(np.uint16)), (j, name)
     # the folded stack gathers only at its first input
     assert [f.gather[j][n] is None for j in range(nb) for n in LAYERS].count(False) == 1
+
+
+def test_fp6_stack_matches_int4_stack(clq):
+    # the same codes in either storage give the same fp16 outputs layer by
+    # layer, so the whole chain stays bit-identical; the fp6 stack also
+    # replays as a graph
+    M, block = 1024, 64
+    st4, _, x = build(6, M, block, "int4")
+    y4 = host(st4.forward(dev(x))).copy()
+    del st4
+    st6, _, _ = build(6, M, block, "fp6")
+    y6 = host(st6.forward(dev(x))).copy()
+    assert np.array_equal(y4.view(np.uint16), y6.view(np.uint16))
+    st6.capture()
+    for _ in range(2):
+        got = host(st6.replay(dev(x)))
+        assert np.array_equal(got.view(np.uint16), y6.view(np.uint16))
+
+
+def test_fp6_stack_rejects_fuse(clq):
+    # checked before any weight is touched
+    from paper_2509_24416_amd.stack import DiTStack
+    with pytest.raises(ValueError):
+        DiTStack([], 64, 64, fuse=True, codes="fp6")
+    with pytest.raises(ValueError):
+        DiTStack([], 64, 64, codes="int8")
