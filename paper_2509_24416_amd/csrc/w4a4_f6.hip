@@ -89,14 +89,32 @@ __device__ __forceinline__ uint32_t fma_mix2(float p0, float w0, float p1, float
 constexpr int kUnit = kF6Unit;  // bytes of a 32 x 64 fp6 unit
 constexpr int kNS = 4;          // ring slots
 constexpr int kGroupM = 8;      // token panels per tile group (L2 reuse of channel panels)
-constexpr int kWN = 1, kWM = 4, kFN = 4, kFM = 2;
-constexpr int kNW = kWN * kWM, kNT = kNW * 64;
-constexpr int kBN = kWN * kFN * 32, kBM = kWM * kFM * 32;
-constexpr int kWUnits = kBN / 32, kXUnits = kBM / 32, kUnits = kWUnits + kXUnits;
-constexpr int kUPW = kUnits / kNW;          // units per wave and stage
-constexpr int kVPW = 2 * kUPW;              // transfers per wave and stage
-constexpr int kSlot = kUnits * kUnit;
-static_assert(kUnits % kNW == 0, "units split evenly over waves");
+
+// Tile shapes: four waves, each 128 channels (4 fragments of 32) by FM
+// fragments of 32 tokens; two workgroups per compute unit.
+template <int FM_>
+struct F6Tile {
+    static constexpr int WN = 1, WM = 4, FN = 4, FM = FM_;
+    static constexpr int NW = WN * WM, NT = NW * 64;
+    static constexpr int BN = WN * FN * 32, BM = WM * FM * 32;
+    static constexpr int WUnits = BN / 32, XUnits = BM / 32, Units = WUnits + XUnits;
+    static constexpr int UPW = Units / NW;   // units per wave and stage
+    static constexpr int VPW = 2 * UPW;      // transfers per wave and stage
+    static constexpr int Slot = Units * kUnit;
+    static_assert(Units % NW == 0, "units split evenly over waves");
+};
+using F6Tile256 = F6Tile<2>;   // 128 channels x 256 tokens
+using F6Tile128 = F6Tile<1>;   // 128 channels x 128 tokens: twice the tiles, for small token counts
+
+// global -> LDS transfers of 16 and 4 bytes per lane (plain functions, so that
+// the builtin's operands never depend on a template parameter, which the
+// host compilation pass does not accept)
+__device__ __forceinline__ void dma_lds16(const uint8_t *src, uint8_t *dst) {
+    __builtin_amdgcn_global_load_lds(src, (CLQ_LDS void *)dst, 16, 0, 0);
+}
+__device__ __forceinline__ void dma_lds4(const uint8_t *src, uint8_t *dst) {
+    __builtin_amdgcn_global_load_lds(src, (CLQ_LDS void *)dst, 4, 0, 0);
+}
 
 struct F6Args {
     const uint8_t *Xq;
@@ -113,10 +131,12 @@ struct Seg {
     int j, L, k;
 };
 
-template <bool I32OUT, bool RAGGED, bool BIAS>
-__global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
+template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+__global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
 {
     constexpr int NS = kNS;
+    constexpr int kFN = C::FN, kFM = C::FM, kNW = C::NW, kBN = C::BN, kBM = C::BM;
+    constexpr int kWUnits = C::WUnits, kXUnits = C::XUnits, kUPW = C::UPW, kVPW = C::VPW, kSlot = C::Slot;
     constexpr bool BIAS_CH = BIAS && !RAGGED && !I32OUT;
     constexpr int XS_CH = kBM / 64, WS_CH = kBN / 64, B_CH = kBN / 128;
     constexpr int E_CH = I32OUT ? 0 : XS_CH + WS_CH + (BIAS_CH ? B_CH : 0);
@@ -167,7 +187,7 @@ __global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
     Seg pc{-1, 0, 0};
     next_seg(pc);
     int p_s = 0;
-    const uint8_t *usrc[kUPW];
+    const uint8_t *usrc[C::UPW];
     const uint8_t *esrc[EPW > 0 ? EPW : 1];
     int edst[EPW > 0 ? EPW : 1];
     auto p_setup = [&]() {
@@ -213,7 +233,7 @@ __global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
             uint8_t *ed = &ebuf[pc.j % NS][0];
 #pragma unroll
             for (int j = 0; j < EPW; ++j)
-                __builtin_amdgcn_global_load_lds(esrc[j], (CLQ_LDS void *)(ed + edst[j]), 4, 0, 0);
+                dma_lds4(esrc[j], ed + edst[j]);
             e_now = 1;
             e_next = -1;
         }
@@ -222,13 +242,12 @@ __global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
         const uint32_t voff = (uint32_t)(pc.k * kUnit + lane * 16);
 #pragma unroll
         for (int j = 0; j < kUPW; ++j)
-            __builtin_amdgcn_global_load_lds(usrc[j] + voff, (CLQ_LDS void *)(dst + (wave * kUPW + j) * kUnit), 16, 0, 0);
+            dma_lds16(usrc[j] + voff, dst + (wave * kUPW + j) * kUnit);
         // the units' last 512 bytes: 16 bytes on each of lanes 0..31
         if (lane < 32) {
 #pragma unroll
             for (int j = 0; j < kUPW; ++j)
-                __builtin_amdgcn_global_load_lds(usrc[j] + voff + 1024,
-                                                 (CLQ_LDS void *)(dst + (wave * kUPW + j) * kUnit + 1024), 16, 0, 0);
+                dma_lds16(usrc[j] + voff + 1024, dst + (wave * kUPW + j) * kUnit + 1024);
         }
         if (p_s < total - 1) {
             ++p_s;
@@ -268,10 +287,15 @@ __global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
         });
     };
     auto stage_ready = [&]() {
-        static_assert(kFN == 4 && kFM == 2, "operand list below");
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]), "+v"(rb[1]),
-                       "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]), "+v"(sb[1]));
+        static_assert(kFN == 4 && (kFM == 1 || kFM == 2), "operand lists below");
+        if constexpr (kFM == 2)
+            asm volatile("s_waitcnt lgkmcnt(0)"
+                         : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]), "+v"(rb[1]),
+                           "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]), "+v"(sb[1]));
+        else
+            asm volatile("s_waitcnt lgkmcnt(0)"
+                         : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]),
+                           "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]));
     };
     auto take_operands = [&]() {
 #pragma unroll
@@ -312,9 +336,11 @@ __global__ void __launch_bounds__(kNT, 2) f6_gemm_kernel(F6Args a)
         float xsm[kFM];
         int mrow[kFM];
         if constexpr (!I32OUT) {
-            static_assert(kFM == 2, "two token scales per lane");
-            asm volatile("ds_read_b32 %0, %2\n\tds_read_b32 %1, %2 offset:128\n\ts_waitcnt lgkmcnt(0)"
-                         : "=&v"(xsm[0]), "=&v"(xsm[1]) : "v"(axs));
+            if constexpr (kFM == 2)
+                asm volatile("ds_read_b32 %0, %2\n\tds_read_b32 %1, %2 offset:128\n\ts_waitcnt lgkmcnt(0)"
+                             : "=&v"(xsm[0]), "=&v"(xsm[1]) : "v"(axs));
+            else
+                asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=&v"(xsm[0]) : "v"(axs));
         }
 #pragma unroll
         for (int fm = 0; fm < kFM; ++fm) mrow[fm] = tm * kBM + (wm * kFM + fm) * 32 + (lane & 31);
@@ -499,6 +525,38 @@ hipError_t launch_repack_f6(const uint8_t *in, int64_t units, uint8_t *out, hipS
     return hipGetLastError();
 }
 
+namespace {
+
+template <class C>
+hipError_t launch_gemm_f6_tile(F6Args g, bool i32out, bool ragged, hipStream_t stream) {
+    g.tiles_m = (g.M + C::BM - 1) / C::BM;
+    g.tiles_n = (g.N + C::BN - 1) / C::BN;
+    const int ntiles = g.tiles_m * g.tiles_n;
+    const int full = (f6_device_cus() * 2 + 7) / 8 * 8;
+    const int grid = std::max(8, (std::min(ntiles, full) + 7) / 8 * 8);
+    const dim3 gd((unsigned)grid), bd(C::NT);
+    if (i32out) {
+        if (ragged) hipLaunchKernelGGL((f6_gemm_kernel<C, true, true, false>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_kernel<C, true, false, false>), gd, bd, 0, stream, g);
+    } else if (ragged) {
+        if (g.bias) hipLaunchKernelGGL((f6_gemm_kernel<C, false, true, true>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_kernel<C, false, true, false>), gd, bd, 0, stream, g);
+    } else {
+        if (g.bias) hipLaunchKernelGGL((f6_gemm_kernel<C, false, false, true>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_kernel<C, false, false, false>), gd, bd, 0, stream, g);
+    }
+    return hipGetLastError();
+}
+
+// 128-token tiles while the 256-token ones would not give every compute
+// unit a tile (small token counts: twice the tiles, the same k loop)
+int f6_tile_tokens(int64_t M, int64_t N) {
+    const int64_t t256 = (M + 255) / 256 * ((N + 127) / 128);
+    return t256 <= f6_device_cus() ? 128 : 256;
+}
+
+}  // namespace
+
 hipError_t launch_gemm_f6(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
                           const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy, bool i32out,
                           hipStream_t stream) {
@@ -513,24 +571,9 @@ hipError_t launch_gemm_f6(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
     g.M = (int)M;
     g.N = (int)N;
     g.K = K;
-    g.tiles_m = (int)((M + kBM - 1) / kBM);
-    g.tiles_n = (int)((N + kBN - 1) / kBN);
-    const int ntiles = g.tiles_m * g.tiles_n;
-    const int full = (f6_device_cus() * 2 + 7) / 8 * 8;
-    const int grid = std::max(8, (std::min(ntiles, full) + 7) / 8 * 8);
     const bool ragged = N % 16 != 0 || (bias && reinterpret_cast<uintptr_t>(bias) % 4 != 0);
-    const dim3 gd((unsigned)grid), bd(kNT);
-    if (i32out) {
-        if (ragged) hipLaunchKernelGGL((f6_gemm_kernel<true, true, false>), gd, bd, 0, stream, g);
-        else hipLaunchKernelGGL((f6_gemm_kernel<true, false, false>), gd, bd, 0, stream, g);
-    } else if (ragged) {
-        if (bias) hipLaunchKernelGGL((f6_gemm_kernel<false, true, true>), gd, bd, 0, stream, g);
-        else hipLaunchKernelGGL((f6_gemm_kernel<false, true, false>), gd, bd, 0, stream, g);
-    } else {
-        if (bias) hipLaunchKernelGGL((f6_gemm_kernel<false, false, true>), gd, bd, 0, stream, g);
-        else hipLaunchKernelGGL((f6_gemm_kernel<false, false, false>), gd, bd, 0, stream, g);
-    }
-    return hipGetLastError();
+    if (f6_tile_tokens(M, N) == 128) return launch_gemm_f6_tile<F6Tile128>(g, i32out, ragged, stream);
+    return launch_gemm_f6_tile<F6Tile256>(g, i32out, ragged, stream);
 }
 
 }  // namespace clq

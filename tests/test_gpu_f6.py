@@ -161,12 +161,16 @@ def test_f6_linear_row_stride_and_zero_rows(clq):
     assert oracle.err_metric(Y[:16, :N].astype(np.float64), r["y64"], r["p64"], b) <= TOL
 
 
-def test_f6_matches_int4_fp16_output(clq):
+# 256-token tiles (the first shape) and 128-token tiles (fewer 256-token
+# tiles than compute units), against the int4 persistent and two-halves
+# kernels
+@pytest.mark.parametrize("M,N,K", [(4096, 3456, 1152), (1024, 3456, 1152), (1000, 1152, 4608)])
+def test_f6_matches_int4_fp16_output(clq, M, N, K):
     # the same sums and the same epilogue arithmetic: the int4 path's sums
     # are 256 times the fp6 path's, exact in fp32 below 2^24 codes' worth,
     # and its scale is x_scale / 256, so every product is the same real
     # number rounded once: equal outputs
-    M, N, K, block = 4096, 3456, 1152, 64
+    block = 64
     X = workloads.activations(M, K, "L1", seed=21)
     W = workloads.weights(N, K, seed=22)
     b = workloads.bias(N, seed=23)
