@@ -460,13 +460,18 @@ clq_status clq_clps_search(const void *X, int64_t ldx, const void *W, const floa
  *                               fall back to automatic when K < 256).  Every
  *                               choice gives the same results; for measuring
  *                               the schedule heuristics.
+ *   CLQ_DEBUG_F6_SCHEDULE       the fp6 GEMM's kernel choice: 0 automatic
+ *                               (default); 1 the persistent kernel; 2 the
+ *                               two-halves kernel on 128-token tiles; 3 on
+ *                               64-token tiles.  Same results either way.
  * clq_debug_set returns CLQ_ERR_ARG for an unknown knob or a value out of
  * range; clq_debug_get returns the current value, or -1 for an unknown knob. */
 typedef enum {
     CLQ_DEBUG_SYNC = 0,
     CLQ_DEBUG_SPLIT_SPIN_LIMIT = 1,
     CLQ_DEBUG_SPLIT_DROP_SIGNAL = 2,
-    CLQ_DEBUG_GEMM_SCHEDULE = 3
+    CLQ_DEBUG_GEMM_SCHEDULE = 3,
+    CLQ_DEBUG_F6_SCHEDULE = 4
 } clq_debug_knob;
 
 clq_status clq_debug_set(int32_t knob, int64_t value);

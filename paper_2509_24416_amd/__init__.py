@@ -125,7 +125,7 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_f6_from_int4", "clq_diag_mfma_probe_f6")
 
 CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
-CLQ_DEBUG_GEMM_SCHEDULE = 3
+CLQ_DEBUG_GEMM_SCHEDULE, CLQ_DEBUG_F6_SCHEDULE = 3, 4
 
 OBS_METRICS = ("absmax", "range", "par", "topk_mean", "percentile")
 

@@ -202,6 +202,10 @@ clq_status clq_debug_set(int32_t knob, int64_t value) {
             if (value < 0 || value > 4) return CLQ_ERR_ARG;
             __atomic_store_n(&clq::gemm_force_schedule, (int)value, __ATOMIC_RELAXED);
             return CLQ_OK;
+        case CLQ_DEBUG_F6_SCHEDULE:
+            if (value < 0 || value > 3) return CLQ_ERR_ARG;
+            __atomic_store_n(&clq::f6_schedule_force, (int)value, __ATOMIC_RELAXED);
+            return CLQ_OK;
     }
     return CLQ_ERR_ARG;
 }
@@ -212,6 +216,7 @@ int64_t clq_debug_get(int32_t knob) {
         case CLQ_DEBUG_SPLIT_SPIN_LIMIT: return __atomic_load_n(&clq::gemm_spin_limit, __ATOMIC_RELAXED);
         case CLQ_DEBUG_SPLIT_DROP_SIGNAL: return __atomic_load_n(&clq::gemm_drop_signal, __ATOMIC_RELAXED);
         case CLQ_DEBUG_GEMM_SCHEDULE: return __atomic_load_n(&clq::gemm_force_schedule, __ATOMIC_RELAXED);
+        case CLQ_DEBUG_F6_SCHEDULE: return __atomic_load_n(&clq::f6_schedule_force, __ATOMIC_RELAXED);
     }
     return -1;
 }

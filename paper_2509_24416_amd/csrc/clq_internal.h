@@ -138,6 +138,8 @@ hipError_t launch_mfma_probe_f6(const void *ops, int iters, int *sink, int grid,
 extern int gemm_spin_limit;
 extern int gemm_drop_signal;
 extern int gemm_force_schedule;   // 0 automatic, 1..4 a forced GEMM kernel choice (debug knob)
+extern int f6_schedule_force;     // 0 automatic, 1..3 a forced fp6 GEMM kernel choice (debug knob)
+int f6_schedule(int64_t M, int64_t N, int K);   // the fp6 GEMM kernel a shape gets: 1, 2 or 3
 
 // The W4A4 GEMM's schedule for a shape.  kernel: 0 the persistent kernel
 // (256-token tiles), 1 / 2 the two-halves kernel with 128- / 64-token tiles;

@@ -28,7 +28,9 @@
 // 64 codes, no operand widening, and a 4-slot ring: the slot of stage s is
 // refilled with stage s + 4 in iteration s, its contents having been read
 // into registers in iteration s - 1 (the workgroup barrier of iteration s
-// orders those reads before the transfer).  Whole tiles only.
+// orders those reads before the transfer).  Whole tiles only: 128 channels by
+// 256 tokens, or by 128 tokens where the larger tiles would leave compute
+// units without a tile.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -90,8 +92,9 @@ constexpr int kUnit = kF6Unit;  // bytes of a 32 x 64 fp6 unit
 constexpr int kNS = 4;          // ring slots
 constexpr int kGroupM = 8;      // token panels per tile group (L2 reuse of channel panels)
 
-// Tile shapes: four waves, each 128 channels (4 fragments of 32) by FM
-// fragments of 32 tokens; two workgroups per compute unit.
+// Tile shape of the persistent kernel: four waves, each 128 channels (4
+// fragments of 32) by FM fragments of 32 tokens; two workgroups per compute
+// unit.
 template <int FM_>
 struct F6Tile {
     static constexpr int WN = 1, WM = 4, FN = 4, FM = FM_;
@@ -104,7 +107,6 @@ struct F6Tile {
     static_assert(Units % NW == 0, "units split evenly over waves");
 };
 using F6Tile256 = F6Tile<2>;   // 128 channels x 256 tokens
-using F6Tile128 = F6Tile<1>;   // 128 channels x 128 tokens: twice the tiles, for small token counts
 
 // global -> LDS transfers of 16 and 4 bytes per lane (plain functions, so that
 // the builtin's operands never depend on a template parameter, which the
@@ -114,6 +116,17 @@ __device__ __forceinline__ void dma_lds16(const uint8_t *src, uint8_t *dst) {
 }
 __device__ __forceinline__ void dma_lds4(const uint8_t *src, uint8_t *dst) {
     __builtin_amdgcn_global_load_lds(src, (CLQ_LDS void *)dst, 4, 0, 0);
+}
+
+// waits for all but N outstanding transfers (and the LDS reads), then the
+// workgroup barrier
+template <int N>
+__device__ __forceinline__ void wait_landed_barrier() {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
 struct F6Args {
@@ -490,6 +503,297 @@ __global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// ---- few tiles with long k loops: the k loop in two halves ---------------------
+// The two-halves scheme of the int4 GEMM on fp6 operands.  Each tile (128
+// channels x BM tokens) gets two halves of NWH waves: half 0 runs the first
+// half of the k-stages and half 1 the rest, each through its own NS-slot LDS
+// ring (the fp6 kernel's ring protocol), in lockstep on the workgroup
+// barrier; a second half one stage shorter idles on its last step.  At the
+// end the halves swap their fp32 sums (exact integers, so exact sums) through
+// the idle rings and each finishes two of the four channel fragments with
+// the epilogue arithmetic of the kernel above.  One tile per workgroup, two
+// workgroups per compute unit.
+template <int NWH_, int NS_>
+struct F6HalfTile {
+    static constexpr int NWH = NWH_, NS = NS_, FN = 4, FM = 2;
+    static constexpr int NT = 2 * NWH * 64;
+    static constexpr int BN = FN * 32, BM = NWH * FM * 32;
+    static constexpr int WUnits = BN / 32, XUnits = BM / 32, Units = WUnits + XUnits;
+    static constexpr int UPW = Units / NWH;   // units per wave and stage, within a half
+    static constexpr int VPW = 2 * UPW;       // transfers per wave and stage
+    static constexpr int Slot = Units * kUnit;
+    static constexpr int Exch = NWH * 16384;  // one half's outgoing sums: 2 fragments x 2 x 16 floats x 64 lanes per wave
+    static constexpr int Pool = 2 * NS * Slot > 2 * Exch ? 2 * NS * Slot : 2 * Exch;
+    static_assert(Units % NWH == 0, "units split evenly over a half's waves");
+};
+using F6Half128 = F6HalfTile<2, 3>;   // 128 x 128 tiles, 72 KB of rings
+using F6Half64 = F6HalfTile<1, 4>;    // 128 x 64 tiles, 72 KB of rings
+
+// the mixed fma of fma_mix2 with fp32 bias operands (each exactly an fp16 value)
+__device__ __forceinline__ uint32_t fma_mix2f(float p0, float w0, float b0, float p1, float w1, float b1) {
+    uint32_t r;
+    asm("v_fma_mixlo_f16 %0, %1, %2, %3\n\t"
+        "v_fma_mixhi_f16 %0, %4, %5, %6"
+        : "=&v"(r)
+        : "v"(p0), "v"(w0), "v"(b0), "v"(p1), "v"(w1), "v"(b1));
+    return r;
+}
+
+template <class C, bool I32OUT, bool RAGGED, bool BIAS>
+__global__ void __launch_bounds__(C::NT, C::NWH == 1 ? 1 : 2) f6_gemm_halves_kernel(F6Args a)
+{
+    static_assert(!(I32OUT && BIAS), "no bias on the integer output");
+    constexpr int NS = C::NS, kFN = C::FN, kFM = C::FM, kUPW = C::UPW, kVPW = C::VPW, kSlot = C::Slot;
+    __shared__ __align__(16) uint8_t pool[C::Pool];
+    // the tile's epilogue operands, staged after the k loop as floats:
+    // channel scales, biases (fp16 widened, exact), token scales
+    constexpr int EPN = 2 * C::BN + C::BM;
+    __shared__ float ep[EPN];
+    const float *ep_ws = ep, *ep_b = ep + C::BN, *ep_xs = ep + 2 * C::BN;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w8 = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = w8 / C::NWH, wm = w8 % C::NWH;
+    const int M = a.M, N = a.N, nks = a.K >> 6;
+    // one tile per workgroup: workgroups are dealt to the 8 XCDs
+    // round-robin, and each XCD takes a contiguous run of the grouped order
+    int L;
+    {
+        const int G = gridDim.x, x = blockIdx.x & 7, j = blockIdx.x >> 3;
+        const int per = G >> 3, rem = G & 7;
+        L = x * per + min(x, rem) + j;
+    }
+    int tm, tn;
+    {
+        const int gsz = kGroupM * a.tiles_n;
+        const int g = L / gsz, r = L - g * gsz;
+        const int m0 = g * kGroupM;
+        const int gm = min(a.tiles_m - m0, kGroupM);
+        tn = r / gm;
+        tm = m0 + (r - tn * gm);
+    }
+    const int h0 = (nks + 1) >> 1;
+    const int kb = half ? h0 : 0, len = half ? nks - h0 : h0;   // len >= 1 (nks >= 2)
+    const int wunits_total = (int)(padded_rows(N) >> 5);
+    const int xunits_total = (int)(padded_act_rows(M) >> 5);
+    uint8_t *ring = pool + half * NS * kSlot;
+    const uint8_t *usrc[C::UPW];
+#pragma unroll
+    for (int j = 0; j < kUPW; ++j) {
+        const int u = wm * kUPW + j;
+        if (u < C::WUnits) {
+            const int ug = min(tn * C::WUnits + u, wunits_total - 1);
+            usrc[j] = a.Wq + ((int64_t)ug * nks + kb) * kUnit;
+        } else {
+            const int ux = min(tm * C::XUnits + (u - C::WUnits), xunits_total - 1);
+            usrc[j] = a.Xq + ((int64_t)ux * nks + kb) * kUnit;
+        }
+    }
+    // stage k of this half into slot q; past the end the last stage is
+    // loaded again (into a slot whose contents are never read), so every wave
+    // issues the same transfers and the wait counts stay fixed
+    auto produce = [&](int q, int k) {
+        const uint32_t voff = (uint32_t)(min(k, len - 1) * kUnit + lane * 16);
+        uint8_t *dst = ring + q * kSlot;
+#pragma unroll
+        for (int j = 0; j < kUPW; ++j) dma_lds16(usrc[j] + voff, dst + (wm * kUPW + j) * kUnit);
+        if (lane < 32) {
+#pragma unroll
+            for (int j = 0; j < kUPW; ++j) dma_lds16(usrc[j] + voff + 1024, dst + (wm * kUPW + j) * kUnit + 1024);
+        }
+    };
+    v4u ra[kFN], rb[kFM];
+    v2u sa[kFN], sb[kFM];
+    v8i opa[kFN], opb[kFM];
+    const uint32_t wl0 = (uint32_t)(lane * 16), wl1 = (uint32_t)f6_tail_offset(lane);
+    const uint32_t xo = (uint32_t)((C::WUnits + wm * kFM) * kUnit);
+    auto read_stage = [&](int q) {
+        uint32_t b16 = wl0, b8 = wl1;
+        asm volatile("" : "+v"(b16), "+v"(b8));
+        const uint32_t base = lds_addr(ring + q * kSlot);
+        b16 += base;
+        b8 += base;
+        const uint32_t bx16 = b16 + xo, bx8 = b8 + xo;
+        static_for<0, kFN>([&](auto f) {
+            constexpr int o = decltype(f)::value * kUnit;
+            ra[f] = lds_read16<o>(b16);
+            sa[f] = lds_read8<o>(b8);
+        });
+        static_for<0, kFM>([&](auto f) {
+            constexpr int o = decltype(f)::value * kUnit;
+            rb[f] = lds_read16<o>(bx16);
+            sb[f] = lds_read8<o>(bx8);
+        });
+    };
+    auto stage_ready = [&]() {
+        static_assert(kFN == 4 && kFM == 2, "operand list below");
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]), "+v"(rb[1]),
+                       "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]), "+v"(sb[1]));
+    };
+    auto take_operands = [&]() {
+#pragma unroll
+        for (int f = 0; f < kFN; ++f)
+            opa[f] = v8i{(int)ra[f][0], (int)ra[f][1], (int)ra[f][2], (int)ra[f][3], (int)sa[f][0], (int)sa[f][1], 0, 0};
+#pragma unroll
+        for (int f = 0; f < kFM; ++f)
+            opb[f] = v8i{(int)rb[f][0], (int)rb[f][1], (int)rb[f][2], (int)rb[f][3], (int)sb[f][0], (int)sb[f][1], 0, 0};
+    };
+    v16f acc[kFN][kFM];
+#pragma unroll
+    for (int fn = 0; fn < kFN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < kFM; ++fm) acc[fn][fm] = v16f{};
+    auto mma = [&]() {
+#pragma unroll
+        for (int fn = 0; fn < kFN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < kFM; ++fm)
+                acc[fn][fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opa[fn], opb[fm], acc[fn][fm], 2, 2, 0, 0, 0, 0);
+    };
+
+    // epilogue operands: loaded first (EPR per thread at clamped indices,
+    // ahead of the transfers), held in registers through the k loop and
+    // written to LDS after it, when no transfer into LDS is in flight
+    constexpr int EPR = (EPN + C::NT - 1) / C::NT;
+    float epv[EPR];
+    _Float16 epb[EPR];
+#pragma unroll
+    for (int r = 0; r < EPR; ++r) {
+        const int e = min(tid + r * C::NT, EPN - 1);
+        const int ec = e & (C::BN - 1), er = max(e - 2 * C::BN, 0);
+        const float *esrc = e < 2 * C::BN ? a.ws + min(tn * C::BN + ec, N - 1) : a.xs + min(tm * C::BM + er, M - 1);
+        epv[r] = I32OUT ? 0.0f : *esrc;
+        epb[r] = (_Float16)0.0f;
+        if constexpr (BIAS) epb[r] = reinterpret_cast<const _Float16 *>(a.bias)[min(tn * C::BN + ec, N - 1)];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // stage s+1 has landed once at most the NS - 2 later productions are
+    // outstanding (completion is in issue order)
+    // prologue: stages 0..NS-1 in flight, stage 0 read into registers
+    for (int q = 0; q < NS; ++q) produce(q, q);
+    wait_vm_barrier<(NS - 1) * kVPW>();
+    read_stage(0);
+    stage_ready();
+    // both halves take h0 steps
+    int q = 0;
+    for (int s = 0; s < h0; ++s) {
+        const int nq = q + 1 == NS ? 0 : q + 1;
+        const bool active = s < len;
+        take_operands();
+        wait_landed_barrier<(NS - 2) * kVPW>();
+        read_stage(nq);
+        produce(q, s + NS);
+        __builtin_amdgcn_sched_barrier(0);
+        if (active) mma();
+        __builtin_amdgcn_sched_barrier(0);
+        stage_ready();
+        q = nq;
+    }
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+    // the epilogue operands into LDS (a thread past the end writes the last
+    // value again); the barrier after the sends below publishes them
+#pragma unroll
+    for (int r = 0; r < EPR; ++r) {
+        const int e = min(tid + r * C::NT, EPN - 1);
+        ep[e] = e >= C::BN && e < 2 * C::BN ? (float)epb[r] : epv[r];
+    }
+
+    // the halves swap sums through the idle rings: half 0 finishes channel
+    // fragments 0-1 and half 1 fragments 2-3, each adding the other's
+    auto send = [&](auto f0c) {
+        constexpr int f0 = decltype(f0c)::value;
+        v4f *out = reinterpret_cast<v4f *>(pool + half * C::Exch + wm * 16384);
+        static_for<0, 2>([&](auto fc) {
+            constexpr int fn = f0 + decltype(fc)::value;
+#pragma unroll
+            for (int fm = 0; fm < kFM; ++fm)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const v16f &x = acc[fn][fm];
+                    out[((decltype(fc)::value * kFM + fm) * 4 + q4) * 64 + lane] =
+                        v4f{x[4 * q4], x[4 * q4 + 1], x[4 * q4 + 2], x[4 * q4 + 3]};
+                }
+        });
+    };
+    auto receive = [&](auto f0c) {
+        constexpr int f0 = decltype(f0c)::value;
+        const v4f *in = reinterpret_cast<const v4f *>(pool + (1 - half) * C::Exch + wm * 16384);
+        static_for<0, 2>([&](auto fc) {
+            constexpr int fn = f0 + decltype(fc)::value;
+#pragma unroll
+            for (int fm = 0; fm < kFM; ++fm)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const v4f y = in[((decltype(fc)::value * kFM + fm) * 4 + q4) * 64 + lane];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[fn][fm][4 * q4 + e] += y[e];
+                }
+        });
+    };
+    if (half == 0) send(IC<2>{});
+    else send(IC<0>{});
+    __syncthreads();
+    if (half == 0) receive(IC<0>{});
+    else receive(IC<2>{});
+
+    // epilogue: lane owns token m and 16 consecutive channels; each half
+    // its two channel fragments
+    const int h16 = (lane >> 5) * 16;
+    auto epilogue = [&](auto f0c) {
+        static_for<0, 2>([&](auto fc) {
+            constexpr int fn = decltype(f0c)::value + decltype(fc)::value;
+            const int c0 = fn * 32 + h16, n0 = tn * C::BN + c0;
+            float wsv[16], bw[16];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                wsv[v] = ep_ws[c0 + v];
+                bw[v] = BIAS ? ep_b[c0 + v] : 0.0f;
+            }
+#pragma unroll
+            for (int fm = 0; fm < kFM; ++fm) {
+                const int r0 = (wm * kFM + fm) * 32 + (lane & 31), m = tm * C::BM + r0;
+                const v16f &x = acc[fn][fm];
+                if constexpr (I32OUT) {   // the exact integer sums
+                    int32_t *dst = reinterpret_cast<int32_t *>(a.Y) + (int64_t)m * a.ldy + n0;
+                    if (m < M && n0 < N) {
+                        if (!RAGGED || n0 + 16 <= N) {
+#pragma unroll
+                            for (int q4 = 0; q4 < 4; ++q4)
+                                reinterpret_cast<v4i *>(dst)[q4] =
+                                    v4i{(int)x[4 * q4], (int)x[4 * q4 + 1], (int)x[4 * q4 + 2], (int)x[4 * q4 + 3]};
+                        } else {
+#pragma unroll
+                            for (int v = 0; v < 16; ++v)
+                                if (n0 + v < N) dst[v] = (int)x[v];
+                        }
+                    }
+                    continue;
+                }
+                uint32_t hv[8];
+                const float xsc = ep_xs[r0];
+#pragma unroll
+                for (int v = 0; v < 16; v += 2)
+                    hv[v / 2] = fma_mix2f(x[v] * xsc, wsv[v], bw[v], x[v + 1] * xsc, wsv[v + 1], bw[v + 1]);
+                uint16_t *dst = reinterpret_cast<uint16_t *>(a.Y) + (int64_t)m * a.ldy + n0;
+                if (m < M && n0 < N) {
+                    if (!RAGGED || n0 + 16 <= N) {
+                        reinterpret_cast<v4u *>(dst)[0] = v4u{hv[0], hv[1], hv[2], hv[3]};
+                        reinterpret_cast<v4u *>(dst)[1] = v4u{hv[4], hv[5], hv[6], hv[7]};
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 16; ++v)
+                            if (n0 + v < N) dst[v] = (uint16_t)(hv[v >> 1] >> (16 * (v & 1)));
+                    }
+                }
+            }
+        });
+    };
+    if (half == 0) epilogue(IC<0>{});
+    else epilogue(IC<2>{});
+}
+
 // ---- format conversion: packed int4 units -> fp6 units ---------------------------
 // One thread per lane slot: its 16 bytes (32 nibbles) become its six fp6
 // dwords (the code order of f6_codes.h).
@@ -548,14 +852,44 @@ hipError_t launch_gemm_f6_tile(F6Args g, bool i32out, bool ragged, hipStream_t s
     return hipGetLastError();
 }
 
-// 128-token tiles while the 256-token ones would not give every compute
-// unit a tile (small token counts: twice the tiles, the same k loop)
-int f6_tile_tokens(int64_t M, int64_t N) {
-    const int64_t t256 = (M + 255) / 256 * ((N + 127) / 128);
-    return t256 <= f6_device_cus() ? 128 : 256;
+template <class C>
+hipError_t launch_gemm_f6_halves(F6Args g, bool i32out, bool ragged, hipStream_t stream) {
+    g.tiles_m = (g.M + C::BM - 1) / C::BM;
+    g.tiles_n = (g.N + C::BN - 1) / C::BN;
+    const dim3 gd((unsigned)(g.tiles_m * g.tiles_n)), bd(C::NT);   // one tile per workgroup
+    if (i32out) {
+        if (ragged) hipLaunchKernelGGL((f6_gemm_halves_kernel<C, true, true, false>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_halves_kernel<C, true, false, false>), gd, bd, 0, stream, g);
+    } else if (ragged) {
+        if (g.bias) hipLaunchKernelGGL((f6_gemm_halves_kernel<C, false, true, true>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_halves_kernel<C, false, true, false>), gd, bd, 0, stream, g);
+    } else {
+        if (g.bias) hipLaunchKernelGGL((f6_gemm_halves_kernel<C, false, false, true>), gd, bd, 0, stream, g);
+        else hipLaunchKernelGGL((f6_gemm_halves_kernel<C, false, false, false>), gd, bd, 0, stream, g);
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
+
+int f6_schedule_force = 0;
+
+// The fp6 GEMM schedule for an M x N x K product: 1 the persistent kernel,
+// 2 the two-halves kernel on 128-token tiles, 3 on 64-token tiles.  Long k
+// loops (K >= 2048, unless the layer is four times wider than deep) take the
+// two halves; so do shorter ones while the 256-token tiles would not give
+// every compute unit a tile; 64-token tiles while the 128-token ones would
+// fill at most half the compute units.
+int f6_schedule(int64_t M, int64_t N, int K) {
+    const int force = __atomic_load_n(&f6_schedule_force, __ATOMIC_RELAXED);
+    if (force >= 1 && force <= 3) return force;
+    const int cus = f6_device_cus();
+    const int64_t tn = (N + 127) / 128;
+    const int64_t t256 = (M + 255) / 256 * tn, t128 = (M + 127) / 128 * tn;
+    const bool halves = (K >= 2048 && N < 4 * (int64_t)K) || t256 <= cus;
+    if (!halves) return 1;
+    return K >= 2048 && 2 * t128 <= cus ? 3 : 2;
+}
 
 hipError_t launch_gemm_f6(const uint8_t *Xq, const float *xs, const uint8_t *Wq, const float *ws,
                           const uint16_t *bias, int64_t M, int64_t N, int K, void *Y, int64_t ldy, bool i32out,
@@ -572,8 +906,11 @@ hipError_t launch_gemm_f6(const uint8_t *Xq, const float *xs, const uint8_t *Wq,
     g.N = (int)N;
     g.K = K;
     const bool ragged = N % 16 != 0 || (bias && reinterpret_cast<uintptr_t>(bias) % 4 != 0);
-    if (f6_tile_tokens(M, N) == 128) return launch_gemm_f6_tile<F6Tile128>(g, i32out, ragged, stream);
-    return launch_gemm_f6_tile<F6Tile256>(g, i32out, ragged, stream);
+    switch (f6_schedule(M, N, K)) {
+        case 2: return launch_gemm_f6_halves<F6Half128>(g, i32out, ragged, stream);
+        case 3: return launch_gemm_f6_halves<F6Half64>(g, i32out, ragged, stream);
+        default: return launch_gemm_f6_tile<F6Tile256>(g, i32out, ragged, stream);
+    }
 }
 
 }  // namespace clq

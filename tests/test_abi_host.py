@@ -317,6 +317,18 @@ def test_debug_knobs(lib):
     assert lib.clq_debug_get(SYNC) == 0
 
 
+def test_f6_schedule_knob(lib):
+    F6 = 4
+    assert lib.clq_debug_get(F6) == 0
+    assert lib.clq_debug_set(F6, -1) == ARG and lib.clq_debug_set(F6, 4) == ARG
+    try:
+        for v in (1, 2, 3):
+            assert lib.clq_debug_set(F6, v) == OK and lib.clq_debug_get(F6) == v
+    finally:
+        assert lib.clq_debug_set(F6, 0) == OK
+    assert lib.clq_debug_get(F6) == 0
+
+
 def test_schedule_knob(lib):
     SCHED = 3
     assert lib.clq_debug_get(SCHED) == 0

@@ -217,3 +217,37 @@ def test_f6_argument_errors(clq):
     Xq64, xs64 = clq.clq_rotate_quant_act_f6(X64, 64)
     with pytest.raises(clq.ClqError):
         clq.clq_w4a4_linear_f6(Xq64, xs64, qw64)      # K < 128
+
+
+# every fp6 GEMM schedule (the persistent kernel, the two-halves kernel on
+# 128- and 64-token tiles) on few and many tiles, ragged shapes and short and
+# long k loops: the same integer sums and the same fp16 bits
+F6_FORCED = [(1024, 1152, 1152), (300, 1000, 640), (1000, 1152, 4608), (4096, 3456, 1152), (8192, 1152, 4608),
+             (65, 200, 256), (2, 16, 128), (777, 3072, 3072)]
+
+
+@pytest.mark.parametrize("M,N,K", F6_FORCED)
+def test_f6_forced_schedules_agree(clq, M, N, K):
+    block = 64
+    X = workloads.activations(M, K, "L1", seed=M + 5)
+    W = workloads.weights(N, K, seed=N + 5)
+    b = workloads.bias(N, seed=N + 6)
+    qw = clq.clq_quantize_weights_f6(dev(W), block)
+    Xq, xs = clq.clq_rotate_quant_act_f6(dev(X), block)
+    rows = np.unique(np.r_[0:3, M // 2, M - 3:M].clip(0, M - 1))
+    r = oracle.linear(X[rows], W, b, block)
+    ref = None
+    try:
+        for force in (1, 2, 3):
+            clq.clq_debug_set(clq.CLQ_DEBUG_F6_SCHEDULE, force)
+            acc = host(clq.clq_w4a4_accum_f6(Xq, xs, qw))
+            Y = host(clq.clq_w4a4_linear_f6(Xq, xs, qw, dev(b)))
+            if ref is None:
+                ref, refY = acc, Y
+                assert np.array_equal(acc[rows], r["acc"])
+                assert oracle.err_metric(Y[rows].astype(np.float64), r["y64"], r["p64"], b) <= TOL
+            else:
+                assert np.array_equal(acc, ref), force
+                assert np.array_equal(Y.view(np.uint16), refY.view(np.uint16)), force
+    finally:
+        clq.clq_debug_set(clq.CLQ_DEBUG_F6_SCHEDULE, 0)
