@@ -928,7 +928,9 @@ def main():
                if (wbits, abits) == (4, 4) else None)
     plans = [clq.clq_w4a4_schedule(l.M, l.N, l.K) for l in layers] if (abits == 4 and codes == "int4") else None
     if codes == "fp6":
-        gemm_name = "f6_gemm_kernel (mean over the 4 linears)"
+        plans = [{"kernel": clq.clq_w4a4_schedule_f6(l.M, l.N, l.K)} for l in layers]
+        kinds = sorted({clq.F6_SCHEDULES[p["kernel"]].split(" (")[0] for p in plans})
+        gemm_name = " / ".join(kinds) + " (mean over the 4 linears)"
     elif abits == 4:
         kinds = sorted({("w4a4_gemm_kernel" if p["kernel"] == 0 else "w4a4_gemm_halves_kernel") for p in plans})
         gemm_name = " / ".join(kinds) + " (mean over the 4 linears)"

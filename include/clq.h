@@ -276,6 +276,12 @@ clq_status clq_w4a4_linear_f6(const void *Xq, const float *x_scale, const void *
                               int64_t N, int64_t K, void *Y, int64_t ldy,
                               hipStream_t stream);
 
+/* Diagnostic (host only, nothing enqueued): the kernel clq_w4a4_linear_f6
+ * picks for an M x N x K product on the current device: *choice = 1 the
+ * persistent grid of 256-token tiles, 2 / 3 two halves of the k loop per
+ * 128- / 64-token tile (the CLQ_DEBUG_F6_SCHEDULE knob included).  K >= 128. */
+clq_status clq_w4a4_schedule_f6(int64_t M, int64_t N, int64_t K, int32_t *choice);
+
 /* Diagnostic: the exact integer sums of the fp6 operands as int32 [M][N],
  * row stride ldacc (elements, a multiple of 4).  K >= 128. */
 clq_status clq_w4a4_accum_f6(const void *Xq, const void *Wq, int64_t M, int64_t N,

@@ -100,6 +100,7 @@ _lib.clq_w4a4_linear_f6.argtypes = [_p, _p, _p, _p, _p, _i64, _i64, _i64, _p, _i
 _lib.clq_w4a4_accum_f6.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _p]
 _lib.clq_unswizzle_f6.argtypes = [_p, _i64, _i64, _i32, _p, _p]
 _lib.clq_f6_from_int4.argtypes = [_p, _i64, _i64, _i32, _p, _p]
+_lib.clq_w4a4_schedule_f6.argtypes = [_i64, _i64, _i64, _p]
 for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_w4a4_accum_i32", "clq_unswizzle_weights", "clq_unswizzle_act",
            "clq_obs_channel_scores", "clq_obs_permutation", "clq_rotate_quant_act8",
@@ -108,7 +109,7 @@ for _f in ("clq_quantize_weights", "clq_rotate_quant_act", "clq_w4a4_linear",
            "clq_w4a4_schedule", "clq_w4a4_linear_noalloc", "clq_diag_mfma_probe",
            "clq_w4a4_rq_linear", "clq_w4a4_rq_schedule", "clq_quantize_weights_f6",
            "clq_rotate_quant_act_f6", "clq_w4a4_linear_f6", "clq_w4a4_accum_f6", "clq_unswizzle_f6",
-           "clq_f6_from_int4", "clq_diag_mfma_probe_f6"):
+           "clq_f6_from_int4", "clq_diag_mfma_probe_f6", "clq_w4a4_schedule_f6"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_bytes",
@@ -122,7 +123,7 @@ EXPORTS = ("clq_version", "clq_status_string", "clq_weight_bytes", "clq_act_byte
            "clq_diag_mfma_probe_bytes", "clq_diag_mfma_probe", "clq_w4a4_rq_linear",
            "clq_w4a4_rq_schedule", "clq_weight_bytes_f6", "clq_act_bytes_f6", "clq_quantize_weights_f6",
            "clq_rotate_quant_act_f6", "clq_w4a4_linear_f6", "clq_w4a4_accum_f6", "clq_unswizzle_f6",
-           "clq_f6_from_int4", "clq_diag_mfma_probe_f6")
+           "clq_f6_from_int4", "clq_diag_mfma_probe_f6", "clq_w4a4_schedule_f6")
 
 CLQ_DEBUG_SYNC, CLQ_DEBUG_SPLIT_SPIN_LIMIT, CLQ_DEBUG_SPLIT_DROP_SIGNAL = 0, 1, 2
 CLQ_DEBUG_GEMM_SCHEDULE, CLQ_DEBUG_F6_SCHEDULE = 3, 4
@@ -190,6 +191,18 @@ def clq_diag_mfma_probe_f6(ops, iters, grid, sink, stream=None):
     _check(_lib.clq_diag_mfma_probe_f6(_ptr(ops), ops.numel(), iters, grid, _ptr(sink), _stream(stream)),
            "clq_diag_mfma_probe_f6")
     return grid * iters * 64 * 2 * 32 * 32 * 64
+
+
+F6_SCHEDULES = {1: "f6_gemm_kernel", 2: "f6_gemm_halves_kernel (128-token tiles)",
+                3: "f6_gemm_halves_kernel (64-token tiles)"}
+
+
+def clq_w4a4_schedule_f6(M, N, K):
+    """The fp6 GEMM kernel choice for an M x N x K product: 1 persistent
+    (256-token tiles), 2 / 3 two halves of the k loop (128- / 64-token tiles)."""
+    c = ctypes.c_int32()
+    _check(_lib.clq_w4a4_schedule_f6(M, N, K, ctypes.byref(c)), "clq_w4a4_schedule_f6")
+    return c.value
 
 
 def clq_w4a4_schedule(M, N, K, with_workspace=True):

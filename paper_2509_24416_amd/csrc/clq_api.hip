@@ -164,6 +164,15 @@ clq_status clq_w4a4_schedule(int64_t M, int64_t N, int64_t K, int32_t with_works
     return CLQ_OK;
 }
 
+clq_status clq_w4a4_schedule_f6(int64_t M, int64_t N, int64_t K, int32_t *choice) {
+    if (!choice) return CLQ_ERR_NULL;
+    clq_status s;
+    if ((s = check_rows(M)) != CLQ_OK || (s = check_rows(N)) != CLQ_OK || (s = check_k(K)) != CLQ_OK) return s;
+    if (K < 128) return CLQ_ERR_SHAPE;
+    *choice = clq::f6_schedule(M, N, (int)K);
+    return CLQ_OK;
+}
+
 size_t clq_diag_mfma_probe_bytes(void) { return clq::mfma_probe_bytes(); }
 
 clq_status clq_diag_mfma_probe(const void *ops, size_t ops_bytes, int32_t iters, int32_t grid, int32_t *sink,

@@ -875,19 +875,21 @@ hipError_t launch_gemm_f6_halves(F6Args g, bool i32out, bool ragged, hipStream_t
 int f6_schedule_force = 0;
 
 // The fp6 GEMM schedule for an M x N x K product: 1 the persistent kernel,
-// 2 the two-halves kernel on 128-token tiles, 3 on 64-token tiles.  Long k
-// loops (K >= 2048, unless the layer is four times wider than deep) take the
-// two halves; so do shorter ones while the 256-token tiles would not give
-// every compute unit a tile; 64-token tiles while the 128-token ones would
-// fill at most half the compute units.
+// 2 the two-halves kernel on 128-token tiles, 3 on 64-token tiles.  The two
+// halves while the 256-token tiles would not give every compute unit a tile,
+// on 64-token tiles for long k loops (K >= 2048) whose 128-token tiles would
+// fill at most half the compute units.  With more tiles the persistent
+// kernel wins inside a block's chain of launches, long k loops included
+// (its operands then come from HBM, and the one-tile-per-workgroup halves
+// read them more often), although the halves win those shapes when timed
+// alone with their operands cache-resident.
 int f6_schedule(int64_t M, int64_t N, int K) {
     const int force = __atomic_load_n(&f6_schedule_force, __ATOMIC_RELAXED);
     if (force >= 1 && force <= 3) return force;
     const int cus = f6_device_cus();
     const int64_t tn = (N + 127) / 128;
     const int64_t t256 = (M + 255) / 256 * tn, t128 = (M + 127) / 128 * tn;
-    const bool halves = (K >= 2048 && N < 4 * (int64_t)K) || t256 <= cus;
-    if (!halves) return 1;
+    if (t256 > cus) return 1;
     return K >= 2048 && 2 * t128 <= cus ? 3 : 2;
 }
 

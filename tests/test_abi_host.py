@@ -83,12 +83,13 @@ def lib():
     L.clq_unswizzle_f6.argtypes = [p, i64, i64, i32, p, p]
     L.clq_f6_from_int4.argtypes = [p, i64, i64, i32, p, p]
     L.clq_diag_mfma_probe_f6.argtypes = [p, ctypes.c_size_t, i32, i32, p, p]
+    L.clq_w4a4_schedule_f6.argtypes = [i64, i64, i64, p]
     return L
 
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 42, names
+    assert len(names) == 43, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -315,6 +316,31 @@ def test_debug_knobs(lib):
         assert lib.clq_debug_set(DROP, 0) == OK
         assert lib.clq_debug_set(SYNC, 0) == OK
     assert lib.clq_debug_get(SYNC) == 0
+
+
+def f6_choice(lib, M, N, K):
+    c = ctypes.c_int32(-1)
+    assert lib.clq_w4a4_schedule_f6(M, N, K, ctypes.byref(c)) == OK
+    return c.value
+
+
+def test_f6_schedule_rule(lib):
+    # 256 compute units (the MI355X's count, and the fallback without a GPU)
+    assert f6_choice(lib, 1024, 3456, 1152) == 2     # 108 tiles of 256 tokens: two halves, 128-token tiles
+    assert f6_choice(lib, 1024, 1152, 4608) == 3     # long k, 72 tiles of 128 tokens: 64-token tiles
+    assert f6_choice(lib, 4096, 1152, 4608) == 2     # 144 tiles of 256 tokens
+    assert f6_choice(lib, 4096, 3456, 1152) == 1     # 432 tiles: the persistent kernel
+    assert f6_choice(lib, 43200, 1152, 4608) == 1    # long k, many tiles
+    assert f6_choice(lib, 43200, 3456, 1152) == 1
+    assert f6_choice(lib, 4608, 3072, 12288) == 1    # 432 tiles
+    c = ctypes.c_int32()
+    assert lib.clq_w4a4_schedule_f6(4096, 1152, 4608, None) == NULL
+    assert lib.clq_w4a4_schedule_f6(4096, 1152, 64, ctypes.byref(c)) == SHAPE
+    assert lib.clq_w4a4_schedule_f6(0, 1152, 1152, ctypes.byref(c)) == SHAPE
+    try:
+        assert lib.clq_debug_set(4, 3) == OK and f6_choice(lib, 43200, 3456, 1152) == 3
+    finally:
+        assert lib.clq_debug_set(4, 0) == OK
 
 
 def test_f6_schedule_knob(lib):
