@@ -144,6 +144,21 @@ struct Seg {
     int j, L, k;
 };
 
+// The LDS reads of one stage's operands have landed: one wait that names
+// every destination register, so that no use is scheduled before it.
+template <int FM>
+__device__ __forceinline__ void wait_operands(v4u (&ra)[4], v4u (&rb)[FM], v2u (&sa)[4], v2u (&sb)[FM]) {
+    static_assert(FM == 1 || FM == 2, "operand lists below");
+    if constexpr (FM == 2)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]), "+v"(rb[1]),
+                       "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]), "+v"(sb[1]));
+    else
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]),
+                       "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]));
+}
+
 template <class C, bool I32OUT, bool RAGGED, bool BIAS>
 __global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
 {
@@ -274,12 +289,17 @@ __global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
 
     // ---- consumer -------------------------------------------------------------
     // operands of one stage: 16 + 8 bytes of each of the wave's 4 channel and
-    // 2 token units
-    v4u ra[kFN], rb[kFM];
-    v2u sa[kFN], sb[kFM];
-    v8i opa[kFN], opb[kFM];
+    // 2 token units, in two register sets used by alternate stages (stage s
+    // in set s & 1), so that the next stage's reads land while the matrix
+    // instructions read the other set, with no copies between them.  The
+    // ragged-shape instances, whose epilogue needs more registers, read into
+    // set 1 and copy it to set 0 at the start of each iteration instead.
+    constexpr bool kAlt = !RAGGED;
+    v4u ra[2][kFN], rb[2][kFM];
+    v2u sa[2][kFN], sb[2][kFM];
     const uint32_t wl0 = (uint32_t)(lane * 16), wl1 = (uint32_t)f6_tail_offset(lane);
-    auto read_stage = [&](auto qc) {
+    auto read_stage = [&](auto qc, auto pc) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
         uint32_t b16 = wl0, b8 = wl1;
         asm volatile("" : "+v"(b16), "+v"(b8));
         b16 += lds_addr(slot(qc));
@@ -290,33 +310,18 @@ __global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
         const uint32_t bx16 = b16 + xo, bx8 = b8 + xo;
         static_for<0, kFN>([&](auto f) {
             constexpr int o = decltype(f)::value * kUnit;
-            ra[f] = lds_read16<o>(b16);
-            sa[f] = lds_read8<o>(b8);
+            ra[P][f] = lds_read16<o>(b16);
+            sa[P][f] = lds_read8<o>(b8);
         });
         static_for<0, kFM>([&](auto f) {
             constexpr int o = decltype(f)::value * kUnit;
-            rb[f] = lds_read16<o>(bx16);
-            sb[f] = lds_read8<o>(bx8);
+            rb[P][f] = lds_read16<o>(bx16);
+            sb[P][f] = lds_read8<o>(bx8);
         });
     };
-    auto stage_ready = [&]() {
-        static_assert(kFN == 4 && (kFM == 1 || kFM == 2), "operand lists below");
-        if constexpr (kFM == 2)
-            asm volatile("s_waitcnt lgkmcnt(0)"
-                         : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]), "+v"(rb[1]),
-                           "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]), "+v"(sb[1]));
-        else
-            asm volatile("s_waitcnt lgkmcnt(0)"
-                         : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]),
-                           "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]));
-    };
-    auto take_operands = [&]() {
-#pragma unroll
-        for (int f = 0; f < kFN; ++f)
-            opa[f] = v8i{(int)ra[f][0], (int)ra[f][1], (int)ra[f][2], (int)ra[f][3], (int)sa[f][0], (int)sa[f][1], 0, 0};
-#pragma unroll
-        for (int f = 0; f < kFM; ++f)
-            opb[f] = v8i{(int)rb[f][0], (int)rb[f][1], (int)rb[f][2], (int)rb[f][3], (int)sb[f][0], (int)sb[f][1], 0, 0};
+    auto stage_ready = [&](auto pc) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
+        wait_operands(ra[P], rb[P], sa[P], sb[P]);
     };
     v16f acc[kFN][kFM];
     auto zero_acc = [&]() {
@@ -326,7 +331,17 @@ __global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
             for (int fm = 0; fm < kFM; ++fm) acc[fn][fm] = v16f{};
     };
     // format codes 2, 2: both operands fp6 e2m3; no block scales
-    auto mma = [&]() {
+    auto mma = [&](auto pc) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
+        v8i opa[kFN], opb[kFM];
+#pragma unroll
+        for (int f = 0; f < kFN; ++f)
+            opa[f] = v8i{(int)ra[P][f][0], (int)ra[P][f][1], (int)ra[P][f][2], (int)ra[P][f][3],
+                         (int)sa[P][f][0], (int)sa[P][f][1], 0, 0};
+#pragma unroll
+        for (int f = 0; f < kFM; ++f)
+            opb[f] = v8i{(int)rb[P][f][0], (int)rb[P][f][1], (int)rb[P][f][2], (int)rb[P][f][3],
+                         (int)sb[P][f][0], (int)sb[P][f][1], 0, 0};
 #pragma unroll
         for (int fn = 0; fn < kFN; ++fn)
 #pragma unroll
@@ -468,8 +483,8 @@ __global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
         case 2: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(3 * kVPW + 2 * EPW) : "memory"); break;
         default: asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(3 * kVPW + 3 * EPW) : "memory"); break;
     }
-    read_stage(IC<0>{});
-    stage_ready();
+    read_stage(IC<0>{}, IC<kAlt ? 0 : 1>{});
+    stage_ready(IC<kAlt ? 0 : 1>{});
     zero_acc();
 
     Seg cc{-1, 0, 0};
@@ -478,16 +493,30 @@ __global__ void __launch_bounds__(C::NT, 2) f6_gemm_kernel(F6Args a)
     auto iter = [&](auto qc) __attribute__((always_inline)) -> bool {
         constexpr int q = decltype(qc)::value;
         constexpr IC<(q + 1) % NS> nqc{};
-        take_operands();
+        constexpr IC<kAlt ? (q & 1) : 0> cur{};
+        constexpr IC<kAlt ? ((q + 1) & 1) : 1> nxt{};
+        static_assert(NS % 2 == 0, "stage s uses register set s & 1 across the ring's wrap");
+        if constexpr (!kAlt) {
+#pragma unroll
+            for (int f = 0; f < kFN; ++f) {
+                ra[0][f] = ra[1][f];
+                sa[0][f] = sa[1][f];
+            }
+#pragma unroll
+            for (int f = 0; f < kFM; ++f) {
+                rb[0][f] = rb[1][f];
+                sb[0][f] = sb[1][f];
+            }
+        }
         landed_wait();
         // slot q held stage s, read into registers last iteration: refill it
         // with stage s + 4 (the producer's next)
-        if (s + 1 < total) read_stage(nqc);
+        if (s + 1 < total) read_stage(nqc, nxt);
         produce(qc);
         __builtin_amdgcn_sched_barrier(0);
-        mma();
+        mma(cur);
         __builtin_amdgcn_sched_barrier(0);
-        stage_ready();
+        stage_ready(nxt);
         if (cc.k == nks - 1) {
             epilogue(cc.L, cc.j);
             zero_acc();
