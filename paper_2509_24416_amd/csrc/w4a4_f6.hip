@@ -630,12 +630,15 @@ __global__ void __launch_bounds__(C::NT, C::NWH == 1 ? 1 : 2) f6_gemm_halves_ker
             for (int j = 0; j < kUPW; ++j) dma_lds16(usrc[j] + voff + 1024, dst + (wm * kUPW + j) * kUnit + 1024);
         }
     };
-    v4u ra[kFN], rb[kFM];
-    v2u sa[kFN], sb[kFM];
-    v8i opa[kFN], opb[kFM];
+    // two operand register sets used by alternate stages (the persistent
+    // kernel's scheme; the ragged instances read into set 1 and copy it)
+    constexpr bool kAlt = !RAGGED;
+    v4u ra[2][kFN], rb[2][kFM];
+    v2u sa[2][kFN], sb[2][kFM];
     const uint32_t wl0 = (uint32_t)(lane * 16), wl1 = (uint32_t)f6_tail_offset(lane);
     const uint32_t xo = (uint32_t)((C::WUnits + wm * kFM) * kUnit);
-    auto read_stage = [&](int q) {
+    auto read_stage = [&](int q, auto pc) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
         uint32_t b16 = wl0, b8 = wl1;
         asm volatile("" : "+v"(b16), "+v"(b8));
         const uint32_t base = lds_addr(ring + q * kSlot);
@@ -644,35 +647,35 @@ __global__ void __launch_bounds__(C::NT, C::NWH == 1 ? 1 : 2) f6_gemm_halves_ker
         const uint32_t bx16 = b16 + xo, bx8 = b8 + xo;
         static_for<0, kFN>([&](auto f) {
             constexpr int o = decltype(f)::value * kUnit;
-            ra[f] = lds_read16<o>(b16);
-            sa[f] = lds_read8<o>(b8);
+            ra[P][f] = lds_read16<o>(b16);
+            sa[P][f] = lds_read8<o>(b8);
         });
         static_for<0, kFM>([&](auto f) {
             constexpr int o = decltype(f)::value * kUnit;
-            rb[f] = lds_read16<o>(bx16);
-            sb[f] = lds_read8<o>(bx8);
+            rb[P][f] = lds_read16<o>(bx16);
+            sb[P][f] = lds_read8<o>(bx8);
         });
     };
-    auto stage_ready = [&]() {
-        static_assert(kFN == 4 && kFM == 2, "operand list below");
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(ra[0]), "+v"(ra[1]), "+v"(ra[2]), "+v"(ra[3]), "+v"(rb[0]), "+v"(rb[1]),
-                       "+v"(sa[0]), "+v"(sa[1]), "+v"(sa[2]), "+v"(sa[3]), "+v"(sb[0]), "+v"(sb[1]));
-    };
-    auto take_operands = [&]() {
-#pragma unroll
-        for (int f = 0; f < kFN; ++f)
-            opa[f] = v8i{(int)ra[f][0], (int)ra[f][1], (int)ra[f][2], (int)ra[f][3], (int)sa[f][0], (int)sa[f][1], 0, 0};
-#pragma unroll
-        for (int f = 0; f < kFM; ++f)
-            opb[f] = v8i{(int)rb[f][0], (int)rb[f][1], (int)rb[f][2], (int)rb[f][3], (int)sb[f][0], (int)sb[f][1], 0, 0};
+    auto stage_ready = [&](auto pc) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
+        wait_operands(ra[P], rb[P], sa[P], sb[P]);
     };
     v16f acc[kFN][kFM];
 #pragma unroll
     for (int fn = 0; fn < kFN; ++fn)
 #pragma unroll
         for (int fm = 0; fm < kFM; ++fm) acc[fn][fm] = v16f{};
-    auto mma = [&]() {
+    auto mma = [&](auto pc) __attribute__((always_inline)) {
+        constexpr int P = decltype(pc)::value;
+        v8i opa[kFN], opb[kFM];
+#pragma unroll
+        for (int f = 0; f < kFN; ++f)
+            opa[f] = v8i{(int)ra[P][f][0], (int)ra[P][f][1], (int)ra[P][f][2], (int)ra[P][f][3],
+                         (int)sa[P][f][0], (int)sa[P][f][1], 0, 0};
+#pragma unroll
+        for (int f = 0; f < kFM; ++f)
+            opb[f] = v8i{(int)rb[P][f][0], (int)rb[P][f][1], (int)rb[P][f][2], (int)rb[P][f][3],
+                         (int)sb[P][f][0], (int)sb[P][f][1], 0, 0};
 #pragma unroll
         for (int fn = 0; fn < kFN; ++fn)
 #pragma unroll
@@ -702,23 +705,41 @@ __global__ void __launch_bounds__(C::NT, C::NWH == 1 ? 1 : 2) f6_gemm_halves_ker
     // prologue: stages 0..NS-1 in flight, stage 0 read into registers
     for (int q = 0; q < NS; ++q) produce(q, q);
     wait_vm_barrier<(NS - 1) * kVPW>();
-    read_stage(0);
-    stage_ready();
-    // both halves take h0 steps
-    int q = 0;
-    for (int s = 0; s < h0; ++s) {
+    read_stage(0, IC<kAlt ? 0 : 1>{});
+    stage_ready(IC<kAlt ? 0 : 1>{});
+    // both halves take h0 steps; stage s in register set s & 1
+    int q = 0, s = 0;
+    auto step = [&](auto pc) __attribute__((always_inline)) -> bool {
+        constexpr IC<kAlt ? decltype(pc)::value : 0> cur{};
+        constexpr IC<kAlt ? 1 - decltype(pc)::value : 1> nxt{};
         const int nq = q + 1 == NS ? 0 : q + 1;
         const bool active = s < len;
-        take_operands();
+        if constexpr (!kAlt) {
+#pragma unroll
+            for (int f = 0; f < kFN; ++f) {
+                ra[0][f] = ra[1][f];
+                sa[0][f] = sa[1][f];
+            }
+#pragma unroll
+            for (int f = 0; f < kFM; ++f) {
+                rb[0][f] = rb[1][f];
+                sb[0][f] = sb[1][f];
+            }
+        }
         wait_landed_barrier<(NS - 2) * kVPW>();
-        read_stage(nq);
+        read_stage(nq, nxt);
         produce(q, s + NS);
         __builtin_amdgcn_sched_barrier(0);
-        if (active) mma();
+        if (active) mma(cur);
         __builtin_amdgcn_sched_barrier(0);
-        stage_ready();
+        stage_ready(nxt);
         q = nq;
-    }
+        ++s;
+        return s < h0;
+    };
+    if (h0 > 0)
+        while (step(IC<0>{}) && step(IC<1>{})) {
+        }
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 
     // the epilogue operands into LDS (a thread past the end writes the last
